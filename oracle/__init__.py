@@ -1,0 +1,22 @@
+"""CPU oracle for the per-operator decoder-layer forward (fp64, NumPy).
+
+TEST INFRASTRUCTURE ONLY.  Only the test suite, the smoke check and the CPU
+baseline leg of the benchmark may import this package.  The HIP library and its
+Python binding never import it and share no code with it.
+
+Every function is the plain textbook definition of the operator the paper names
+(Section 2.1's operator characterization: RMS Norm, QKV Linear and the MLP
+linears, the fused SiLU-and-multiply activation, FlashAttention-style prefill
+attention, decode attention over a paged KV cache), evaluated in fp64 with no
+tiling, no online softmax and no split of the key range.  See `ops` for the
+per-function citations and `cost` for the algorithmic flop/byte closed forms.
+
+Parity status: every function here is pinned by brute force, closed forms or
+invariants in the CPU tests (tests/test_oracle_pins.py); none is "parity
+unpinned".
+"""
+from .ops import (  # noqa: F401
+    rmsnorm, linear, silu, swiglu, softmax, attn_prefill, attn_prefill_rows,
+    attn_decode, attn_decode_rows, gather_paged, decoder_layer_prefill,
+)
+from . import cost  # noqa: F401

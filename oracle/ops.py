@@ -1,0 +1,214 @@
+"""fp64 definitions of the decoder-layer operators (test infrastructure only).
+
+The paper (Section 2.1, "Cross-Dimension Analysis" and the sensitivity study;
+Appendix C, "Dataflow Characteristics") treats a decoder layer as a dataflow of
+separately profiled operators: RMS Norm, QKV Linear, attention, the MLP linears
+and the fused SiLU-multiply activation.  It does not print their formulas, so
+each function below is the standard definition of the named operator, written
+out in fp64.  The readings taken where the paper is silent are listed in the
+module-level READINGS dict and repeated in the design notes.
+
+All arrays are converted to float64 on entry.  Outputs are float64 and are never
+rounded to a narrower type.
+"""
+from __future__ import annotations
+
+import numpy as np
+
+READINGS = {
+    "rmsnorm": "y = x / sqrt(mean(x^2) + eps) * w; eps inside the root; gain w multiplies "
+               "(not 1+w).",
+    "linear": "y = x W^T (+ b), W stored [N, K] row-major.",
+    "swiglu": "input [M, 2F]: first F columns are the gate, last F the up projection; "
+              "out = silu(gate) * up, silu(z) = z / (1 + exp(-z)).",
+    "gqa": "query head h reads KV head h // (Hq / Hkv) (contiguous groups).",
+    "causal": "within one prompt, key j is visible to query i iff j <= i; prompts do not "
+              "see each other.",
+    "scale": "scores are scale * q.k with scale passed in (1/sqrt(D) in the workloads).",
+    "decode": "one query per sequence attends to all context_lens[b] cached keys; the new "
+              "token's K/V is already in the cache; context_len 0 gives a zero output.",
+    "paged": "cached key j of sequence b lives in physical block block_table[b, j // bs] "
+             "at slot j % bs; cache layout [num_blocks, bs, Hkv, D].",
+}
+
+
+def _f64(a) -> np.ndarray:
+    return np.asarray(a, dtype=np.float64)
+
+
+# ---------------------------------------------------------------- RMS Norm ---
+def rmsnorm(x, w, eps: float) -> np.ndarray:
+    """RMS Norm (Section 2.1: the memory-heavy, compute-light operator).
+
+    y[m, j] = x[m, j] / sqrt((1/H) * sum_j x[m, j]^2 + eps) * w[j]
+    """
+    x = _f64(x)
+    w = _f64(w)
+    ms = np.mean(x * x, axis=-1, keepdims=True)
+    return x / np.sqrt(ms + eps) * w
+
+
+# ------------------------------------------------------------------ Linear ---
+def linear(x, W, b=None) -> np.ndarray:
+    """Linear projection (Section 2.1: QKV Linear, wide projections, MLP).
+
+    y[m, n] = sum_k x[m, k] * W[n, k] (+ b[n]), with W stored [N, K].
+    """
+    y = np.matmul(_f64(x), _f64(W).T)
+    if b is not None:
+        y = y + _f64(b)
+    return y
+
+
+# ---------------------------------------------------------- SiLU-and-mul ---
+def silu(z) -> np.ndarray:
+    """silu(z) = z * sigmoid(z) = z / (1 + exp(-z))."""
+    z = _f64(z)
+    with np.errstate(over="ignore"):
+        return z / (1.0 + np.exp(-z))
+
+
+def swiglu(u) -> np.ndarray:
+    """Fused act_and_mul / "SiLu Mul" (Section 2.1 memory study; Appendix C).
+
+    u is the merged gate-up projection output [M, 2F]; out = silu(u[:, :F]) * u[:, F:].
+    """
+    u = _f64(u)
+    F = u.shape[-1] // 2
+    return silu(u[..., :F]) * u[..., F:]
+
+
+# ----------------------------------------------------------------- softmax ---
+def softmax(s, axis: int = -1) -> np.ndarray:
+    """Row softmax exp(s - max s) / sum exp(s - max s) in fp64."""
+    s = _f64(s)
+    m = np.max(s, axis=axis, keepdims=True)
+    e = np.exp(s - m)
+    return e / np.sum(e, axis=axis, keepdims=True)
+
+
+# -------------------------------------------------------- prefill attention --
+def _kv_head(h: int, n_q_heads: int, n_kv_heads: int) -> int:
+    return h // (n_q_heads // n_kv_heads)
+
+
+def attn_prefill(q, k, v, cu_seqlens, scale: float, causal: bool = True) -> np.ndarray:
+    """Self-attention over a ragged batch of prompts (Section 2.1: quadratic in
+    sequence length; FlashAttention gives the same result without storing the
+    score matrix; grouped-query attention as in the Table 3 models).
+
+    q: [T, Hq, D]; k, v: [T, Hkv, D]; cu_seqlens: [B+1] prompt offsets.
+    For prompt b, query i and head h (KV head g = h // (Hq/Hkv)):
+        s_j = scale * q[c_b+i, h] . k[c_b+j, g]   for visible j
+        o[c_b+i, h] = sum_j softmax(s)_j * v[c_b+j, g]
+    The full score matrix of each (prompt, head) is materialized.
+    """
+    q, k, v = _f64(q), _f64(k), _f64(v)
+    T, Hq, D = q.shape
+    Hkv = k.shape[1]
+    out = np.zeros((T, Hq, D), np.float64)
+    cu = np.asarray(cu_seqlens, np.int64)
+    for b in range(len(cu) - 1):
+        s0, s1 = int(cu[b]), int(cu[b + 1])
+        L = s1 - s0
+        if L == 0:
+            continue
+        visible = np.tril(np.ones((L, L), bool)) if causal else np.ones((L, L), bool)
+        for h in range(Hq):
+            g = _kv_head(h, Hq, Hkv)
+            s = scale * (q[s0:s1, h, :] @ k[s0:s1, g, :].T)
+            s = np.where(visible, s, -np.inf)
+            p = softmax(s, axis=-1)
+            out[s0:s1, h, :] = p @ v[s0:s1, g, :]
+    return out
+
+
+def attn_prefill_rows(q, k, v, cu_seqlens, rows, scale: float, causal: bool = True):
+    """The same definition evaluated only at the (token, head) pairs in `rows`.
+
+    Returns an array [len(rows), D].  Used for sampled parity at full size.
+    """
+    q, k, v = np.asarray(q), np.asarray(k), np.asarray(v)
+    Hq = q.shape[1]
+    Hkv = k.shape[1]
+    cu = np.asarray(cu_seqlens, np.int64)
+    out = np.zeros((len(rows), q.shape[2]), np.float64)
+    for r, (t, h) in enumerate(rows):
+        b = int(np.searchsorted(cu, t, side="right") - 1)
+        s0, s1 = int(cu[b]), int(cu[b + 1])
+        last = t if causal else s1 - 1
+        g = _kv_head(int(h), Hq, Hkv)
+        kk = _f64(k[s0:last + 1, g, :])
+        vv = _f64(v[s0:last + 1, g, :])
+        s = scale * (kk @ _f64(q[t, h, :]))
+        p = softmax(s)
+        out[r] = p @ vv
+    return out
+
+
+# --------------------------------------------------------- decode attention --
+def gather_paged(cache, block_table_row, n: int) -> np.ndarray:
+    """Keys (or values) 0..n-1 of one sequence from a paged cache
+    [num_blocks, bs, Hkv, D]: row j = cache[block_table_row[j // bs], j % bs]."""
+    bs = cache.shape[1]
+    j = np.arange(n)
+    return np.asarray(cache)[np.asarray(block_table_row)[j // bs], j % bs]
+
+
+def attn_decode(q, k_cache, v_cache, block_table, context_lens, scale: float) -> np.ndarray:
+    """One-token decode attention over a paged KV cache (Section 2.1 decode
+    phase; Appendix E: decode is memory-bound; PagedAttention in the serving
+    engine of Section 5).
+
+    q: [B, Hq, D]; k_cache, v_cache: [num_blocks, bs, Hkv, D];
+    block_table: [B, max_blocks]; context_lens: [B].
+    o[b, h] = sum_{j < n_b} softmax_j(scale * q[b, h] . K_b[j, g]) V_b[j, g].
+    """
+    q = _f64(q)
+    B, Hq, D = q.shape
+    Hkv = k_cache.shape[2]
+    out = np.zeros((B, Hq, D), np.float64)
+    for b in range(B):
+        n = int(context_lens[b])
+        if n == 0:
+            continue
+        K = _f64(gather_paged(k_cache, block_table[b], n))  # [n, Hkv, D]
+        V = _f64(gather_paged(v_cache, block_table[b], n))
+        for h in range(Hq):
+            g = _kv_head(h, Hq, Hkv)
+            p = softmax(scale * (K[:, g, :] @ q[b, h, :]))
+            out[b, h] = p @ V[:, g, :]
+    return out
+
+
+def attn_decode_rows(q, k_cache, v_cache, block_table, context_lens, seqs, scale: float):
+    """attn_decode for a subset of sequences; returns [len(seqs), Hq, D]."""
+    seqs = list(seqs)
+    return attn_decode(np.asarray(q)[seqs], k_cache, v_cache,
+                       np.asarray(block_table)[seqs], np.asarray(context_lens)[seqs], scale)
+
+
+# ----------------------------------------------------- whole decoder layer ---
+def decoder_layer_prefill(x, p, cu_seqlens, n_q_heads, n_kv_heads, head_dim, eps):
+    """The layer dataflow the operators form (Section 2.2: a model is a data
+    flow graph of operators): norm -> QKV -> attention -> O, norm -> gate-up ->
+    SiLU-mul -> down.  Residual adds and rotary embeddings are not among the
+    profiled operators here and are omitted, so this is the operator chain only.
+
+    p: dict with w_norm1, w_qkv, w_o, w_norm2, w_gate_up, w_down.
+    Returns dict of every intermediate (fp64).
+    """
+    T = x.shape[0]
+    D = head_dim
+    h1 = rmsnorm(x, p["w_norm1"], eps)
+    qkv = linear(h1, p["w_qkv"])
+    q = qkv[:, : n_q_heads * D].reshape(T, n_q_heads, D)
+    k = qkv[:, n_q_heads * D:(n_q_heads + n_kv_heads) * D].reshape(T, n_kv_heads, D)
+    v = qkv[:, (n_q_heads + n_kv_heads) * D:].reshape(T, n_kv_heads, D)
+    a = attn_prefill(q, k, v, cu_seqlens, 1.0 / np.sqrt(D), causal=True)
+    o = linear(a.reshape(T, n_q_heads * D), p["w_o"])
+    h2 = rmsnorm(o, p["w_norm2"], eps)
+    gu = linear(h2, p["w_gate_up"])
+    act = swiglu(gu)
+    y = linear(act, p["w_down"])
+    return {"h1": h1, "qkv": qkv, "attn": a, "o": o, "h2": h2, "gate_up": gu, "act": act, "y": y}

@@ -1,0 +1,370 @@
+"""Pins for the CPU oracle: it is checked against things other than itself.
+
+Each `check_*` function takes an implementation and raises AssertionError when
+it disagrees with a brute-force loop, a hand-worked example under tests/golden,
+a closed form, or an invariant of the operator's definition.  The plain tests
+run every check on the oracle; the mutation tests plant plausible mistakes in
+copies of the oracle (on the CPU) and require at least one check to catch each.
+"""
+import math
+import os
+import types
+
+import numpy as np
+import pytest
+
+import oracle
+from oracle import cost as ocost
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+def _rows(name):
+    out = []
+    with open(os.path.join(GOLDEN, name)) as f:
+        for line in f:
+            line = line.strip()
+            if not line or line.startswith("#"):
+                continue
+            out.append([np.array([float(t) for t in part.split()]) for part in line.split("|")])
+    return out
+
+
+# --------------------------------------------------------------- brute force --
+def bf_linear(x, W, b=None):
+    M, K = len(x), len(x[0])
+    N = len(W)
+    y = [[0.0] * N for _ in range(M)]
+    for m in range(M):
+        for n in range(N):
+            acc = 0.0
+            for k in range(K):
+                acc += float(x[m][k]) * float(W[n][k])
+            y[m][n] = acc + (float(b[n]) if b is not None else 0.0)
+    return np.array(y)
+
+
+def bf_rmsnorm(x, w, eps):
+    out = []
+    for row in x:
+        ss = 0.0
+        for v in row:
+            ss += float(v) * float(v)
+        r = math.sqrt(ss / len(row) + eps)
+        out.append([float(v) / r * float(wj) for v, wj in zip(row, w)])
+    return np.array(out)
+
+
+def bf_attention_one(qv, keys, vals, scale):
+    """softmax-weighted sum for one query, in plain Python floats."""
+    s = [scale * sum(float(a) * float(b) for a, b in zip(qv, kk)) for kk in keys]
+    m = max(s)
+    e = [math.exp(t - m) for t in s]
+    z = sum(e)
+    D = len(vals[0])
+    return [sum(e[j] / z * float(vals[j][d]) for j in range(len(keys))) for d in range(D)]
+
+
+def bf_attn_prefill(q, k, v, cu, scale, causal):
+    T, Hq, D = q.shape
+    Hkv = k.shape[1]
+    out = np.zeros((T, Hq, D))
+    for b in range(len(cu) - 1):
+        s0, s1 = cu[b], cu[b + 1]
+        for i in range(s1 - s0):
+            for h in range(Hq):
+                g = h // (Hq // Hkv)
+                last = i if causal else (s1 - s0 - 1)
+                keys = [k[s0 + j, g] for j in range(last + 1)]
+                vals = [v[s0 + j, g] for j in range(last + 1)]
+                out[s0 + i, h] = bf_attention_one(q[s0 + i, h], keys, vals, scale)
+    return out
+
+
+# -------------------------------------------------------------------- checks --
+def check_linear(impl):
+    rng = np.random.default_rng(1)
+    for (M, N, K) in [(1, 1, 1), (3, 5, 7), (8, 4, 6), (2, 8, 8)]:
+        x = rng.standard_normal((M, K))
+        W = rng.standard_normal((N, K))
+        b = rng.standard_normal(N)
+        np.testing.assert_allclose(impl.linear(x, W), bf_linear(x, W), rtol=1e-12, atol=1e-12)
+        np.testing.assert_allclose(impl.linear(x, W, b), bf_linear(x, W, b), rtol=1e-12, atol=1e-12)
+    for (M, K, N), x, W, y in [(tuple(int(t) for t in r[0]), r[1], r[2], r[3]) for r in _rows("linear_hand.txt")]:
+        np.testing.assert_array_equal(impl.linear(x.reshape(M, K), W.reshape(N, K)), y.reshape(M, N))
+    x = rng.standard_normal((5, 6))
+    np.testing.assert_array_equal(impl.linear(x, np.eye(6)), x)
+
+
+def check_rmsnorm(impl):
+    rng = np.random.default_rng(2)
+    for eps, x, w, y in _rows("rmsnorm_hand.txt"):
+        np.testing.assert_allclose(impl.rmsnorm(x[None], w, float(eps[0]))[0], y, rtol=1e-15, atol=0)
+    x = rng.standard_normal((6, 16))
+    w = 1.0 + 0.02 * rng.standard_normal(16)
+    np.testing.assert_allclose(impl.rmsnorm(x, w, 1e-5), bf_rmsnorm(x, w, 1e-5), rtol=1e-13)
+    # unit RMS with unit gain: exactly 1 at eps = 0, 1/sqrt(1 + eps/mean(x^2)) otherwise
+    y = impl.rmsnorm(x, np.ones(16), 0.0)
+    np.testing.assert_allclose(np.sqrt(np.mean(y * y, axis=-1)), 1.0, rtol=1e-14)
+    eps = 0.3
+    y = impl.rmsnorm(x, np.ones(16), eps)
+    ms = np.mean(x * x, axis=-1)
+    np.testing.assert_allclose(np.sqrt(np.mean(y * y, axis=-1)), 1 / np.sqrt(1 + eps / ms), rtol=1e-13)
+    # constant row c: y = c / sqrt(c^2 + eps) * w
+    c = -1.7
+    np.testing.assert_allclose(impl.rmsnorm(np.full((1, 8), c), np.arange(1, 9.0), 0.5)[0],
+                               c / math.sqrt(c * c + 0.5) * np.arange(1, 9.0), rtol=1e-14)
+
+
+def check_swiglu(impl):
+    (u, out), = _rows("swiglu_hand.txt")
+    np.testing.assert_allclose(impl.swiglu(u[None])[0], out, rtol=1e-15, atol=1e-300)
+    assert impl.silu(np.array([0.0]))[0] == 0.0
+    np.testing.assert_allclose(impl.silu(np.array([1.0, -1.0])),
+                               [1 / (1 + math.exp(-1)), -math.exp(-1) / (1 + math.exp(-1))], rtol=1e-15)
+    rng = np.random.default_rng(3)
+    g = rng.standard_normal((4, 9)) * 4
+    np.testing.assert_allclose(impl.swiglu(np.concatenate([g, np.ones_like(g)], 1)), impl.silu(g), rtol=1e-15)
+    np.testing.assert_allclose(impl.silu(g), [[v / (1 + math.exp(-v)) for v in row] for row in g], rtol=1e-14)
+    # large negative gate: silu -> -0, no NaN
+    assert np.isfinite(impl.silu(np.array([-1000.0, 1000.0]))).all()
+
+
+def check_softmax(impl):
+    rng = np.random.default_rng(4)
+    s = rng.standard_normal((7, 13)) * 10
+    p = impl.softmax(s)
+    np.testing.assert_allclose(p.sum(-1), 1.0, rtol=0, atol=1e-12)
+    np.testing.assert_allclose(impl.softmax(s + 123.0), p, rtol=1e-12)
+    for row, prow in zip(s, p):
+        e = [math.exp(t - max(row)) for t in row]
+        np.testing.assert_allclose(prow, [t / sum(e) for t in e], rtol=1e-13)
+
+
+def check_attn_prefill(impl):
+    # hand-worked two-key example, causal and not
+    for causal, q, k, v, o in _rows("attn_two_keys.txt"):
+        sh = (2, 1, 2)
+        got = impl.attn_prefill(q.reshape(sh), k.reshape(sh), v.reshape(sh), [0, 2], 1.0, bool(causal[0]))
+        np.testing.assert_allclose(got.reshape(-1), o, rtol=1e-14, atol=1e-14)
+    rng = np.random.default_rng(5)
+    # brute force on tiny ragged GQA batches, causal and not
+    lens = [3, 1, 5, 0, 2]
+    cu = np.concatenate([[0], np.cumsum(lens)])
+    T = int(cu[-1])
+    for Hq, Hkv in [(4, 2), (2, 2), (3, 1)]:
+        q = rng.standard_normal((T, Hq, 4))
+        k = rng.standard_normal((T, Hkv, 4))
+        v = rng.standard_normal((T, Hkv, 4))
+        for causal in (True, False):
+            np.testing.assert_allclose(impl.attn_prefill(q, k, v, cu, 0.7, causal),
+                                       bf_attn_prefill(q, k, v, cu, 0.7, causal), rtol=1e-12, atol=1e-12)
+    # single-key attention returns V exactly
+    q = rng.standard_normal((1, 2, 8))
+    k = rng.standard_normal((1, 1, 8))
+    v = rng.standard_normal((1, 1, 8))
+    out = impl.attn_prefill(q, k, v, [0, 1], 0.3, True)
+    assert np.array_equal(out[0, 0], v[0, 0]) and np.array_equal(out[0, 1], v[0, 0])
+    # all keys equal: causal output is the running mean of v
+    L = 6
+    q = rng.standard_normal((L, 1, 4))
+    k = np.tile(rng.standard_normal((1, 1, 4)), (L, 1, 1))
+    v = rng.standard_normal((L, 1, 4))
+    out = impl.attn_prefill(q, k, v, [0, L], 0.5, True)
+    np.testing.assert_allclose(out[:, 0], np.cumsum(v[:, 0], 0) / np.arange(1, L + 1)[:, None], rtol=1e-13)
+    # causal: perturbing k, v at positions > i leaves rows <= i unchanged
+    L = 9
+    q = rng.standard_normal((L, 2, 8))
+    k = rng.standard_normal((L, 1, 8))
+    v = rng.standard_normal((L, 1, 8))
+    base = impl.attn_prefill(q, k, v, [0, L], 0.4, True)
+    k2, v2 = k.copy(), v.copy()
+    k2[5:] += 3.0
+    v2[5:] -= 2.0
+    pert = impl.attn_prefill(q, k2, v2, [0, L], 0.4, True)
+    assert np.array_equal(base[:5], pert[:5])
+    assert not np.allclose(base[5:], pert[5:])
+    # GQA == MHA with each KV head repeated over its group
+    Hq, Hkv = 6, 2
+    q = rng.standard_normal((L, Hq, 8))
+    k = rng.standard_normal((L, Hkv, 8))
+    v = rng.standard_normal((L, Hkv, 8))
+    gqa = impl.attn_prefill(q, k, v, [0, L], 0.35, True)
+    mha = impl.attn_prefill(q, np.repeat(k, Hq // Hkv, axis=1), np.repeat(v, Hq // Hkv, axis=1), [0, L], 0.35, True)
+    np.testing.assert_allclose(gqa, mha, rtol=1e-14)
+    # batch composition: a ragged batch equals independent per-prompt calls
+    lens = [4, 7, 1]
+    cu = np.concatenate([[0], np.cumsum(lens)])
+    T = int(cu[-1])
+    q = rng.standard_normal((T, 4, 8))
+    k = rng.standard_normal((T, 2, 8))
+    v = rng.standard_normal((T, 2, 8))
+    full = impl.attn_prefill(q, k, v, cu, 0.35, True)
+    for b in range(3):
+        s0, s1 = cu[b], cu[b + 1]
+        one = impl.attn_prefill(q[s0:s1], k[s0:s1], v[s0:s1], [0, s1 - s0], 0.35, True)
+        np.testing.assert_allclose(full[s0:s1], one, rtol=1e-14)
+    # row-sampled evaluation agrees with the full evaluation
+    rows = [(0, 0), (3, 1), (4, 3), (10, 2), (11, 0)]
+    np.testing.assert_allclose(impl.attn_prefill_rows(q, k, v, cu, rows, 0.35, True),
+                               np.stack([full[t, h] for t, h in rows]), rtol=1e-13)
+    fulln = impl.attn_prefill(q, k, v, cu, 0.35, False)
+    np.testing.assert_allclose(impl.attn_prefill_rows(q, k, v, cu, rows, 0.35, False),
+                               np.stack([fulln[t, h] for t, h in rows]), rtol=1e-13)
+
+
+def check_attn_decode(impl):
+    (bt, kc, vc, q, o), = _rows("decode_paged_hand.txt")
+    got = impl.attn_decode(q.reshape(1, 1, 2), kc.reshape(3, 2, 1, 2), vc.reshape(3, 2, 1, 2),
+                           bt.astype(np.int64).reshape(1, 2), np.array([3]), 1.0)
+    np.testing.assert_allclose(got.reshape(-1), o, rtol=1e-14)
+    rng = np.random.default_rng(6)
+    bs, Hkv, Hq, D = 4, 2, 4, 8
+    ctx = np.array([1, 5, 8, 0, 13])
+    nblk = (ctx + bs - 1) // bs
+    nb = int(nblk.sum()) + 3
+    perm = rng.permutation(nb)
+    table = np.zeros((len(ctx), int(nblk.max())), np.int64)
+    pos = 0
+    for b, n in enumerate(nblk):
+        table[b, :n] = perm[pos:pos + n]
+        pos += n
+    kc = rng.standard_normal((nb, bs, Hkv, D))
+    vc = rng.standard_normal((nb, bs, Hkv, D))
+    q = rng.standard_normal((len(ctx), Hq, D))
+    out = impl.attn_decode(q, kc, vc, table, ctx, 0.3)
+    # brute force gather through the block table, element by element
+    for b, n in enumerate(ctx):
+        for h in range(Hq):
+            g = h // (Hq // Hkv)
+            if n == 0:
+                assert np.all(out[b, h] == 0)
+                continue
+            keys = [kc[table[b, j // bs], j % bs, g] for j in range(n)]
+            vals = [vc[table[b, j // bs], j % bs, g] for j in range(n)]
+            np.testing.assert_allclose(out[b, h], bf_attention_one(q[b, h], keys, vals, 0.3), rtol=1e-12, atol=1e-13)
+    # single cached key returns V exactly
+    assert np.array_equal(out[0, 0], vc[table[0, 0], 0, 0])
+    # relabelling physical blocks (and moving the data with them) changes nothing
+    relabel = rng.permutation(nb)
+    kc2 = np.empty_like(kc)
+    vc2 = np.empty_like(vc)
+    kc2[relabel] = kc
+    vc2[relabel] = vc
+    out2 = impl.attn_decode(q, kc2, vc2, relabel[table], ctx, 0.3)
+    np.testing.assert_allclose(out2, out, rtol=1e-14)
+    # decode over the first n tokens == last row of causal prefill over those n tokens
+    n = 11
+    kseq = rng.standard_normal((n, Hkv, D))
+    vseq = rng.standard_normal((n, Hkv, D))
+    qseq = rng.standard_normal((n, Hq, D))
+    pre = impl.attn_prefill(qseq, kseq, vseq, [0, n], 0.25, True)
+    nb = (n + bs - 1) // bs
+    kc = np.zeros((nb, bs, Hkv, D))
+    vc = np.zeros((nb, bs, Hkv, D))
+    for j in range(n):
+        kc[j // bs, j % bs] = kseq[j]
+        vc[j // bs, j % bs] = vseq[j]
+    dec = impl.attn_decode(qseq[n - 1:n], kc, vc, np.arange(nb)[None], np.array([n]), 0.25)
+    np.testing.assert_allclose(dec[0], pre[n - 1], rtol=1e-13)
+
+
+def check_cost(c):
+    # causal visible pairs counted by a loop
+    lens = [1, 2, 5, 0, 9]
+    pairs = sum(1 for L in lens for i in range(L) for j in range(L) if j <= i)
+    f, b = c.attn_prefill(lens, 4, 2, 8, 2, True)
+    assert f == 4 * 8 * 4 * pairs
+    T = sum(lens)
+    assert b == 2 * (2 * T * 4 * 8 + 2 * T * 2 * 8)
+    f, _ = c.attn_prefill(lens, 4, 2, 8, 2, False)
+    assert f == 4 * 8 * 4 * sum(L * L for L in lens)
+    assert c.linear(3, 5, 7, 2) == (2 * 3 * 5 * 7, 2 * (21 + 35 + 15))
+    assert c.linear(3, 5, 7, 4, bias=True)[1] == 4 * (21 + 35 + 15 + 5)
+    assert c.rmsnorm(4, 8, 2)[1] == 2 * (2 * 32 + 8)
+    assert c.swiglu(4, 8, 2)[1] == 2 * 3 * 32
+    ctx = [1, 16, 17, 0]
+    f, b = c.attn_decode(ctx, 8, 2, 4, 2, 16)
+    assert f == 4 * 4 * 8 * 34
+    assert b == 2 * (2 * 2 * 4 * 34 + 2 * 4 * 8 * 4) + 4 * ((1 + 1 + 2 + 0) + 4)
+
+
+CHECKS = [check_linear, check_rmsnorm, check_swiglu, check_softmax, check_attn_prefill, check_attn_decode]
+
+
+@pytest.mark.parametrize("check", CHECKS, ids=lambda f: f.__name__)
+def test_oracle_pinned(check):
+    check(oracle)
+
+
+def test_cost_closed_forms():
+    check_cost(ocost)
+
+
+# ------------------------------------------------------------ planted errors --
+def _mutant(**overrides):
+    m = types.SimpleNamespace(**{n: getattr(oracle, n) for n in dir(oracle) if not n.startswith("_")})
+    for k, v in overrides.items():
+        setattr(m, k, v)
+    return m
+
+
+def _mut_attn(kv_map=None, causal_strict=False, drop_scale=False, no_max=False):
+    """A copy of the prefill definition with one planted mistake."""
+    def f(q, k, v, cu, scale, causal=True):
+        q, k, v = np.asarray(q, float), np.asarray(k, float), np.asarray(v, float)
+        T, Hq, D = q.shape
+        Hkv = k.shape[1]
+        out = np.zeros((T, Hq, D))
+        for b in range(len(cu) - 1):
+            s0, s1 = int(cu[b]), int(cu[b + 1])
+            L = s1 - s0
+            if L == 0:
+                continue
+            vis = np.tril(np.ones((L, L), bool), -1 if causal_strict else 0) if causal else np.ones((L, L), bool)
+            vis[0, 0] = True
+            for h in range(Hq):
+                g = kv_map(h, Hq, Hkv) if kv_map else h // (Hq // Hkv)
+                s = (1.0 if drop_scale else scale) * (q[s0:s1, h] @ k[s0:s1, g].T)
+                s = np.where(vis, s, -np.inf)
+                e = np.exp(s - (0 if no_max else s.max(-1, keepdims=True)))
+                out[s0:s1, h] = (e / e.sum(-1, keepdims=True)) @ v[s0:s1, g]
+        return out
+    return f
+
+
+MUTANTS = {
+    "linear_k_reversed": (check_linear, dict(linear=lambda x, W, b=None: np.asarray(x, float) @ np.asarray(W, float)[:, ::-1].T + (0 if b is None else b))),
+    "linear_bias_dropped": (check_linear, dict(linear=lambda x, W, b=None: np.asarray(x, float) @ np.asarray(W, float).T)),
+    "rmsnorm_eps_outside": (check_rmsnorm, dict(rmsnorm=lambda x, w, eps: np.asarray(x) / (np.sqrt(np.mean(np.asarray(x) ** 2, -1, keepdims=True)) + eps) * w)),
+    "rmsnorm_sum_not_mean": (check_rmsnorm, dict(rmsnorm=lambda x, w, eps: np.asarray(x) / np.sqrt(np.sum(np.asarray(x) ** 2, -1, keepdims=True) + eps) * w)),
+    "rmsnorm_one_plus_w": (check_rmsnorm, dict(rmsnorm=lambda x, w, eps: oracle.rmsnorm(x, 1 + np.asarray(w, float), eps))),
+    "swiglu_halves_swapped": (check_swiglu, dict(swiglu=lambda u: oracle.silu(np.asarray(u)[:, np.asarray(u).shape[1] // 2:]) * np.asarray(u)[:, : np.asarray(u).shape[1] // 2])),
+    "silu_sign": (check_swiglu, dict(silu=lambda z: np.asarray(z, float) / (1 + np.exp(np.asarray(z, float))),
+                                     swiglu=lambda u: (lambda z: z / (1 + np.exp(z)))(np.asarray(u, float)[:, : np.asarray(u).shape[1] // 2]) * np.asarray(u, float)[:, np.asarray(u).shape[1] // 2:])),
+    "softmax_no_normalize": (check_softmax, dict(softmax=lambda s, axis=-1: np.exp(np.asarray(s) - np.max(s, axis=axis, keepdims=True)))),
+    "attn_gqa_modulo": (check_attn_prefill, dict(attn_prefill=_mut_attn(kv_map=lambda h, Hq, Hkv: h % Hkv))),
+    "attn_causal_strict": (check_attn_prefill, dict(attn_prefill=_mut_attn(causal_strict=True))),
+    "attn_scale_dropped": (check_attn_prefill, dict(attn_prefill=_mut_attn(drop_scale=True))),
+    "decode_slot_index": (check_attn_decode, dict(attn_decode=lambda q, kc, vc, bt, n, scale: oracle.attn_decode(q, kc[:, ::-1], vc[:, ::-1], bt, n, scale))),
+    "decode_gqa_modulo": (check_attn_decode, dict(attn_decode=lambda q, kc, vc, bt, n, scale: oracle.attn_decode(q, np.asarray(kc)[:, :, ::-1], np.asarray(vc)[:, :, ::-1], bt, n, scale))),
+}
+
+
+@pytest.mark.parametrize("name", sorted(MUTANTS))
+def test_planted_mistake_is_caught(name):
+    check, over = MUTANTS[name]
+    with pytest.raises(AssertionError):
+        check(_mutant(**over))
+
+
+@pytest.mark.parametrize("name,mut", [
+    ("causal_pairs_strict", dict(attn_prefill=lambda L, Hq, Hkv, D, s, causal=True: (4 * D * Hq * int(sum(l * (l - 1) // 2 for l in L)), 0))),
+    ("decode_blocks_floor", dict(attn_decode=lambda n, Hq, Hkv, D, s, bs: (4 * D * Hq * sum(n), s * (2 * Hkv * D * sum(n) + 2 * len(n) * Hq * D) + 4 * (sum(x // bs for x in n) + len(n))))),
+])
+def test_planted_cost_mistake_is_caught(name, mut):
+    c = types.SimpleNamespace(**{k: getattr(ocost, k) for k in ("linear", "rmsnorm", "swiglu", "attn_prefill", "attn_decode")})
+    for k, v in mut.items():
+        setattr(c, k, v)
+    with pytest.raises(AssertionError):
+        check_cost(c)
