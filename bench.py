@@ -1,0 +1,315 @@
+"""Benchmark of the per-operator decoder-layer forward on one MI355X.
+
+One step = one pass of every operator of the hot path over one batch:
+  prefill layer of a Llama-3-8B-shaped model on a ragged batch of 16 prompts
+  (8871 tokens): RMSNorm -> QKV linear -> causal GQA prefill attention -> O
+  linear -> RMSNorm -> gate-up linear -> SwiGLU -> down linear,
+  then decode attention for 256 sequences over a paged KV cache (contexts
+  uniform in [128, 8192], 4.5 GB of K/V).
+Every operator is timed on its own with device events on the stream it runs
+on.  `value` = prefill tokens per second of the whole step (the decode
+attention is inside the step time, so this is conservative).
+
+Prints one JSON line.  --gpus above 1 is refused (this build runs on one GPU).
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_BF16 = 2.5e15     # dense bf16 MFMA, FLOP/s
+PEAK_HBM = 8.0e12      # HBM3E, B/s
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_counters.json")
+KERNEL_SOURCES = {"gemm_bf16_kernel": "paper_2608_13499_amd/csrc/k_gemm.hip",
+                  "attn_prefill_bf16_kernel": "paper_2608_13499_amd/csrc/k_attn_prefill.hip",
+                  "attn_decode_split_kernel": "paper_2608_13499_amd/csrc/k_attn_decode.hip",
+                  "rmsnorm_kernel": "paper_2608_13499_amd/csrc/k_norm_act.hip",
+                  "swiglu_kernel": "paper_2608_13499_amd/csrc/k_norm_act.hip"}
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def source_sha(kernel: str) -> str:
+    with open(os.path.join(ROOT, KERNEL_SOURCES[kernel]), "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()[:16]
+
+
+def measured_traffic(kernel: str, launches_per_unit=1):
+    """HBM bytes per launch from the committed counter summary, or None when
+    the kernel source changed since the counters were taken."""
+    try:
+        with open(TRAFFIC_FILE) as f:
+            t = json.load(f)
+    except (OSError, ValueError):
+        return None
+    e = t.get(kernel)
+    if not e or e.get("source_sha") != source_sha(kernel):
+        return None
+    return e.get("bytes_per_launch")
+
+
+class Layer:
+    """Preallocated operands of one step (inputs resident in HBM)."""
+
+    def __init__(self, ops, wl, torch):
+        self.ops, self.torch = ops, torch
+        self.pc = wl.C2
+        self.dc = wl.C3
+        pc, dc = self.pc, self.dc
+        self.p = wl.prefill_layer_inputs(pc)
+        self.d = wl.decode_inputs(dc)
+        M, H, F = self.p["M"], pc.hidden, pc.ffn
+        Hq, Hkv, D = pc.n_q_heads, pc.n_kv_heads, pc.head_dim
+        bf = torch.bfloat16
+        e = lambda *s: torch.empty(*s, dtype=bf, device="cuda")
+        self.h1, self.qkv, self.attn = e(M, H), e(M, pc.qkv_out), e(M, Hq, D)
+        self.o, self.h2, self.gu, self.act, self.y = e(M, H), e(M, H), e(M, 2 * F), e(M, F), e(M, H)
+        self.q = self.qkv[:, : Hq * D].view(M, Hq, D)
+        self.k = self.qkv[:, Hq * D:(Hq + Hkv) * D].view(M, Hkv, D)
+        self.v = self.qkv[:, (Hq + Hkv) * D:].view(M, Hkv, D)
+        self.scale = 1.0 / math.sqrt(D)
+        self.max_seqlen = int(self.p["lengths"].max())
+        dd = self.d
+        B = len(dd["context_lens_host"])
+        self.ws = torch.empty(ops.opscale_attn_decode_workspace_size(B, dc.n_q_heads, dc.head_dim,
+                                                                    dd["max_context_len"]),
+                              dtype=torch.uint8, device="cuda")
+        self.dout = torch.empty_like(dd["q"])
+        self.names = ["rmsnorm_1", "qkv_linear", "attn_prefill", "o_linear", "rmsnorm_2",
+                      "gate_up_linear", "swiglu", "down_linear", "attn_decode"]
+
+    def step(self, events=None):
+        ops, p, d = self.ops, self.p, self.d
+        eps = self.pc.eps
+
+        def mark(i):
+            if events is not None:
+                events[i].record()
+        mark(0)
+        ops.opscale_rmsnorm(p["x"], p["w_norm1"], y=self.h1, eps=eps); mark(1)
+        ops.opscale_linear(self.h1, p["w_qkv"], y=self.qkv); mark(2)
+        ops.opscale_attn_prefill(self.q, self.k, self.v, p["cu_seqlens"], self.max_seqlen, self.scale,
+                                 True, out=self.attn); mark(3)
+        ops.opscale_linear(self.attn.view(self.p["M"], -1), p["w_o"], y=self.o); mark(4)
+        ops.opscale_rmsnorm(self.o, p["w_norm2"], y=self.h2, eps=eps); mark(5)
+        ops.opscale_linear(self.h2, p["w_gate_up"], y=self.gu); mark(6)
+        ops.opscale_swiglu(self.gu, out=self.act); mark(7)
+        ops.opscale_linear(self.act, p["w_down"], y=self.y); mark(8)
+        ops.opscale_attn_decode(d["q"], d["k_cache"], d["v_cache"], d["block_table"], d["context_lens"],
+                                d["max_context_len"], self.scale, workspace=self.ws, out=self.dout); mark(9)
+
+    def work(self):
+        """Algorithmic (flops, bytes, bound, units, unit-name) per operator."""
+        from_cost = _closed_forms()
+        pc, dc = self.pc, self.dc
+        M, H, F = self.p["M"], pc.hidden, pc.ffn
+        Hq, Hkv, D = pc.n_q_heads, pc.n_kv_heads, pc.head_dim
+        lens = self.p["lengths"]
+        ctx = self.d["context_lens_host"]
+        s = 2
+        return {
+            "rmsnorm_1": (*from_cost["rmsnorm"](M, H, s), "hbm", M, "tokens/s"),
+            "qkv_linear": (*from_cost["linear"](M, pc.qkv_out, H, s), "mfma", M, "tokens/s"),
+            "attn_prefill": (*from_cost["attn_prefill"](lens, Hq, Hkv, D, s), "mfma", M, "tokens/s"),
+            "o_linear": (*from_cost["linear"](M, H, Hq * D, s), "mfma", M, "tokens/s"),
+            "rmsnorm_2": (*from_cost["rmsnorm"](M, H, s), "hbm", M, "tokens/s"),
+            "gate_up_linear": (*from_cost["linear"](M, 2 * F, H, s), "mfma", M, "tokens/s"),
+            "swiglu": (*from_cost["swiglu"](M, F, s), "hbm", M, "tokens/s"),
+            "down_linear": (*from_cost["linear"](M, H, F, s), "mfma", M, "tokens/s"),
+            "attn_decode": (*from_cost["attn_decode"](ctx, dc.n_q_heads, dc.n_kv_heads, dc.head_dim, s,
+                                                      dc.block_size), "hbm", len(ctx), "seq/s"),
+        }
+
+
+def _closed_forms():
+    """Algorithmic flop/byte counts of each operator (same closed forms as the
+    library's timing struct; restated here so the benchmark's roofline does not
+    depend on the library's own accounting)."""
+    def rmsnorm(M, H, s):
+        return 4 * M * H, s * (2 * M * H + H)
+
+    def linear(M, N, K, s):
+        return 2 * M * N * K, s * (M * K + N * K + M * N)
+
+    def swiglu(M, F, s):
+        return 6 * M * F, 3 * s * M * F
+
+    def attn_prefill(lens, Hq, Hkv, D, s):
+        T = int(sum(int(x) for x in lens))
+        pairs = sum(int(x) * (int(x) + 1) // 2 for x in lens)
+        return 4 * D * Hq * pairs, s * (2 * T * Hq * D + 2 * T * Hkv * D)
+
+    def attn_decode(ctx, Hq, Hkv, D, s, bs):
+        N = int(sum(int(x) for x in ctx))
+        nb = sum((int(x) + bs - 1) // bs for x in ctx)
+        return 4 * D * Hq * N, s * (2 * Hkv * D * N + 2 * len(ctx) * Hq * D) + 4 * (nb + len(ctx))
+    return dict(rmsnorm=rmsnorm, linear=linear, swiglu=swiglu, attn_prefill=attn_prefill,
+                attn_decode=attn_decode)
+
+
+def cpu_baseline(budget_s: float = 20.0):
+    """Time the fp64 CPU oracle on a bounded sample of the same prefill layer
+    and extrapolate to the full batch (rows scale linearly; attention by the
+    causal pair count).  Reported as a baseline only."""
+    import numpy as np
+
+    import oracle
+    import workloads as wl
+    cfg = wl.C2
+    lens = wl.seq_lengths(cfg)
+    M, H, F = int(lens.sum()), cfg.hidden, cfg.ffn
+    Hq, Hkv, D = cfg.n_q_heads, cfg.n_kv_heads, cfg.head_dim
+    rows = 256
+    g = lambda tag, shape, std=1.0, mean=0.0: wl.normal(wl.rng_for(cfg, tag), shape, std, mean).astype(np.float64)
+    x = g("x", (rows, H))
+    wn = g("w_norm", (H,), 0.02, 1.0)
+    Ws = {"qkv": g("w_qkv", (cfg.qkv_out, H), 0.02), "o": g("w_o", (H, Hq * D), 0.02),
+          "gate_up": g("w_gate_up", (2 * F, H), 0.02), "down": g("w_down", (H, F), 0.02)}
+    t = {}
+    t0 = time.perf_counter()
+    h = oracle.rmsnorm(x, wn, cfg.eps)
+    t["rmsnorm"] = 2 * (time.perf_counter() - t0)
+    t0 = time.perf_counter()
+    qkv = oracle.linear(h, Ws["qkv"])
+    o = oracle.linear(x[:, : Hq * D], Ws["o"])
+    gu = oracle.linear(h, Ws["gate_up"])
+    t["linears_a"] = time.perf_counter() - t0
+    t0 = time.perf_counter()
+    act = oracle.swiglu(gu)
+    t["swiglu"] = time.perf_counter() - t0
+    t0 = time.perf_counter()
+    oracle.linear(act, Ws["down"])
+    t["linears_b"] = time.perf_counter() - t0
+    per_row = sum(t.values()) / rows
+    # attention: whole prompts, shortest first, until the budget share is used
+    order = np.argsort(lens)
+    done_pairs, att_s, used = 0, 0.0, []
+    for b in order:
+        L = int(lens[b])
+        q = g("q", (L, Hq, D))
+        k = g("k", (L, Hkv, D))
+        v = g("v", (L, Hkv, D))
+        t0 = time.perf_counter()
+        oracle.attn_prefill(q, k, v, [0, L], 1 / math.sqrt(D), True)
+        att_s += time.perf_counter() - t0
+        done_pairs += L * (L + 1) // 2
+        used.append(L)
+        if att_s > budget_s * 0.5:
+            break
+    all_pairs = int(sum(int(L) * (int(L) + 1) // 2 for L in lens))
+    total_s = per_row * M + att_s * all_pairs / done_pairs
+    try:
+        from threadpoolctl import threadpool_info
+        cores = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
+    except Exception:  # pragma: no cover
+        cores = len(os.sched_getaffinity(0))
+    return {"value": M / total_s, "unit": "tokens/s", "cores": int(cores), "kind": "oracle",
+            "sample": f"fp64 NumPy oracle on {rows} token rows of every per-row operator (RMSNorm, 4 linears, "
+                      f"SwiGLU) and {len(used)} whole prompts of attention (lengths {used}), "
+                      f"extrapolated to the {M}-token batch by rows and causal key-query pairs; "
+                      f"decode attention not included; measured {sum(t.values()) + att_s:.1f} s"}
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--calibrate-copy-mib", type=int, default=0,
+                    help="run one device copy of this many MiB before the steps (counter calibration)")
+    a = ap.parse_args()
+    if a.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
+        print(f"bench.py runs on one GPU only (asked for {a.gpus}); multi-GPU sharding is not part of "
+              "this build.", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    import paper_2608_13499_amd as ops
+    import workloads as wl
+    assert torch.cuda.is_available(), "no GPU"
+    ops.load()
+    torch.cuda.set_device(0)
+    log("building inputs ...")
+    layer = Layer(ops, wl, torch)
+    torch.cuda.synchronize()
+    if a.calibrate_copy_mib:
+        src = torch.empty(a.calibrate_copy_mib << 20, dtype=torch.uint8, device="cuda")
+        dst = torch.empty_like(src)
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
+    log("warmup ...")
+    for _ in range(a.warmup):
+        layer.step()
+    torch.cuda.synchronize()
+    n = len(layer.names)
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(n + 1)] for _ in range(a.steps)]
+    log(f"timing {a.steps} steps ...")
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for s in range(a.steps):
+        layer.step(evs[s])
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    ms_step = (t1 - t0) * 1e3 / a.steps
+    per_op_us = {nm: sum(evs[s][i].elapsed_time(evs[s][i + 1]) for s in range(a.steps)) * 1e3 / a.steps
+                 for i, nm in enumerate(layer.names)}
+    work = layer.work()
+    per_op = {}
+    for nm in layer.names:
+        fl, by, bound, units, unit = work[nm]
+        t_s = per_op_us[nm] * 1e-6
+        att = min(PEAK_BF16, fl / by * PEAK_HBM)
+        per_op[nm] = {"us": round(per_op_us[nm], 2), unit: round(units / t_s, 1),
+                      "tflops": round(fl / t_s * 1e-12, 2), "gbps": round(by / t_s * 1e-9, 1),
+                      "bound": bound, "roofline_frac": round((fl / t_s) / att, 4)}
+    dom = max(layer.names, key=lambda nm: per_op_us[nm])
+    fl, by, bound, _, _ = work[dom]
+    kernel = {"mfma": "gemm_bf16_kernel", "hbm": "rmsnorm_kernel"}[bound] if "linear" in dom or "norm" in dom else \
+        {"attn_prefill": "attn_prefill_bf16_kernel", "attn_decode": "attn_decode_split_kernel",
+         "swiglu": "swiglu_kernel"}[dom]
+    t_dom = per_op_us[dom] * 1e-6
+    if bound == "mfma":
+        roof = {"bound": "mfma", "achieved": round(fl / t_dom * 1e-12, 2), "peak": PEAK_BF16 * 1e-12,
+                "unit": "TFLOP/s"}
+    else:
+        roof = {"bound": "hbm", "achieved": round(by / t_dom * 1e-9, 1), "peak": PEAK_HBM * 1e-9, "unit": "GB/s"}
+    roof["frac"] = round(roof["achieved"] / roof["peak"], 4)
+    roof["traffic"] = measured_traffic(kernel)
+    roof["kernel"] = f"{kernel} ({dom})"
+    roof["work_per_launch"] = {"flops": fl, "bytes": by}
+    M = layer.p["M"]
+    out = {
+        "metric": "per-operator prefill tokens/s + % of MFMA/HBM roofline, Llama-8B-shaped layer",
+        "value": round(M / (ms_step * 1e-3), 1),
+        "unit": "tokens/s",
+        "n_gpus": 1, "steps": a.steps, "warmup": a.warmup,
+        "ms_per_step": round(ms_step, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": f"{layer.pc.name} (16 prompts, {M} tokens, hidden 4096, 32/8 heads x 128, "
+                               f"FFN 14336) + {layer.dc.name} attention (256 seqs, contexts U[128,8192])",
+                   "global_batch": M, "seq_len": int(layer.p["lengths"].max()), "parallelism": "none"},
+        "roofline": roof,
+        "per_op": per_op,
+    }
+    if not a.no_cpu_baseline:
+        log("cpu baseline (oracle) ...")
+        out["cpu_baseline"] = cpu_baseline()
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

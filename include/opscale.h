@@ -1,0 +1,233 @@
+/*
+ * opscale.h -- C ABI of the per-operator decoder-layer forward for AMD MI355X
+ * (CDNA4, gfx950).
+ *
+ * The paper treats an LLM as a dataflow of operators that are profiled,
+ * provisioned and scaled one by one (Section 2.2 "Rethinking the Scaling
+ * Unit"; Section 4 "Operator Profiling").  Each entry point below is one such
+ * operator of a Llama-style decoder layer: RMS Norm, the QKV / O / gate-up /
+ * down linears, the fused SiLU-multiply activation, causal grouped-query
+ * prefill attention over a ragged batch of prompts, and decode attention over a
+ * paged KV cache.  Every call can return its kernel-only device time, measured
+ * with device events around the launches and excluding host overhead (Section
+ * 2.1 "Compute Sensitivity"), together with the operator's algorithmic flops
+ * and bytes, the inputs of the profiler's T_v / M_v / C_v tables (Section 3.1,
+ * Section 4).
+ *
+ * Conventions shared by every entry point
+ *  - Pointers: all tensor pointers are DEVICE pointers to caller-owned memory,
+ *    16-byte aligned.  The library never allocates or frees device memory in an
+ *    operator call; the decode split-KV scratch is a caller workspace.
+ *  - Layout: row-major, innermost dimension contiguous.  Element type is given
+ *    by `dt` and shared by every tensor of the call (indices are int32).
+ *  - Sizes: int64 element counts.  A zero-sized problem (M == 0, B == 0 or
+ *    total_tokens == 0) is a successful no-op.  Negative sizes are invalid.
+ *  - Streams: work is enqueued on `stream` (0 = the null stream).  With
+ *    `timing == NULL` a call is fully asynchronous.  With `timing != NULL` the
+ *    call records two device events on `stream` around its launches, waits for
+ *    the second, and fills the struct (a blocking call).
+ *  - Errors: a call validates every argument before enqueuing anything and
+ *    returns OPSCALE_ERR_INVALID_ARG / _UNSUPPORTED / _WORKSPACE with nothing
+ *    enqueued.  A failed HIP call returns OPSCALE_ERR_HIP.  The thread-local
+ *    message of the last failure is available from opscale_last_error().
+ *    Nothing aborts, exits or throws across this interface.
+ *  - Concurrency: entry points are re-entrant; the only library state is a
+ *    pair of timing events per host thread, created on first use.
+ */
+#ifndef OPSCALE_H
+#define OPSCALE_H
+
+#include <stddef.h>
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  OPSCALE_OK = 0,
+  OPSCALE_ERR_INVALID_ARG = 1, /* null pointer, bad size, misalignment */
+  OPSCALE_ERR_UNSUPPORTED = 2, /* valid but not implemented (e.g. head_dim 96) */
+  OPSCALE_ERR_WORKSPACE = 3,   /* caller workspace smaller than required */
+  OPSCALE_ERR_HIP = 4          /* a HIP runtime call or launch failed */
+} opscale_status;
+
+typedef enum {
+  OPSCALE_F32 = 0,  /* fp32 storage, fp32 arithmetic */
+  OPSCALE_BF16 = 1  /* bf16 storage, fp32 accumulation, bf16 result */
+} opscale_dtype;
+
+/* Kernel-only time of one call plus its algorithmic work: flops counted as
+ * 2 per multiply-add of the contractions, bytes as every input read once and
+ * every output written once (weights once, K/V once per KV head, causal
+ * attention over the visible lower triangle only). */
+typedef struct {
+  float elapsed_us;
+  double alg_flops;
+  double alg_bytes;
+} opscale_timing;
+
+/* Library version string, e.g. "opscale 0.1.0 gfx950". */
+const char* opscale_version(void);
+const char* opscale_status_string(opscale_status s);
+/* Message of the last failed call on this host thread ("" if none). */
+const char* opscale_last_error(void);
+
+/*
+ * RMS Norm (Section 2.1: the memory-bound, compute-light operator).
+ *   y[m, j] = x[m, j] / sqrt(mean_j x[m, j]^2 + eps) * w[j]
+ * x, y: [M, H]; w: [H].  Sum of squares in fp32, one rounding at the output.
+ * In-place (y == x) is allowed.  H * sizeof(dt) must be a multiple of 16.
+ */
+opscale_status opscale_rmsnorm(const void* x, const void* w, void* y, int64_t M, int64_t H,
+                               float eps, opscale_dtype dt, hipStream_t stream,
+                               opscale_timing* timing);
+
+/*
+ * Linear projection (Section 2.1: QKV Linear, wide projections, MLP linears).
+ *   y[m, n] = sum_k x[m, k] * W[n, k] (+ bias[n])
+ * x: [M, K]; W: [N, K] (the nn.Linear weight layout); bias: [N] or NULL;
+ * y: [M, N], must not alias x or W.  bf16: MFMA with fp32 accumulation.
+ * K * sizeof(dt) and N * sizeof(dt) must be multiples of 16.
+ */
+opscale_status opscale_linear(const void* x, const void* W, const void* bias, void* y,
+                              int64_t M, int64_t N, int64_t K, opscale_dtype dt,
+                              hipStream_t stream, opscale_timing* timing);
+
+/*
+ * Fused SiLU-and-multiply, the SwiGLU activation ("act_and_mul" / "SiLu Mul",
+ * Section 2.1 memory study and Appendix C).
+ *   out[m, f] = silu(gate_up[m, f]) * gate_up[m, F + f],  silu(z) = z / (1 + e^-z)
+ * gate_up: [M, 2F] (gate half first: the merged gate-up linear's output);
+ * out: [M, F].  fp32 arithmetic.  F * sizeof(dt) must be a multiple of 16.
+ */
+opscale_status opscale_swiglu(const void* gate_up, void* out, int64_t M, int64_t F,
+                              opscale_dtype dt, hipStream_t stream, opscale_timing* timing);
+
+/*
+ * Prefill self-attention over a ragged batch (Section 2.1: quadratic in prompt
+ * length, FlashAttention-style with no stored score matrix; grouped-query
+ * attention as in the Table 3 models).
+ * For prompt b (tokens cu_seqlens[b] .. cu_seqlens[b+1]-1), local query i,
+ * query head h and KV head g = h / (Hq / Hkv):
+ *   o[t, h, :] = sum_{j visible} softmax_j(scale * q[t, h, :] . k[c_b + j, g, :]) v[c_b + j, g, :]
+ * where key j is visible iff j <= i (causal != 0) or j < L_b (causal == 0).
+ * q: token t, head h at q + t * q_row_stride + h * D (elements); k and v: token t,
+ *   KV head g at k/v + t * kv_row_stride + g * D.  The strides let q, k, v be
+ *   views into the packed output of the QKV linear.
+ * o: [total_tokens, Hq, D] contiguous.
+ * cu_seqlens: DEVICE int32 [B + 1], cu_seqlens[0] = 0, non-decreasing,
+ *   cu_seqlens[B] = total_tokens.  Zero-length prompts are allowed.
+ * max_seqlen: an upper bound on the prompt lengths, used to size the launch;
+ *   the result does not depend on it being tight (it must be >= 1).
+ * D must be 64 or 128; Hkv must divide Hq.  bf16: QK^T and PV on MFMA, fp32
+ *   online softmax, probabilities rounded to bf16 for the PV product.
+ */
+opscale_status opscale_attn_prefill(const void* q, const void* k, const void* v,
+                                    int64_t q_row_stride, int64_t kv_row_stride, void* o,
+                                    const int32_t* cu_seqlens, int32_t B, int64_t total_tokens,
+                                    int32_t max_seqlen, int32_t Hq, int32_t Hkv, int32_t D,
+                                    float scale, int32_t causal, opscale_dtype dt,
+                                    hipStream_t stream, opscale_timing* timing);
+
+/*
+ * Bytes of device workspace that opscale_attn_decode needs for these sizes
+ * (split-KV partial results).  0 is never returned for B > 0.
+ */
+size_t opscale_attn_decode_workspace_size(int32_t B, int32_t Hq, int32_t D,
+                                          int32_t max_context_len);
+
+/*
+ * Decode attention, one new query token per sequence, over a paged KV cache
+ * (Section 2.1 decode phase; Appendix E: decode is memory-bound; the serving
+ * engine of Section 5 keeps K/V in a paged cache).
+ *   o[b, h, :] = sum_{j < n_b} softmax_j(scale * q[b, h, :] . K_b[j, g, :]) V_b[j, g, :]
+ * with n_b = context_lens[b] (already including the new token, whose K/V were
+ * written to the cache beforehand) and K_b[j] = k_cache[block_table[b, j / bs], j % bs].
+ * q, o: [B, Hq, D]; k_cache, v_cache: [num_blocks, block_size, Hkv, D];
+ * block_table: DEVICE int32 [B, max_blocks_per_seq]; context_lens: DEVICE int32 [B].
+ * A context length of 0 yields a zero output row.  Lengths above
+ * max_blocks_per_seq * block_size are clamped to it.  Block ids outside
+ * [0, num_blocks) read as zeros (no fault).
+ * max_context_len: an upper bound on context_lens used to size the split-KV
+ *   launch and the workspace; results do not depend on it.
+ * workspace: DEVICE scratch of at least opscale_attn_decode_workspace_size(B,
+ *   Hq, D, max_context_len) bytes, else OPSCALE_ERR_WORKSPACE.  Contents on
+ *   entry are ignored.  Calls sharing a workspace must be stream-ordered.
+ * block_size must be a power of two in [1, 1024]; D 64 or 128; Hkv | Hq and
+ *   Hq / Hkv <= 16.
+ */
+opscale_status opscale_attn_decode(const void* q, const void* k_cache, const void* v_cache,
+                                   const int32_t* block_table, const int32_t* context_lens,
+                                   void* o, int32_t B, int32_t Hq, int32_t Hkv, int32_t D,
+                                   int32_t block_size, int32_t max_blocks_per_seq,
+                                   int64_t num_blocks, int32_t max_context_len, float scale,
+                                   opscale_dtype dt, void* workspace, size_t workspace_bytes,
+                                   hipStream_t stream, opscale_timing* timing);
+
+/* ---------------------------------------------------------------------------
+ * Operator profiling (Section 4 "Operator Profiling": per-operator compute
+ * time T_v and memory M_v; Appendix C "Dataflow Characteristics": the payload
+ * an operator hands to the next one, the basis of C_v).
+ * ------------------------------------------------------------------------- */
+typedef enum {
+  OPSCALE_OP_RMSNORM = 0,
+  OPSCALE_OP_LINEAR = 1,
+  OPSCALE_OP_SWIGLU = 2,
+  OPSCALE_OP_ATTN_PREFILL = 3,
+  OPSCALE_OP_ATTN_DECODE = 4
+} opscale_op;
+
+/* One operator call: the argument list of the matching entry point. */
+typedef struct {
+  opscale_op op;
+  opscale_dtype dt;
+  union {
+    struct { const void* x; const void* w; void* y; int64_t M, H; float eps; } rmsnorm;
+    struct { const void* x; const void* W; const void* bias; void* y; int64_t M, N, K; } linear;
+    struct { const void* gate_up; void* out; int64_t M, F; } swiglu;
+    struct {
+      const void *q, *k, *v; int64_t q_row_stride, kv_row_stride; void* o;
+      const int32_t* cu_seqlens; int32_t B; int64_t total_tokens; int32_t max_seqlen;
+      int32_t Hq, Hkv, D; float scale; int32_t causal;
+    } attn_prefill;
+    struct {
+      const void *q, *k_cache, *v_cache; const int32_t *block_table, *context_lens; void* o;
+      int32_t B, Hq, Hkv, D, block_size, max_blocks_per_seq; int64_t num_blocks;
+      int32_t max_context_len; float scale; void* workspace; size_t workspace_bytes;
+    } attn_decode;
+  } u;
+} opscale_op_desc;
+
+typedef struct {
+  int32_t iters;
+  float us_median, us_p10, us_p90, us_min, us_mean;
+  double alg_flops, alg_bytes;
+  double tflops;          /* alg_flops / median time, in TFLOP/s */
+  double gbps;            /* alg_bytes / median time, in GB/s (1e9) */
+  double attainable_tflops; /* min(compute peak, flops/byte * HBM peak) */
+  double roofline_frac;   /* tflops / attainable_tflops */
+  int32_t bound;          /* 0: matrix-core bound, 1: HBM bound */
+  int64_t weight_bytes;   /* M_v, static part: parameters */
+  int64_t transient_bytes;/* M_v, transient part: activations / KV touched */
+  int64_t io_bytes;       /* output payload passed to the next operator */
+} opscale_profile;
+
+/*
+ * Run the described operator `warmup` times untimed, then `iters` times, each
+ * preceded (when flush_buf != NULL) by a device write of flush_bytes to
+ * flush_buf so that no operand is served from the 256 MB last-level cache.
+ * Each iteration is timed alone with device events.  Fills `out` with the
+ * timing distribution, the algorithmic work and the roofline fraction against
+ * MI355X peaks (bf16 matrix 2.5 PFLOP/s, fp32 matrix 157.3 TFLOP/s, HBM
+ * 8 TB/s).  Blocking.  iters must be >= 1.
+ */
+opscale_status opscale_op_profile(const opscale_op_desc* desc, int32_t warmup, int32_t iters,
+                                  void* flush_buf, size_t flush_bytes, hipStream_t stream,
+                                  opscale_profile* out);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* OPSCALE_H */

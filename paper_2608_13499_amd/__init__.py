@@ -1,0 +1,12 @@
+"""MI355X (gfx950) per-operator decoder-layer forward: RMSNorm, linear, SwiGLU,
+ragged causal GQA prefill attention and paged decode attention as hand-written
+HIP kernels behind the C ABI in include/opscale.h.  This package holds the HIP
+sources (csrc/), their build script and the ctypes binding."""
+from ._lib import (  # noqa: F401
+    OpscaleError, Timing, Profile, OpDesc, load, LIB_PATH, EXPORTS,
+    opscale_version, opscale_rmsnorm, opscale_linear, opscale_swiglu, opscale_attn_prefill,
+    opscale_attn_decode_workspace_size, opscale_attn_decode, opscale_op_profile,
+    desc_rmsnorm, desc_linear, desc_swiglu, desc_attn_prefill, desc_attn_decode,
+    OPSCALE_OK, OPSCALE_ERR_INVALID_ARG, OPSCALE_ERR_UNSUPPORTED, OPSCALE_ERR_WORKSPACE,
+    OPSCALE_ERR_HIP, OPSCALE_F32, OPSCALE_BF16,
+)

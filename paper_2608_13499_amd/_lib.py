@@ -1,0 +1,328 @@
+"""ctypes binding of libopscale (include/opscale.h).
+
+Argument marshalling only: every operator runs in the library's HIP kernels.
+PyTorch supplies device memory and the current HIP stream.  The functions keep
+the C names; tensors are passed instead of raw pointers, and sizes are taken
+from the tensor shapes.  A missing library or a failed call raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libopscale.so")
+
+OPSCALE_OK, OPSCALE_ERR_INVALID_ARG, OPSCALE_ERR_UNSUPPORTED, OPSCALE_ERR_WORKSPACE, OPSCALE_ERR_HIP = range(5)
+OPSCALE_F32, OPSCALE_BF16 = 0, 1
+OP_RMSNORM, OP_LINEAR, OP_SWIGLU, OP_ATTN_PREFILL, OP_ATTN_DECODE = range(5)
+
+c_i32, c_i64, c_f32, c_f64, c_vp, c_sz = (ctypes.c_int32, ctypes.c_int64, ctypes.c_float,
+                                          ctypes.c_double, ctypes.c_void_p, ctypes.c_size_t)
+
+
+class OpscaleError(RuntimeError):
+    def __init__(self, status: int, message: str):
+        super().__init__(f"opscale status {status}: {message}")
+        self.status = status
+
+
+class Timing(ctypes.Structure):
+    _fields_ = [("elapsed_us", c_f32), ("alg_flops", c_f64), ("alg_bytes", c_f64)]
+
+
+class _RmsnormArgs(ctypes.Structure):
+    _fields_ = [("x", c_vp), ("w", c_vp), ("y", c_vp), ("M", c_i64), ("H", c_i64), ("eps", c_f32)]
+
+
+class _LinearArgs(ctypes.Structure):
+    _fields_ = [("x", c_vp), ("W", c_vp), ("bias", c_vp), ("y", c_vp), ("M", c_i64), ("N", c_i64), ("K", c_i64)]
+
+
+class _SwigluArgs(ctypes.Structure):
+    _fields_ = [("gate_up", c_vp), ("out", c_vp), ("M", c_i64), ("F", c_i64)]
+
+
+class _PrefillArgs(ctypes.Structure):
+    _fields_ = [("q", c_vp), ("k", c_vp), ("v", c_vp), ("q_row_stride", c_i64), ("kv_row_stride", c_i64),
+                ("o", c_vp), ("cu_seqlens", c_vp), ("B", c_i32), ("total_tokens", c_i64),
+                ("max_seqlen", c_i32), ("Hq", c_i32), ("Hkv", c_i32), ("D", c_i32), ("scale", c_f32),
+                ("causal", c_i32)]
+
+
+class _DecodeArgs(ctypes.Structure):
+    _fields_ = [("q", c_vp), ("k_cache", c_vp), ("v_cache", c_vp), ("block_table", c_vp),
+                ("context_lens", c_vp), ("o", c_vp), ("B", c_i32), ("Hq", c_i32), ("Hkv", c_i32),
+                ("D", c_i32), ("block_size", c_i32), ("max_blocks_per_seq", c_i32), ("num_blocks", c_i64),
+                ("max_context_len", c_i32), ("scale", c_f32), ("workspace", c_vp), ("workspace_bytes", c_sz)]
+
+
+class _OpUnion(ctypes.Union):
+    _fields_ = [("rmsnorm", _RmsnormArgs), ("linear", _LinearArgs), ("swiglu", _SwigluArgs),
+                ("attn_prefill", _PrefillArgs), ("attn_decode", _DecodeArgs)]
+
+
+class OpDesc(ctypes.Structure):
+    _fields_ = [("op", c_i32), ("dt", c_i32), ("u", _OpUnion)]
+
+
+class Profile(ctypes.Structure):
+    _fields_ = [("iters", c_i32), ("us_median", c_f32), ("us_p10", c_f32), ("us_p90", c_f32),
+                ("us_min", c_f32), ("us_mean", c_f32), ("alg_flops", c_f64), ("alg_bytes", c_f64),
+                ("tflops", c_f64), ("gbps", c_f64), ("attainable_tflops", c_f64),
+                ("roofline_frac", c_f64), ("bound", c_i32), ("weight_bytes", c_i64),
+                ("transient_bytes", c_i64), ("io_bytes", c_i64)]
+
+    def as_dict(self):
+        return {name: getattr(self, name) for name, _ in self._fields_}
+
+
+EXPORTS = {
+    "opscale_version": (ctypes.c_char_p, []),
+    "opscale_status_string": (ctypes.c_char_p, [c_i32]),
+    "opscale_last_error": (ctypes.c_char_p, []),
+    "opscale_rmsnorm": (c_i32, [c_vp, c_vp, c_vp, c_i64, c_i64, c_f32, c_i32, c_vp, ctypes.POINTER(Timing)]),
+    "opscale_linear": (c_i32, [c_vp, c_vp, c_vp, c_vp, c_i64, c_i64, c_i64, c_i32, c_vp, ctypes.POINTER(Timing)]),
+    "opscale_swiglu": (c_i32, [c_vp, c_vp, c_i64, c_i64, c_i32, c_vp, ctypes.POINTER(Timing)]),
+    "opscale_attn_prefill": (c_i32, [c_vp, c_vp, c_vp, c_i64, c_i64, c_vp, c_vp, c_i32, c_i64, c_i32,
+                                     c_i32, c_i32, c_i32, c_f32, c_i32, c_i32, c_vp, ctypes.POINTER(Timing)]),
+    "opscale_attn_decode_workspace_size": (c_sz, [c_i32, c_i32, c_i32, c_i32]),
+    "opscale_attn_decode": (c_i32, [c_vp, c_vp, c_vp, c_vp, c_vp, c_vp, c_i32, c_i32, c_i32, c_i32, c_i32,
+                                    c_i32, c_i64, c_i32, c_f32, c_i32, c_vp, c_sz, c_vp,
+                                    ctypes.POINTER(Timing)]),
+    "opscale_op_profile": (c_i32, [ctypes.POINTER(OpDesc), c_i32, c_i32, c_vp, c_sz, c_vp,
+                                   ctypes.POINTER(Profile)]),
+}
+
+_lib = None
+
+
+def load(path: Optional[str] = None):
+    """Load libopscale.so once; raise if it has not been built."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    path = path or LIB_PATH
+    if not os.path.exists(path):
+        raise OpscaleError(-1, f"{path} is missing: build it with `python -m paper_2608_13499_amd.build`")
+    lib = ctypes.CDLL(path)
+    for name, (res, args) in EXPORTS.items():
+        fn = getattr(lib, name)
+        fn.restype = res
+        fn.argtypes = args
+    _lib = lib
+    return lib
+
+
+def _check(status: int):
+    if status != OPSCALE_OK:
+        lib = load()
+        raise OpscaleError(status, lib.opscale_last_error().decode())
+
+
+# ----------------------------------------------------------------- helpers --
+def _dt(t) -> int:
+    import torch
+    if t.dtype == torch.bfloat16:
+        return OPSCALE_BF16
+    if t.dtype == torch.float32:
+        return OPSCALE_F32
+    raise OpscaleError(OPSCALE_ERR_UNSUPPORTED, f"dtype {t.dtype} (supported: bfloat16, float32)")
+
+
+def _dev(*tensors):
+    for t in tensors:
+        if t is not None and not t.is_cuda:
+            raise OpscaleError(OPSCALE_ERR_INVALID_ARG, "tensors must be on the GPU")
+
+
+def _stream(stream) -> int:
+    import torch
+    if stream is None:
+        return torch.cuda.current_stream().cuda_stream
+    if isinstance(stream, int):
+        return stream
+    return stream.cuda_stream
+
+
+def _ptr(t):
+    return None if t is None else t.data_ptr()
+
+
+def _contig(name, t):
+    if not t.is_contiguous():
+        raise OpscaleError(OPSCALE_ERR_INVALID_ARG, f"{name} must be contiguous")
+
+
+# --------------------------------------------------------------- operators --
+def opscale_version() -> str:
+    return load().opscale_version().decode()
+
+
+def opscale_rmsnorm(x, w, y=None, eps: float = 1e-5, stream=None, timed: bool = False):
+    """y = x / sqrt(mean(x^2) + eps) * w over the last dim of x [M, H]."""
+    import torch
+    lib = load()
+    _dev(x, w, y)
+    _contig("x", x)
+    _contig("w", w)
+    if y is None:
+        y = torch.empty_like(x)
+    _contig("y", y)
+    H = x.shape[-1]
+    M = x.numel() // H if H else 0
+    t = Timing() if timed else None
+    _check(lib.opscale_rmsnorm(_ptr(x), _ptr(w), _ptr(y), M, H, eps, _dt(x), _stream(stream),
+                               ctypes.byref(t) if t else None))
+    return (y, t) if timed else y
+
+
+def opscale_linear(x, W, bias=None, y=None, stream=None, timed: bool = False):
+    """y[M, N] = x[M, K] W[N, K]^T (+ bias)."""
+    import torch
+    lib = load()
+    _dev(x, W, bias, y)
+    for n, t_ in (("x", x), ("W", W), ("bias", bias), ("y", y)):
+        if t_ is not None:
+            _contig(n, t_)
+    K = x.shape[-1]
+    M = x.numel() // K
+    N = W.shape[0]
+    if W.shape[1] != K:
+        raise OpscaleError(OPSCALE_ERR_INVALID_ARG, f"W is {tuple(W.shape)}, expected [N, {K}]")
+    if y is None:
+        y = torch.empty(*x.shape[:-1], N, dtype=x.dtype, device=x.device)
+    t = Timing() if timed else None
+    _check(lib.opscale_linear(_ptr(x), _ptr(W), _ptr(bias), _ptr(y), M, N, K, _dt(x), _stream(stream),
+                              ctypes.byref(t) if t else None))
+    return (y, t) if timed else y
+
+
+def opscale_swiglu(gate_up, out=None, stream=None, timed: bool = False):
+    """out[M, F] = silu(gate_up[:, :F]) * gate_up[:, F:]."""
+    import torch
+    lib = load()
+    _dev(gate_up, out)
+    _contig("gate_up", gate_up)
+    F = gate_up.shape[-1] // 2
+    M = gate_up.numel() // (2 * F)
+    if out is None:
+        out = torch.empty(*gate_up.shape[:-1], F, dtype=gate_up.dtype, device=gate_up.device)
+    _contig("out", out)
+    t = Timing() if timed else None
+    _check(lib.opscale_swiglu(_ptr(gate_up), _ptr(out), M, F, _dt(gate_up), _stream(stream),
+                              ctypes.byref(t) if t else None))
+    return (out, t) if timed else out
+
+
+def opscale_attn_prefill(q, k, v, cu_seqlens, max_seqlen: int, scale: float, causal: bool = True,
+                         out=None, stream=None, timed: bool = False):
+    """Ragged causal GQA attention.  q [T, Hq, D], k/v [T, Hkv, D]; the token
+    dimension may be strided (views into a packed QKV tensor), heads and head
+    dim must be contiguous.  cu_seqlens: int32 [B+1] on the GPU."""
+    import torch
+    lib = load()
+    _dev(q, k, v, cu_seqlens, out)
+    T, Hq, D = q.shape
+    Hkv = k.shape[1]
+    for name, t_, H in (("q", q, Hq), ("k", k, Hkv), ("v", v, Hkv)):
+        if t_.stride(2) != 1 or t_.stride(1) != D or t_.shape[0] != T:
+            raise OpscaleError(OPSCALE_ERR_INVALID_ARG, f"{name} must be [T, H, D] with contiguous heads")
+    if k.stride(0) != v.stride(0):
+        raise OpscaleError(OPSCALE_ERR_INVALID_ARG, "k and v must share a row stride")
+    if cu_seqlens.dtype != torch.int32:
+        raise OpscaleError(OPSCALE_ERR_INVALID_ARG, "cu_seqlens must be int32")
+    if out is None:
+        out = torch.empty(T, Hq, D, dtype=q.dtype, device=q.device)
+    _contig("out", out)
+    B = cu_seqlens.numel() - 1
+    t = Timing() if timed else None
+    _check(lib.opscale_attn_prefill(_ptr(q), _ptr(k), _ptr(v), q.stride(0), k.stride(0), _ptr(out),
+                                    _ptr(cu_seqlens), B, T, max_seqlen, Hq, Hkv, D, scale, int(causal),
+                                    _dt(q), _stream(stream), ctypes.byref(t) if t else None))
+    return (out, t) if timed else out
+
+
+def opscale_attn_decode_workspace_size(B: int, Hq: int, D: int, max_context_len: int) -> int:
+    return int(load().opscale_attn_decode_workspace_size(B, Hq, D, max_context_len))
+
+
+def opscale_attn_decode(q, k_cache, v_cache, block_table, context_lens, max_context_len: int,
+                        scale: float, workspace=None, out=None, stream=None, timed: bool = False):
+    """Decode attention over a paged cache [num_blocks, block_size, Hkv, D].
+    block_table int32 [B, max_blocks]; context_lens int32 [B].  `workspace`
+    (a uint8 GPU tensor) is allocated by torch when not given."""
+    import torch
+    lib = load()
+    _dev(q, k_cache, v_cache, block_table, context_lens, workspace, out)
+    for n, t_ in (("q", q), ("k_cache", k_cache), ("v_cache", v_cache), ("block_table", block_table),
+                  ("context_lens", context_lens)):
+        _contig(n, t_)
+    B, Hq, D = q.shape
+    num_blocks, bs, Hkv, _ = k_cache.shape
+    need = opscale_attn_decode_workspace_size(B, Hq, D, max_context_len)
+    if workspace is None:
+        workspace = torch.empty(need, dtype=torch.uint8, device=q.device)
+    if out is None:
+        out = torch.empty_like(q)
+    t = Timing() if timed else None
+    _check(lib.opscale_attn_decode(_ptr(q), _ptr(k_cache), _ptr(v_cache), _ptr(block_table),
+                                   _ptr(context_lens), _ptr(out), B, Hq, Hkv, D, bs, block_table.shape[1],
+                                   num_blocks, max_context_len, scale, _dt(q), _ptr(workspace),
+                                   workspace.numel() * workspace.element_size(), _stream(stream),
+                                   ctypes.byref(t) if t else None))
+    return (out, t) if timed else out
+
+
+def opscale_op_profile(desc: OpDesc, warmup: int = 5, iters: int = 20, flush=None, stream=None) -> Profile:
+    """Profile one operator call described by `desc` (see make_desc_*)."""
+    lib = load()
+    p = Profile()
+    nbytes = 0 if flush is None else flush.numel() * flush.element_size()
+    _check(lib.opscale_op_profile(ctypes.byref(desc), warmup, iters, _ptr(flush), nbytes,
+                                  _stream(stream), ctypes.byref(p)))
+    return p
+
+
+# descriptor builders (keep the tensors alive while the descriptor is used)
+def desc_rmsnorm(x, w, y, eps=1e-5) -> OpDesc:
+    d = OpDesc(op=OP_RMSNORM, dt=_dt(x))
+    H = x.shape[-1]
+    d.u.rmsnorm = _RmsnormArgs(_ptr(x), _ptr(w), _ptr(y), x.numel() // H, H, eps)
+    return d
+
+
+def desc_linear(x, W, y, bias=None) -> OpDesc:
+    d = OpDesc(op=OP_LINEAR, dt=_dt(x))
+    K = x.shape[-1]
+    d.u.linear = _LinearArgs(_ptr(x), _ptr(W), _ptr(bias), _ptr(y), x.numel() // K, W.shape[0], K)
+    return d
+
+
+def desc_swiglu(gate_up, out) -> OpDesc:
+    d = OpDesc(op=OP_SWIGLU, dt=_dt(gate_up))
+    F = gate_up.shape[-1] // 2
+    d.u.swiglu = _SwigluArgs(_ptr(gate_up), _ptr(out), gate_up.numel() // (2 * F), F)
+    return d
+
+
+def desc_attn_prefill(q, k, v, out, cu_seqlens, max_seqlen, scale, causal=True) -> OpDesc:
+    d = OpDesc(op=OP_ATTN_PREFILL, dt=_dt(q))
+    T, Hq, D = q.shape
+    d.u.attn_prefill = _PrefillArgs(_ptr(q), _ptr(k), _ptr(v), q.stride(0), k.stride(0), _ptr(out),
+                                    _ptr(cu_seqlens), cu_seqlens.numel() - 1, T, max_seqlen, Hq,
+                                    k.shape[1], D, scale, int(causal))
+    return d
+
+
+def desc_attn_decode(q, k_cache, v_cache, block_table, context_lens, out, max_context_len, scale,
+                     workspace) -> OpDesc:
+    d = OpDesc(op=OP_ATTN_DECODE, dt=_dt(q))
+    B, Hq, D = q.shape
+    nb, bs, Hkv, _ = k_cache.shape
+    d.u.attn_decode = _DecodeArgs(_ptr(q), _ptr(k_cache), _ptr(v_cache), _ptr(block_table),
+                                  _ptr(context_lens), _ptr(out), B, Hq, Hkv, D, bs, block_table.shape[1],
+                                  nb, max_context_len, scale, _ptr(workspace),
+                                  workspace.numel() * workspace.element_size())
+    return d

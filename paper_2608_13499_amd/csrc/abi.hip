@@ -1,0 +1,515 @@
+// C ABI of libopscale: argument validation, dispatch to the gfx950 kernels,
+// kernel-only timing with device events and the per-operator profile.
+#include <algorithm>
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <functional>
+#include <string>
+#include <vector>
+
+#include "launch.h"
+#include "opscale.h"
+
+namespace {
+
+thread_local std::string g_last_error;
+
+opscale_status fail(opscale_status st, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof(buf), fmt, ap);
+  va_end(ap);
+  g_last_error = buf;
+  return st;
+}
+
+opscale_status hip_fail(hipError_t e, const char* what) {
+  return fail(OPSCALE_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+int esize(opscale_dtype dt) { return dt == OPSCALE_BF16 ? 2 : 4; }
+
+bool dtype_ok(opscale_dtype dt) { return dt == OPSCALE_F32 || dt == OPSCALE_BF16; }
+
+// [a, a+na) and [b, b+nb) overlap?
+bool overlap(const void* a, int64_t na, const void* b, int64_t nb) {
+  const uintptr_t x = reinterpret_cast<uintptr_t>(a), y = reinterpret_cast<uintptr_t>(b);
+  return x < y + (uintptr_t)nb && y < x + (uintptr_t)na;
+}
+
+constexpr int64_t kMaxDim = (int64_t)1 << 31;
+
+// Events used to time one call on this host thread (created on first use).
+struct ThreadEvents {
+  hipEvent_t start = nullptr, stop = nullptr;
+  hipError_t init() {
+    if (start) return hipSuccess;
+    hipError_t e = hipEventCreate(&start);
+    if (e != hipSuccess) return e;
+    e = hipEventCreate(&stop);
+    if (e != hipSuccess) {
+      (void)hipEventDestroy(start);
+      start = nullptr;
+    }
+    return e;
+  }
+};
+thread_local ThreadEvents g_events;
+
+// Runs `launch` on `s`, bracketed by events when `t` is non-null.
+template <class F>
+opscale_status run_timed(hipStream_t s, opscale_timing* t, const char* what, F&& launch) {
+  if (t) {
+    hipError_t e = g_events.init();
+    if (e != hipSuccess) return hip_fail(e, "hipEventCreate");
+    e = hipEventRecord(g_events.start, s);
+    if (e != hipSuccess) return hip_fail(e, "hipEventRecord");
+  }
+  hipError_t e = launch();
+  if (e != hipSuccess) return hip_fail(e, what);
+  if (t) {
+    e = hipEventRecord(g_events.stop, s);
+    if (e != hipSuccess) return hip_fail(e, "hipEventRecord");
+    e = hipEventSynchronize(g_events.stop);
+    if (e != hipSuccess) return hip_fail(e, "hipEventSynchronize");
+    float ms = 0.f;
+    e = hipEventElapsedTime(&ms, g_events.start, g_events.stop);
+    if (e != hipSuccess) return hip_fail(e, "hipEventElapsedTime");
+    t->elapsed_us = ms * 1000.f;
+  }
+  return OPSCALE_OK;
+}
+
+void zero_timing(opscale_timing* t) {
+  if (t) *t = opscale_timing{0.f, 0.0, 0.0};
+}
+
+// ------------------------------------------------------ algorithmic work ----
+struct Work {
+  double flops, bytes;
+  int64_t weight, transient, io;
+};
+
+Work work_rmsnorm(int64_t M, int64_t H, int s) {
+  return {4.0 * M * H, (double)s * (2.0 * M * H + H), s * H, s * 2 * M * H, s * M * H};
+}
+Work work_linear(int64_t M, int64_t N, int64_t K, int s, bool bias) {
+  const double by = (double)s * ((double)M * K + (double)N * K + (double)M * N) + (bias ? (double)s * N : 0.0);
+  return {2.0 * M * N * K, by, s * (N * K + (bias ? N : 0)), s * (M * K + M * N), s * M * N};
+}
+Work work_swiglu(int64_t M, int64_t F, int s) {
+  return {6.0 * M * F, 3.0 * s * M * F, 0, 3 * s * M * F, s * M * F};
+}
+Work work_prefill(const std::vector<int32_t>& cu, int64_t Hq, int64_t Hkv, int64_t D, int s, bool causal) {
+  double pairs = 0;
+  for (size_t b = 0; b + 1 < cu.size(); ++b) {
+    const double L = (double)(cu[b + 1] - cu[b]);
+    pairs += causal ? L * (L + 1) / 2 : L * L;
+  }
+  const int64_t T = cu.empty() ? 0 : cu.back();
+  const int64_t tb = (int64_t)s * (2 * T * Hq * D + 2 * T * Hkv * D);
+  return {4.0 * D * Hq * pairs, (double)tb, 0, tb, (int64_t)s * T * Hq * D};
+}
+Work work_decode(const std::vector<int32_t>& ctx, int64_t Hq, int64_t Hkv, int64_t D, int s, int64_t bs,
+                 int64_t max_blocks) {
+  double N = 0, nb = 0;
+  const int64_t B = (int64_t)ctx.size();
+  for (int32_t c : ctx) {
+    const int64_t n = std::min<int64_t>(std::max<int32_t>(c, 0), max_blocks * bs);
+    N += n;
+    nb += (double)((n + bs - 1) / bs);
+  }
+  const double by = s * (2.0 * Hkv * D * N + 2.0 * B * Hq * D) + 4.0 * (nb + B);
+  return {4.0 * D * Hq * N, by, 0, (int64_t)by, s * B * Hq * D};
+}
+
+opscale_status copy_ints(std::vector<int32_t>& dst, const int32_t* src, int64_t n, hipStream_t s) {
+  dst.resize((size_t)n);
+  if (n == 0) return OPSCALE_OK;
+  hipError_t e = hipMemcpyAsync(dst.data(), src, (size_t)n * 4, hipMemcpyDeviceToHost, s);
+  if (e == hipSuccess) e = hipStreamSynchronize(s);
+  return e == hipSuccess ? OPSCALE_OK : hip_fail(e, "hipMemcpyAsync(lengths)");
+}
+
+// ------------------------------------------------------------ validation ----
+opscale_status check_rmsnorm(const void* x, const void* w, void* y, int64_t M, int64_t H,
+                             float eps, opscale_dtype dt) {
+  if (!dtype_ok(dt)) return fail(OPSCALE_ERR_INVALID_ARG, "rmsnorm: unknown dtype %d", (int)dt);
+  if (M < 0 || H <= 0 || M >= kMaxDim || H > (1 << 24))
+    return fail(OPSCALE_ERR_INVALID_ARG, "rmsnorm: bad sizes M=%lld H=%lld", (long long)M, (long long)H);
+  if ((H * esize(dt)) % 16)
+    return fail(OPSCALE_ERR_INVALID_ARG, "rmsnorm: H*sizeof(dt)=%lld is not a multiple of 16",
+                (long long)(H * esize(dt)));
+  if (!(eps >= 0.f) || std::isinf(eps)) return fail(OPSCALE_ERR_INVALID_ARG, "rmsnorm: eps must be finite and >= 0");
+  if (M == 0) return OPSCALE_OK;
+  if (!x || !w || !y) return fail(OPSCALE_ERR_INVALID_ARG, "rmsnorm: null pointer");
+  if (!aligned16(x) || !aligned16(w) || !aligned16(y))
+    return fail(OPSCALE_ERR_INVALID_ARG, "rmsnorm: pointers must be 16-byte aligned");
+  const int64_t nb = M * H * esize(dt);
+  if (x != y && overlap(x, nb, y, nb))
+    return fail(OPSCALE_ERR_INVALID_ARG, "rmsnorm: y partially overlaps x (only y == x is allowed)");
+  return OPSCALE_OK;
+}
+
+opscale_status check_linear(const void* x, const void* W, const void* bias, void* y, int64_t M,
+                            int64_t N, int64_t K, opscale_dtype dt) {
+  if (!dtype_ok(dt)) return fail(OPSCALE_ERR_INVALID_ARG, "linear: unknown dtype %d", (int)dt);
+  if (M < 0 || N <= 0 || K <= 0 || M >= kMaxDim || N >= kMaxDim || K > (1 << 20))
+    return fail(OPSCALE_ERR_INVALID_ARG, "linear: bad sizes M=%lld N=%lld K=%lld", (long long)M,
+                (long long)N, (long long)K);
+  const int s = esize(dt);
+  if ((K * s) % 16 || (N * s) % 16)
+    return fail(OPSCALE_ERR_INVALID_ARG, "linear: K and N times sizeof(dt) must be multiples of 16 (K=%lld N=%lld)",
+                (long long)K, (long long)N);
+  if (M == 0) return OPSCALE_OK;
+  if (!x || !W || !y) return fail(OPSCALE_ERR_INVALID_ARG, "linear: null pointer");
+  if (!aligned16(x) || !aligned16(W) || !aligned16(y) || (bias && !aligned16(bias)))
+    return fail(OPSCALE_ERR_INVALID_ARG, "linear: pointers must be 16-byte aligned");
+  if (overlap(y, M * N * s, x, M * K * s) || overlap(y, M * N * s, W, N * K * s))
+    return fail(OPSCALE_ERR_INVALID_ARG, "linear: y must not overlap x or W");
+  return OPSCALE_OK;
+}
+
+opscale_status check_swiglu(const void* gu, void* out, int64_t M, int64_t F, opscale_dtype dt) {
+  if (!dtype_ok(dt)) return fail(OPSCALE_ERR_INVALID_ARG, "swiglu: unknown dtype %d", (int)dt);
+  if (M < 0 || F <= 0 || M >= kMaxDim || F >= kMaxDim)
+    return fail(OPSCALE_ERR_INVALID_ARG, "swiglu: bad sizes M=%lld F=%lld", (long long)M, (long long)F);
+  const int s = esize(dt);
+  if ((F * s) % 16)
+    return fail(OPSCALE_ERR_INVALID_ARG, "swiglu: F*sizeof(dt)=%lld is not a multiple of 16", (long long)(F * s));
+  if (M == 0) return OPSCALE_OK;
+  if (!gu || !out) return fail(OPSCALE_ERR_INVALID_ARG, "swiglu: null pointer");
+  if (!aligned16(gu) || !aligned16(out)) return fail(OPSCALE_ERR_INVALID_ARG, "swiglu: pointers must be 16-byte aligned");
+  if (overlap(gu, M * 2 * F * s, out, M * F * s))
+    return fail(OPSCALE_ERR_INVALID_ARG, "swiglu: out must not overlap gate_up");
+  return OPSCALE_OK;
+}
+
+opscale_status check_prefill(const void* q, const void* k, const void* v, int64_t qs, int64_t kvs,
+                             void* o, const int32_t* cu, int32_t B, int64_t T, int32_t max_seqlen,
+                             int32_t Hq, int32_t Hkv, int32_t D, float scale, opscale_dtype dt) {
+  if (!dtype_ok(dt)) return fail(OPSCALE_ERR_INVALID_ARG, "attn_prefill: unknown dtype %d", (int)dt);
+  if (B < 0 || T < 0 || T >= kMaxDim || Hq <= 0 || Hkv <= 0)
+    return fail(OPSCALE_ERR_INVALID_ARG, "attn_prefill: bad sizes B=%d T=%lld Hq=%d Hkv=%d", B, (long long)T, Hq, Hkv);
+  if (Hq % Hkv) return fail(OPSCALE_ERR_INVALID_ARG, "attn_prefill: Hkv=%d does not divide Hq=%d", Hkv, Hq);
+  if (D != 64 && D != 128) return fail(OPSCALE_ERR_UNSUPPORTED, "attn_prefill: head_dim %d (supported: 64, 128)", D);
+  if (!std::isfinite(scale)) return fail(OPSCALE_ERR_INVALID_ARG, "attn_prefill: scale must be finite");
+  if (B == 0 || T == 0) return OPSCALE_OK;
+  if (max_seqlen < 1) return fail(OPSCALE_ERR_INVALID_ARG, "attn_prefill: max_seqlen must be >= 1");
+  const int vec = 16 / esize(dt);
+  if (qs < (int64_t)Hq * D || kvs < (int64_t)Hkv * D || qs % vec || kvs % vec || qs > (1 << 24) || kvs > (1 << 24))
+    return fail(OPSCALE_ERR_INVALID_ARG, "attn_prefill: row strides q=%lld kv=%lld must cover the heads, be multiples of %d and <= 2^24",
+                (long long)qs, (long long)kvs, vec);
+  if (!q || !k || !v || !o || !cu) return fail(OPSCALE_ERR_INVALID_ARG, "attn_prefill: null pointer");
+  if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(o) || (reinterpret_cast<uintptr_t>(cu) & 3))
+    return fail(OPSCALE_ERR_INVALID_ARG, "attn_prefill: q, k, v, o must be 16-byte aligned, cu_seqlens 4-byte");
+  if ((int64_t)B * Hkv * Hq >= kMaxDim) return fail(OPSCALE_ERR_UNSUPPORTED, "attn_prefill: batch too large");
+  return OPSCALE_OK;
+}
+
+opscale_status check_decode(const void* q, const void* kc, const void* vc, const int32_t* table,
+                            const int32_t* ctx, void* o, int32_t B, int32_t Hq, int32_t Hkv, int32_t D,
+                            int32_t bs, int32_t max_blocks, int64_t num_blocks, int32_t max_ctx,
+                            float scale, opscale_dtype dt, void* ws, size_t ws_bytes) {
+  if (!dtype_ok(dt)) return fail(OPSCALE_ERR_INVALID_ARG, "attn_decode: unknown dtype %d", (int)dt);
+  if (B < 0 || Hq <= 0 || Hkv <= 0 || B > 65535 || Hq > 65535)
+    return fail(OPSCALE_ERR_INVALID_ARG, "attn_decode: bad sizes B=%d Hq=%d Hkv=%d", B, Hq, Hkv);
+  if (Hq % Hkv) return fail(OPSCALE_ERR_INVALID_ARG, "attn_decode: Hkv=%d does not divide Hq=%d", Hkv, Hq);
+  if (D != 64 && D != 128) return fail(OPSCALE_ERR_UNSUPPORTED, "attn_decode: head_dim %d (supported: 64, 128)", D);
+  const int G = Hq / Hkv;
+  if (dt == OPSCALE_BF16 && G != 1 && G != 2 && G != 4 && G != 8)
+    return fail(OPSCALE_ERR_UNSUPPORTED, "attn_decode: bf16 supports Hq/Hkv in {1, 2, 4, 8}, got %d", G);
+  if (bs < 1 || bs > 1024 || (bs & (bs - 1)))
+    return fail(OPSCALE_ERR_INVALID_ARG, "attn_decode: block_size %d must be a power of two in [1, 1024]", bs);
+  if (!std::isfinite(scale)) return fail(OPSCALE_ERR_INVALID_ARG, "attn_decode: scale must be finite");
+  if (B == 0) return OPSCALE_OK;
+  if (max_blocks < 1 || (int64_t)max_blocks * bs >= kMaxDim || num_blocks < 1 || max_ctx < 1)
+    return fail(OPSCALE_ERR_INVALID_ARG, "attn_decode: max_blocks_per_seq=%d num_blocks=%lld max_context_len=%d",
+                max_blocks, (long long)num_blocks, max_ctx);
+  if (!q || !kc || !vc || !table || !ctx || !o) return fail(OPSCALE_ERR_INVALID_ARG, "attn_decode: null pointer");
+  if (!aligned16(q) || !aligned16(kc) || !aligned16(vc) || !aligned16(o) ||
+      (reinterpret_cast<uintptr_t>(table) & 3) || (reinterpret_cast<uintptr_t>(ctx) & 3))
+    return fail(OPSCALE_ERR_INVALID_ARG, "attn_decode: tensors must be 16-byte aligned, indices 4-byte");
+  const size_t need = opscale::decode_workspace_bytes(B, Hq, D, max_ctx);
+  if (dt == OPSCALE_BF16 && (!ws || ws_bytes < need || !aligned16(ws)))
+    return fail(OPSCALE_ERR_WORKSPACE, "attn_decode: workspace of %zu bytes (16-byte aligned) needed, got %zu",
+                need, ws ? ws_bytes : (size_t)0);
+  return OPSCALE_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* opscale_version(void) { return "opscale 0.1.0 gfx950"; }
+
+const char* opscale_status_string(opscale_status s) {
+  switch (s) {
+    case OPSCALE_OK: return "ok";
+    case OPSCALE_ERR_INVALID_ARG: return "invalid argument";
+    case OPSCALE_ERR_UNSUPPORTED: return "unsupported";
+    case OPSCALE_ERR_WORKSPACE: return "workspace too small";
+    case OPSCALE_ERR_HIP: return "HIP error";
+  }
+  return "unknown status";
+}
+
+const char* opscale_last_error(void) { return g_last_error.c_str(); }
+
+opscale_status opscale_rmsnorm(const void* x, const void* w, void* y, int64_t M, int64_t H, float eps,
+                               opscale_dtype dt, hipStream_t stream, opscale_timing* timing) {
+  opscale_status st = check_rmsnorm(x, w, y, M, H, eps, dt);
+  if (st != OPSCALE_OK) return st;
+  zero_timing(timing);
+  if (M == 0) return OPSCALE_OK;
+  st = run_timed(stream, timing, "rmsnorm launch", [&] {
+    return opscale::launch_rmsnorm(x, w, y, M, H, eps, dt == OPSCALE_BF16, stream);
+  });
+  if (st == OPSCALE_OK && timing) {
+    const Work wk = work_rmsnorm(M, H, esize(dt));
+    timing->alg_flops = wk.flops;
+    timing->alg_bytes = wk.bytes;
+  }
+  return st;
+}
+
+opscale_status opscale_linear(const void* x, const void* W, const void* bias, void* y, int64_t M,
+                              int64_t N, int64_t K, opscale_dtype dt, hipStream_t stream,
+                              opscale_timing* timing) {
+  opscale_status st = check_linear(x, W, bias, y, M, N, K, dt);
+  if (st != OPSCALE_OK) return st;
+  zero_timing(timing);
+  if (M == 0) return OPSCALE_OK;
+  st = run_timed(stream, timing, "linear launch", [&] {
+    return opscale::launch_linear(x, W, bias, y, M, N, K, dt == OPSCALE_BF16, stream);
+  });
+  if (st == OPSCALE_OK && timing) {
+    const Work wk = work_linear(M, N, K, esize(dt), bias != nullptr);
+    timing->alg_flops = wk.flops;
+    timing->alg_bytes = wk.bytes;
+  }
+  return st;
+}
+
+opscale_status opscale_swiglu(const void* gate_up, void* out, int64_t M, int64_t F, opscale_dtype dt,
+                              hipStream_t stream, opscale_timing* timing) {
+  opscale_status st = check_swiglu(gate_up, out, M, F, dt);
+  if (st != OPSCALE_OK) return st;
+  zero_timing(timing);
+  if (M == 0) return OPSCALE_OK;
+  st = run_timed(stream, timing, "swiglu launch", [&] {
+    return opscale::launch_swiglu(gate_up, out, M, F, dt == OPSCALE_BF16, stream);
+  });
+  if (st == OPSCALE_OK && timing) {
+    const Work wk = work_swiglu(M, F, esize(dt));
+    timing->alg_flops = wk.flops;
+    timing->alg_bytes = wk.bytes;
+  }
+  return st;
+}
+
+opscale_status opscale_attn_prefill(const void* q, const void* k, const void* v, int64_t q_row_stride,
+                                    int64_t kv_row_stride, void* o, const int32_t* cu_seqlens,
+                                    int32_t B, int64_t total_tokens, int32_t max_seqlen, int32_t Hq,
+                                    int32_t Hkv, int32_t D, float scale, int32_t causal,
+                                    opscale_dtype dt, hipStream_t stream, opscale_timing* timing) {
+  opscale_status st = check_prefill(q, k, v, q_row_stride, kv_row_stride, o, cu_seqlens, B,
+                                    total_tokens, max_seqlen, Hq, Hkv, D, scale, dt);
+  if (st != OPSCALE_OK) return st;
+  zero_timing(timing);
+  if (B == 0 || total_tokens == 0) return OPSCALE_OK;
+  st = run_timed(stream, timing, "attn_prefill launch", [&] {
+    return opscale::launch_attn_prefill(q, k, v, q_row_stride, kv_row_stride, o, cu_seqlens, B,
+                                        total_tokens, max_seqlen, Hq, Hkv, D, scale, causal != 0,
+                                        dt == OPSCALE_BF16, stream);
+  });
+  if (st == OPSCALE_OK && timing) {
+    std::vector<int32_t> cu;
+    st = copy_ints(cu, cu_seqlens, (int64_t)B + 1, stream);
+    if (st != OPSCALE_OK) return st;
+    const Work wk = work_prefill(cu, Hq, Hkv, D, esize(dt), causal != 0);
+    timing->alg_flops = wk.flops;
+    timing->alg_bytes = wk.bytes;
+  }
+  return st;
+}
+
+size_t opscale_attn_decode_workspace_size(int32_t B, int32_t Hq, int32_t D, int32_t max_context_len) {
+  if (B <= 0 || Hq <= 0 || D <= 0) return 16;
+  return opscale::decode_workspace_bytes(B, Hq, D, std::max<int32_t>(1, max_context_len));
+}
+
+opscale_status opscale_attn_decode(const void* q, const void* k_cache, const void* v_cache,
+                                   const int32_t* block_table, const int32_t* context_lens, void* o,
+                                   int32_t B, int32_t Hq, int32_t Hkv, int32_t D, int32_t block_size,
+                                   int32_t max_blocks_per_seq, int64_t num_blocks,
+                                   int32_t max_context_len, float scale, opscale_dtype dt,
+                                   void* workspace, size_t workspace_bytes, hipStream_t stream,
+                                   opscale_timing* timing) {
+  opscale_status st = check_decode(q, k_cache, v_cache, block_table, context_lens, o, B, Hq, Hkv, D,
+                                   block_size, max_blocks_per_seq, num_blocks, max_context_len,
+                                   scale, dt, workspace, workspace_bytes);
+  if (st != OPSCALE_OK) return st;
+  zero_timing(timing);
+  if (B == 0) return OPSCALE_OK;
+  st = run_timed(stream, timing, "attn_decode launch", [&] {
+    return opscale::launch_attn_decode(q, k_cache, v_cache, block_table, context_lens, o, B, Hq, Hkv,
+                                       D, block_size, max_blocks_per_seq, num_blocks,
+                                       max_context_len, scale, dt == OPSCALE_BF16, workspace, stream);
+  });
+  if (st == OPSCALE_OK && timing) {
+    std::vector<int32_t> ctx;
+    st = copy_ints(ctx, context_lens, B, stream);
+    if (st != OPSCALE_OK) return st;
+    const Work wk = work_decode(ctx, Hq, Hkv, D, esize(dt), block_size, max_blocks_per_seq);
+    timing->alg_flops = wk.flops;
+    timing->alg_bytes = wk.bytes;
+  }
+  return st;
+}
+
+opscale_status opscale_op_profile(const opscale_op_desc* d, int32_t warmup, int32_t iters,
+                                  void* flush_buf, size_t flush_bytes, hipStream_t stream,
+                                  opscale_profile* out) {
+  if (!d || !out) return fail(OPSCALE_ERR_INVALID_ARG, "op_profile: null desc or out");
+  if (iters < 1 || warmup < 0) return fail(OPSCALE_ERR_INVALID_ARG, "op_profile: iters must be >= 1, warmup >= 0");
+  if (flush_buf && !aligned16(flush_buf)) return fail(OPSCALE_ERR_INVALID_ARG, "op_profile: flush_buf must be 16-byte aligned");
+  const opscale_dtype dt = d->dt;
+  // validate once, then launch without re-validation inside the loop
+  opscale_status st = OPSCALE_OK;
+  std::function<hipError_t()> launch;
+  Work wk{};
+  const bool bf16 = dt == OPSCALE_BF16;
+  switch (d->op) {
+    case OPSCALE_OP_RMSNORM: {
+      const auto& a = d->u.rmsnorm;
+      st = check_rmsnorm(a.x, a.w, a.y, a.M, a.H, a.eps, dt);
+      if (st != OPSCALE_OK) return st;
+      if (a.M == 0) return fail(OPSCALE_ERR_INVALID_ARG, "op_profile: empty problem");
+      launch = [=] { return opscale::launch_rmsnorm(a.x, a.w, a.y, a.M, a.H, a.eps, bf16, stream); };
+      wk = work_rmsnorm(a.M, a.H, esize(dt));
+      break;
+    }
+    case OPSCALE_OP_LINEAR: {
+      const auto& a = d->u.linear;
+      st = check_linear(a.x, a.W, a.bias, a.y, a.M, a.N, a.K, dt);
+      if (st != OPSCALE_OK) return st;
+      if (a.M == 0) return fail(OPSCALE_ERR_INVALID_ARG, "op_profile: empty problem");
+      launch = [=] { return opscale::launch_linear(a.x, a.W, a.bias, a.y, a.M, a.N, a.K, bf16, stream); };
+      wk = work_linear(a.M, a.N, a.K, esize(dt), a.bias != nullptr);
+      break;
+    }
+    case OPSCALE_OP_SWIGLU: {
+      const auto& a = d->u.swiglu;
+      st = check_swiglu(a.gate_up, a.out, a.M, a.F, dt);
+      if (st != OPSCALE_OK) return st;
+      if (a.M == 0) return fail(OPSCALE_ERR_INVALID_ARG, "op_profile: empty problem");
+      launch = [=] { return opscale::launch_swiglu(a.gate_up, a.out, a.M, a.F, bf16, stream); };
+      wk = work_swiglu(a.M, a.F, esize(dt));
+      break;
+    }
+    case OPSCALE_OP_ATTN_PREFILL: {
+      const auto& a = d->u.attn_prefill;
+      st = check_prefill(a.q, a.k, a.v, a.q_row_stride, a.kv_row_stride, a.o, a.cu_seqlens, a.B,
+                         a.total_tokens, a.max_seqlen, a.Hq, a.Hkv, a.D, a.scale, dt);
+      if (st != OPSCALE_OK) return st;
+      if (a.B == 0 || a.total_tokens == 0) return fail(OPSCALE_ERR_INVALID_ARG, "op_profile: empty problem");
+      launch = [=] {
+        return opscale::launch_attn_prefill(a.q, a.k, a.v, a.q_row_stride, a.kv_row_stride, a.o,
+                                            a.cu_seqlens, a.B, a.total_tokens, a.max_seqlen, a.Hq,
+                                            a.Hkv, a.D, a.scale, a.causal != 0, bf16, stream);
+      };
+      std::vector<int32_t> cu;
+      st = copy_ints(cu, a.cu_seqlens, (int64_t)a.B + 1, stream);
+      if (st != OPSCALE_OK) return st;
+      wk = work_prefill(cu, a.Hq, a.Hkv, a.D, esize(dt), a.causal != 0);
+      break;
+    }
+    case OPSCALE_OP_ATTN_DECODE: {
+      const auto& a = d->u.attn_decode;
+      st = check_decode(a.q, a.k_cache, a.v_cache, a.block_table, a.context_lens, a.o, a.B, a.Hq,
+                        a.Hkv, a.D, a.block_size, a.max_blocks_per_seq, a.num_blocks,
+                        a.max_context_len, a.scale, dt, a.workspace, a.workspace_bytes);
+      if (st != OPSCALE_OK) return st;
+      if (a.B == 0) return fail(OPSCALE_ERR_INVALID_ARG, "op_profile: empty problem");
+      launch = [=] {
+        return opscale::launch_attn_decode(a.q, a.k_cache, a.v_cache, a.block_table, a.context_lens,
+                                           a.o, a.B, a.Hq, a.Hkv, a.D, a.block_size,
+                                           a.max_blocks_per_seq, a.num_blocks, a.max_context_len,
+                                           a.scale, bf16, a.workspace, stream);
+      };
+      std::vector<int32_t> ctx;
+      st = copy_ints(ctx, a.context_lens, a.B, stream);
+      if (st != OPSCALE_OK) return st;
+      wk = work_decode(ctx, a.Hq, a.Hkv, a.D, esize(dt), a.block_size, a.max_blocks_per_seq);
+      break;
+    }
+    default:
+      return fail(OPSCALE_ERR_INVALID_ARG, "op_profile: unknown op %d", (int)d->op);
+  }
+  if (!dtype_ok(dt)) return fail(OPSCALE_ERR_INVALID_ARG, "op_profile: unknown dtype");
+
+  hipError_t e = g_events.init();
+  if (e != hipSuccess) return hip_fail(e, "hipEventCreate");
+  for (int i = 0; i < warmup; ++i) {
+    e = launch();
+    if (e != hipSuccess) return hip_fail(e, "op_profile warmup launch");
+  }
+  std::vector<float> us((size_t)iters);
+  for (int i = 0; i < iters; ++i) {
+    if (flush_buf && flush_bytes) {
+      e = opscale::launch_flush(flush_buf, flush_bytes, stream);
+      if (e != hipSuccess) return hip_fail(e, "op_profile flush");
+    }
+    if ((e = hipEventRecord(g_events.start, stream)) != hipSuccess) return hip_fail(e, "hipEventRecord");
+    if ((e = launch()) != hipSuccess) return hip_fail(e, "op_profile launch");
+    if ((e = hipEventRecord(g_events.stop, stream)) != hipSuccess) return hip_fail(e, "hipEventRecord");
+    if ((e = hipEventSynchronize(g_events.stop)) != hipSuccess) return hip_fail(e, "hipEventSynchronize");
+    float ms = 0.f;
+    if ((e = hipEventElapsedTime(&ms, g_events.start, g_events.stop)) != hipSuccess)
+      return hip_fail(e, "hipEventElapsedTime");
+    us[(size_t)i] = ms * 1000.f;
+  }
+  std::vector<float> sorted = us;
+  std::sort(sorted.begin(), sorted.end());
+  auto pct = [&](double p) {
+    const double pos = p * (double)(sorted.size() - 1);
+    const size_t lo = (size_t)std::floor(pos), hi = (size_t)std::ceil(pos);
+    return (float)(sorted[lo] + (sorted[hi] - sorted[lo]) * (pos - (double)lo));
+  };
+  double mean = 0;
+  for (float x : us) mean += x;
+  mean /= (double)us.size();
+
+  // MI355X peaks: bf16 dense matrix 2.5 PFLOP/s, fp32 matrix 157.3 TFLOP/s, HBM 8 TB/s.
+  const double peak_flops = bf16 ? 2.5e15 : 157.3e12;
+  const double peak_bw = 8.0e12;
+  const double t_s = (double)pct(0.5) * 1e-6;
+  opscale_profile p{};
+  p.iters = iters;
+  p.us_median = pct(0.5);
+  p.us_p10 = pct(0.1);
+  p.us_p90 = pct(0.9);
+  p.us_min = sorted.front();
+  p.us_mean = (float)mean;
+  p.alg_flops = wk.flops;
+  p.alg_bytes = wk.bytes;
+  p.tflops = t_s > 0 ? wk.flops / t_s * 1e-12 : 0.0;
+  p.gbps = t_s > 0 ? wk.bytes / t_s * 1e-9 : 0.0;
+  const double ai = wk.bytes > 0 ? wk.flops / wk.bytes : 0.0;
+  const double attainable = std::min(peak_flops, ai * peak_bw);
+  p.attainable_tflops = attainable * 1e-12;
+  p.roofline_frac = attainable > 0 && t_s > 0 ? (wk.flops / t_s) / attainable : 0.0;
+  p.bound = ai * peak_bw < peak_flops ? 1 : 0;
+  p.weight_bytes = wk.weight;
+  p.transient_bytes = wk.transient;
+  p.io_bytes = wk.io;
+  *out = p;
+  return OPSCALE_OK;
+}
+
+}  // extern "C"

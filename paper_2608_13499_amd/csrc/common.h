@@ -1,0 +1,78 @@
+// Device helpers shared by the gfx950 kernels of libopscale.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace opscale {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+
+#define OPS_LDS __attribute__((address_space(3)))
+
+// 0x00020000: raw buffer, 32-bit dword format, no swizzle (the CDNA value).
+constexpr int kBufferFlags = 0x00020000;
+// Any voffset >= num_records reads as zero; used to mask a lane's load.
+constexpr uint32_t kOobOffset = 0x80000000u;
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes, kBufferFlags);
+}
+
+__device__ __forceinline__ u32x4 buffer_load16(__amdgpu_buffer_rsrc_t r, uint32_t voff) {
+  return __builtin_amdgcn_raw_buffer_load_b128(r, voff, 0, 0);
+}
+
+// 16 bytes per lane straight into LDS at lds_wave_base + lane * 16.
+__device__ __forceinline__ void buffer_load16_lds(__amdgpu_buffer_rsrc_t r, OPS_LDS void* lds_wave_base,
+                                                  uint32_t voff) {
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(r, lds_wave_base, 16, voff, 0, 0, 0);
+}
+
+__device__ __forceinline__ float bf_lo(uint32_t u) { return __uint_as_float(u << 16); }
+__device__ __forceinline__ float bf_hi(uint32_t u) { return __uint_as_float(u & 0xffff0000u); }
+
+// Two floats -> packed bf16 pair (round to nearest even, v_cvt_pk_bf16_f32).
+__device__ __forceinline__ uint32_t pack_bf2(float a, float b) {
+  bf16x2 v;
+  v[0] = (__bf16)a;
+  v[1] = (__bf16)b;
+  return __builtin_bit_cast(uint32_t, v);
+}
+
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o, 64);
+  return v;
+}
+
+__device__ __forceinline__ float wave_max(float v) {
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, 64));
+  return v;
+}
+
+__device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
+
+// Wait for every outstanding vector-memory operation of this wave (including
+// buffer loads into LDS) before a barrier makes their data visible.
+__device__ __forceinline__ void wait_vmem() { __builtin_amdgcn_s_waitcnt(0); }
+
+// Block id -> tile id such that the consecutive tile ids land on one XCD.
+// Workgroups are dealt round-robin to the 8 XCDs, so block b runs on XCD
+// b % 8; giving each XCD a contiguous range of tiles keeps neighbouring tiles
+// (which share operand rows) in the same 4 MB L2.  A bijection for any count.
+__device__ __forceinline__ uint32_t xcd_remap(uint32_t bid, uint32_t total) {
+  constexpr uint32_t kXcd = 8;
+  const uint32_t per = total / kXcd, rem = total % kXcd;
+  const uint32_t x = bid % kXcd, i = bid / kXcd;
+  const uint32_t start = x < rem ? x * (per + 1) : rem * (per + 1) + (x - rem) * per;
+  return start + i;
+}
+
+}  // namespace opscale

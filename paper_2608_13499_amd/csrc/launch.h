@@ -1,0 +1,38 @@
+// Host-side launchers of the gfx950 kernels.  Arguments are validated by the
+// C ABI layer (abi.hip) before any of these is called; each launcher only
+// sizes the grid and enqueues on `s`, returning the launch status.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace opscale {
+
+hipError_t launch_rmsnorm(const void* x, const void* w, void* y, int64_t M, int64_t H, float eps,
+                          bool bf16, hipStream_t s);
+
+hipError_t launch_swiglu(const void* gu, void* out, int64_t M, int64_t F, bool bf16, hipStream_t s);
+
+hipError_t launch_linear(const void* x, const void* W, const void* bias, void* y, int64_t M,
+                         int64_t N, int64_t K, bool bf16, hipStream_t s);
+
+hipError_t launch_attn_prefill(const void* q, const void* k, const void* v, int64_t q_stride,
+                               int64_t kv_stride, void* o, const int32_t* cu, int32_t B,
+                               int64_t total_tokens, int32_t max_seqlen, int32_t Hq, int32_t Hkv,
+                               int32_t D, float scale, bool causal, bool bf16, hipStream_t s);
+
+// Split-KV decode: number of key-range splits the launch uses per sequence.
+int32_t decode_max_splits(int32_t max_context_len);
+size_t decode_workspace_bytes(int32_t B, int32_t Hq, int32_t D, int32_t max_context_len);
+
+hipError_t launch_attn_decode(const void* q, const void* kc, const void* vc, const int32_t* table,
+                              const int32_t* ctx, void* o, int32_t B, int32_t Hq, int32_t Hkv,
+                              int32_t D, int32_t block_size, int32_t max_blocks, int64_t num_blocks,
+                              int32_t max_context_len, float scale, bool bf16, void* ws,
+                              hipStream_t s);
+
+// Writes a fixed pattern over `bytes` of `buf` (evicts the last-level cache
+// before a timed iteration).
+hipError_t launch_flush(void* buf, size_t bytes, hipStream_t s);
+
+}  // namespace opscale

@@ -1,0 +1,122 @@
+"""Host-side checks of the C ABI that need no GPU: the library loads, exports
+every symbol include/opscale.h declares, and rejects bad arguments with the
+documented status codes before touching the device."""
+import ctypes
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "opscale.h")
+
+
+def _declared():
+    src = open(HEADER).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(opscale_[a-z_]+)\s*\(", src)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    import paper_2608_13499_amd as ops
+    return ops.load()
+
+
+def test_header_declares_expected_entry_points():
+    d = _declared()
+    for name in ("opscale_rmsnorm", "opscale_linear", "opscale_swiglu", "opscale_attn_prefill",
+                 "opscale_attn_decode", "opscale_attn_decode_workspace_size", "opscale_op_profile",
+                 "opscale_version", "opscale_status_string", "opscale_last_error"):
+        assert name in d
+
+
+def test_library_exports_every_declared_symbol(lib):
+    for name in _declared():
+        assert hasattr(lib, name), name
+    import paper_2608_13499_amd as ops
+    assert set(_declared()) <= set(ops.EXPORTS)
+
+
+def test_version_and_status_strings(lib):
+    assert b"gfx950" in lib.opscale_version()
+    assert lib.opscale_status_string(0) == b"ok"
+    assert lib.opscale_status_string(3) == b"workspace too small"
+
+
+P = ctypes.c_void_p
+A16 = 1 << 20  # a 16-byte aligned fake address: never dereferenced, validation fails first
+
+
+def _err(lib):
+    return lib.opscale_last_error().decode()
+
+
+def test_rmsnorm_validation(lib):
+    assert lib.opscale_rmsnorm(None, None, None, 4, 4096, 1e-5, 1, None, None) == 1
+    assert "null" in _err(lib)
+    assert lib.opscale_rmsnorm(A16, A16, A16 * 2, 4, 4095, 1e-5, 1, None, None) == 1  # H*2 % 16
+    assert lib.opscale_rmsnorm(A16 + 2, A16, A16 * 4, 4, 4096, 1e-5, 1, None, None) == 1  # misaligned
+    assert lib.opscale_rmsnorm(A16, A16, A16 * 4, -1, 4096, 1e-5, 1, None, None) == 1
+    assert lib.opscale_rmsnorm(A16, A16, A16 * 4, 4, 4096, -1.0, 1, None, None) == 1
+    assert lib.opscale_rmsnorm(A16, A16, A16 * 4, 4, 4096, 1e-5, 7, None, None) == 1  # dtype
+    assert lib.opscale_rmsnorm(A16, A16, A16 + 16, 4, 4096, 1e-5, 1, None, None) == 1  # partial overlap
+    assert "overlap" in _err(lib)
+    assert lib.opscale_rmsnorm(None, None, None, 0, 4096, 1e-5, 1, None, None) == 0  # empty: no-op
+
+
+def test_linear_validation(lib):
+    assert lib.opscale_linear(A16, A16 * 2, None, A16 * 4, 8, 256, 100, 1, None, None) == 1  # K*2 % 16
+    assert lib.opscale_linear(A16, A16 * 2, None, A16 * 4, 8, 12, 64, 1, None, None) == 1  # N*2 % 16
+    assert lib.opscale_linear(A16, A16 * 2, None, A16, 8, 256, 64, 1, None, None) == 1  # y aliases x
+    assert lib.opscale_linear(A16, None, None, A16 * 4, 8, 256, 64, 1, None, None) == 1
+    assert lib.opscale_linear(A16, A16 * 2, A16 + 4, A16 * 4, 8, 256, 64, 1, None, None) == 1  # bias align
+    assert lib.opscale_linear(None, None, None, None, 0, 256, 64, 1, None, None) == 0
+
+
+def test_swiglu_validation(lib):
+    assert lib.opscale_swiglu(A16, A16, 8, 256, 1, None, None) == 1  # out overlaps input
+    assert lib.opscale_swiglu(A16, A16 * 64, 8, 3, 0, None, None) == 1  # F*4 % 16
+    assert lib.opscale_swiglu(None, None, 0, 256, 1, None, None) == 0
+
+
+def test_prefill_validation(lib):
+    f = lib.opscale_attn_prefill
+    ok = dict(q=A16, k=A16, v=A16, qs=48 * 128, kvs=48 * 128, o=A16 * 8, cu=A16 * 16, B=2, T=100, ms=64,
+              Hq=32, Hkv=8, D=128, scale=0.08, causal=1, dt=1)
+
+    def call(**kw):
+        a = dict(ok, **kw)
+        return f(a["q"], a["k"], a["v"], a["qs"], a["kvs"], a["o"], a["cu"], a["B"], a["T"], a["ms"], a["Hq"],
+                 a["Hkv"], a["D"], a["scale"], a["causal"], a["dt"], None, None)
+
+    assert call(Hkv=5) == 1                # Hkv does not divide Hq
+    assert call(D=96) == 2                 # unsupported head dim
+    assert call(qs=100) == 1               # stride smaller than the heads
+    assert call(ms=0) == 1
+    assert call(cu=None) == 1
+    assert call(scale=float("nan")) == 1
+    assert call(q=A16 + 8) == 1            # misaligned
+    assert call(T=0) == 0 and call(B=0) == 0
+
+
+def test_decode_validation_and_workspace(lib):
+    f = lib.opscale_attn_decode
+    need = lib.opscale_attn_decode_workspace_size(256, 32, 128, 8192)
+    assert need == 4 * 256 * 32 * 16 * 130
+    ok = dict(q=A16, kc=A16, vc=A16, tab=A16, ctx=A16, o=A16 * 8, B=256, Hq=32, Hkv=8, D=128, bs=16, mb=512,
+              nb=69424, mc=8192, scale=0.08, dt=1, ws=A16 * 32, wsb=need)
+
+    def call(**kw):
+        a = dict(ok, **kw)
+        return f(a["q"], a["kc"], a["vc"], a["tab"], a["ctx"], a["o"], a["B"], a["Hq"], a["Hkv"], a["D"], a["bs"],
+                 a["mb"], a["nb"], a["mc"], a["scale"], a["dt"], a["ws"], a["wsb"], None, None)
+
+    assert call(wsb=need - 1) == 3
+    assert call(ws=None) == 3
+    assert call(bs=12) == 1                # not a power of two
+    assert call(Hq=24, Hkv=8) == 2         # group of 3 unsupported on the bf16 path
+    assert call(D=256) == 2
+    assert call(tab=None) == 1
+    assert call(mb=0) == 1
+    assert call(B=0) == 0

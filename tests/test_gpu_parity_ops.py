@@ -1,0 +1,200 @@
+"""GPU parity of every operator against the fp64 oracle, at sizes the oracle
+evaluates in full: the tiny fp32 decoder layer (tolerance 1e-5) and bf16 shapes
+that span several kernel tiles with ragged tails in every dimension
+(tolerance 2e-2), plus the degenerate cases (single row, single key, empty
+prompts, zero-length contexts, invalid page ids).  All calls go through the C
+ABI via the ctypes binding."""
+import math
+
+import numpy as np
+import pytest
+
+import oracle
+import workloads as wl
+from parity_util import assert_close, cuda, f64, gen, say, torch_dtype
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def ops():
+    import torch
+    assert torch.cuda.is_available()
+    import paper_2608_13499_amd as ops
+    ops.load()
+    return ops
+
+
+# ------------------------------------------------------------------ RMSNorm --
+@pytest.mark.parametrize("dtype,M,H", [
+    ("f32", 128, 256), ("f32", 5, 4), ("bf16", 37, 4096), ("bf16", 3, 8192),
+    ("bf16", 9, 24), ("bf16", 2, 24576), ("bf16", 1, 4096), ("f32", 7, 16384 + 4),
+])
+def test_rmsnorm(ops, dtype, M, H):
+    import torch
+    say(f"rmsnorm {dtype} M={M} H={H}")
+    x = gen(11, "x", (M, H), dtype)
+    w = gen(11, "w_norm", (H,), dtype, std=0.02, mean=1.0)
+    y = ops.opscale_rmsnorm(cuda(x), cuda(w), eps=1e-5)
+    torch.cuda.synchronize()
+    assert_close(f64(y.cpu()), oracle.rmsnorm(f64(x), f64(w), 1e-5), dtype, "rmsnorm")
+
+
+def test_rmsnorm_inplace_and_unit_gain(ops):
+    import torch
+    x = gen(12, "x", (64, 4096), "bf16")
+    xd = cuda(x)
+    ops.opscale_rmsnorm(xd, cuda(torch.ones(4096, dtype=torch.bfloat16)), y=xd, eps=0.0)
+    torch.cuda.synchronize()
+    y = f64(xd.cpu())
+    # unit gain, eps 0: every row has RMS 1 up to bf16 output rounding
+    rms = np.sqrt(np.mean(y * y, axis=1))
+    assert np.abs(rms - 1).max() < 4e-3
+    assert_close(y, oracle.rmsnorm(f64(x), np.ones(4096), 0.0), "bf16", "in-place rmsnorm")
+
+
+# ------------------------------------------------------------------- linear --
+@pytest.mark.parametrize("dtype,M,N,K,bias", [
+    ("f32", 128, 768, 256, False), ("f32", 128, 256, 256, False), ("f32", 128, 1376, 256, False),
+    ("f32", 128, 256, 688, False), ("f32", 3, 12, 20, True),
+    ("bf16", 300, 264, 200, False), ("bf16", 513, 1024, 4096, False), ("bf16", 1, 256, 64, False),
+    ("bf16", 257, 520, 136, True), ("bf16", 64, 6144, 4096, False), ("bf16", 40, 256, 14336, False),
+    ("bf16", 1000, 768, 8, False),
+])
+def test_linear(ops, dtype, M, N, K, bias):
+    import torch
+    say(f"linear {dtype} M={M} N={N} K={K} bias={bias}")
+    x = gen(21, "x", (M, K), dtype)
+    W = gen(21, "w_qkv", (N, K), dtype, std=0.02)
+    b = gen(21, "bias", (N,), dtype) if bias else None
+    y = ops.opscale_linear(cuda(x), cuda(W), None if b is None else cuda(b))
+    torch.cuda.synchronize()
+    assert_close(f64(y.cpu()), oracle.linear(f64(x), f64(W), None if b is None else f64(b)), dtype, "linear")
+
+
+def test_linear_identity_weight(ops):
+    """W = I (bf16-exact) returns x exactly: no accumulation rounding occurs."""
+    import torch
+    x = gen(22, "x", (300, 512), "bf16")
+    W = torch.eye(512, dtype=torch.bfloat16)
+    y = ops.opscale_linear(cuda(x), cuda(W))
+    torch.cuda.synchronize()
+    assert torch.equal(y.cpu(), x)
+
+
+# ------------------------------------------------------------------- SwiGLU --
+@pytest.mark.parametrize("dtype,M,F", [("f32", 128, 688), ("bf16", 33, 1000), ("bf16", 1, 14336),
+                                       ("bf16", 700, 8), ("f32", 3, 4)])
+def test_swiglu(ops, dtype, M, F):
+    import torch
+    say(f"swiglu {dtype} M={M} F={F}")
+    u = gen(31, "gate_up", (M, 2 * F), dtype, std=3.0)
+    out = ops.opscale_swiglu(cuda(u))
+    torch.cuda.synchronize()
+    assert_close(f64(out.cpu()), oracle.swiglu(f64(u)), dtype, "swiglu")
+
+
+# -------------------------------------------------------- prefill attention --
+def _prefill_case(ops, dtype, lens, Hq, Hkv, D, causal, packed, seed=41):
+    import torch
+    lens = np.asarray(lens, np.int64)
+    cu = wl.cu_seqlens(lens)
+    T = int(cu[-1])
+    if packed:  # views into one [T, (Hq + 2 Hkv) D] tensor, as after the QKV linear
+        qkv = gen(seed, "q", (T, (Hq + 2 * Hkv) * D), dtype)
+        qd = cuda(qkv)
+        q = qd[:, : Hq * D].view(T, Hq, D)
+        k = qd[:, Hq * D:(Hq + Hkv) * D].view(T, Hkv, D)
+        v = qd[:, (Hq + Hkv) * D:].view(T, Hkv, D)
+        qh = f64(qkv[:, : Hq * D]).reshape(T, Hq, D)
+        kh = f64(qkv[:, Hq * D:(Hq + Hkv) * D]).reshape(T, Hkv, D)
+        vh = f64(qkv[:, (Hq + Hkv) * D:]).reshape(T, Hkv, D)
+    else:
+        qc, kc, vc = (gen(seed, "q", (T, Hq, D), dtype), gen(seed, "k", (T, Hkv, D), dtype),
+                      gen(seed, "v", (T, Hkv, D), dtype))
+        q, k, v = cuda(qc), cuda(kc), cuda(vc)
+        qh, kh, vh = f64(qc), f64(kc), f64(vc)
+    scale = 1.0 / math.sqrt(D)
+    out = ops.opscale_attn_prefill(q, k, v, cuda(torch.from_numpy(cu)), int(max(1, lens.max())), scale,
+                                   causal)
+    torch.cuda.synchronize()
+    ref = oracle.attn_prefill(qh, kh, vh, cu, scale, causal)
+    return f64(out.cpu()), ref
+
+
+@pytest.mark.parametrize("dtype,lens,Hq,Hkv,D,causal,packed", [
+    ("f32", [128], 4, 4, 64, True, False),
+    ("f32", [5, 70, 0, 1], 4, 2, 128, True, True),
+    ("f32", [33, 7], 2, 1, 64, False, False),
+    ("bf16", [1, 17, 64, 65, 130, 0, 300], 8, 2, 128, True, False),
+    ("bf16", [128, 40, 1], 4, 4, 64, True, False),
+    ("bf16", [200, 31, 97], 16, 2, 128, True, True),
+    ("bf16", [77, 3, 150], 6, 2, 128, True, False),
+    ("bf16", [100, 1, 64], 8, 2, 128, False, False),
+    ("bf16", [513], 2, 2, 64, True, True),
+])
+def test_attn_prefill(ops, dtype, lens, Hq, Hkv, D, causal, packed):
+    say(f"attn_prefill {dtype} lens={lens} Hq={Hq} Hkv={Hkv} D={D} causal={causal} packed={packed}")
+    got, ref = _prefill_case(ops, dtype, lens, Hq, Hkv, D, causal, packed)
+    assert_close(got, ref, dtype, "attn_prefill")
+
+
+def test_attn_prefill_single_key_returns_v(ops):
+    """Prompts of length 1: softmax over one key is exactly 1, output == v."""
+    import torch
+    lens = [1] * 9
+    cu = wl.cu_seqlens(lens)
+    q = gen(42, "q", (9, 8, 128), "bf16")
+    k = gen(42, "k", (9, 2, 128), "bf16")
+    v = gen(42, "v", (9, 2, 128), "bf16")
+    out = ops.opscale_attn_prefill(cuda(q), cuda(k), cuda(v), cuda(torch.from_numpy(cu)), 1, 0.088)
+    torch.cuda.synchronize()
+    exp = v.repeat_interleave(4, dim=1)
+    assert torch.equal(out.cpu(), exp)
+
+
+# --------------------------------------------------------- decode attention --
+def _decode_case(ops, dtype, ctx, Hq, Hkv, D, bs, seed=51, bad_block=False):
+    import torch
+    ctx = np.asarray(ctx, np.int64)
+    rng = wl.rng_for(seed, "block_table")
+    table, nb = wl.paged_cache_layout(ctx, bs, rng, extra_blocks=3)
+    if bad_block:
+        table[0, 0] = nb + 5  # out of range: reads as zeros
+    kc = gen(seed, "k_cache", (nb, bs, Hkv, D), dtype)
+    vc = gen(seed, "v_cache", (nb, bs, Hkv, D), dtype)
+    q = gen(seed, "q", (len(ctx), Hq, D), dtype)
+    scale = 1.0 / math.sqrt(D)
+    maxc = int(max(1, ctx.max()))
+    out = ops.opscale_attn_decode(cuda(q), cuda(kc), cuda(vc), cuda(torch.from_numpy(table)),
+                                  cuda(torch.from_numpy(ctx.astype(np.int32))), maxc, scale)
+    torch.cuda.synchronize()
+    kh, vh = f64(kc), f64(vc)
+    if bad_block:
+        kh = np.concatenate([kh, np.zeros((6,) + kh.shape[1:])])
+        vh = np.concatenate([vh, np.zeros((6,) + vh.shape[1:])])
+    ref = oracle.attn_decode(f64(q), kh, vh, table, ctx, scale)
+    return f64(out.cpu()), ref
+
+
+@pytest.mark.parametrize("dtype,ctx,Hq,Hkv,D,bs", [
+    ("f32", [1, 16, 17, 600, 0], 8, 2, 128, 16),
+    ("f32", [37, 5], 4, 4, 64, 8),
+    ("bf16", [1, 16, 17, 600, 0], 8, 2, 128, 16),
+    ("bf16", [1030, 2, 513, 9], 32, 8, 128, 16),
+    ("bf16", [40, 300], 4, 4, 64, 16),
+    ("bf16", [129, 2049, 31], 16, 2, 128, 32),
+    ("bf16", [100, 7], 4, 2, 128, 1),
+    ("bf16", [4000, 64], 16, 8, 64, 256),
+])
+def test_attn_decode(ops, dtype, ctx, Hq, Hkv, D, bs):
+    say(f"attn_decode {dtype} ctx={ctx} Hq={Hq} Hkv={Hkv} D={D} bs={bs}")
+    got, ref = _decode_case(ops, dtype, ctx, Hq, Hkv, D, bs)
+    assert_close(got, ref, dtype, "attn_decode")
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_attn_decode_invalid_block_reads_zero(ops, dtype):
+    say(f"attn_decode invalid block id {dtype}")
+    got, ref = _decode_case(ops, dtype, [40, 20], 8, 2, 128, 16, bad_block=True)
+    assert_close(got, ref, dtype, "attn_decode bad block")

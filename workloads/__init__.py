@@ -177,3 +177,64 @@ def pick_rows(rng: np.random.Generator, m: int, count: int) -> np.ndarray:
         return np.arange(m, dtype=np.int64)
     r = rng.choice(m, size=count, replace=False)
     return np.unique(np.concatenate([r, [0, m - 1]])).astype(np.int64)
+
+
+def device_normal(shape, seed: int, tag: str, dtype: str, std: float = 1.0, mean: float = 0.0,
+                  device: str = "cuda"):
+    """Seeded normal tensor drawn on the GPU with torch's Philox generator, for
+    full-size workloads whose host generation would be slow.  Deterministic for
+    a given (seed, tag).  The draws differ from `normal`'s; tests that need the
+    values on the host copy the rows they check."""
+    import torch
+    g = torch.Generator(device=device)
+    g.manual_seed(int(seed) * 1000003 + TAG[tag])
+    dt = torch.bfloat16 if dtype == "bf16" else torch.float32
+    t = torch.empty(shape, dtype=torch.float32, device=device)
+    t.normal_(mean=mean, std=std, generator=g)
+    return t.to(dt)
+
+
+def prefill_layer_inputs(cfg: LayerConfig, device: str = "cuda"):
+    """Full-size inputs of one prefill layer on the GPU: the activation x
+    [M, H], the layer weights (nn.Linear layout [out, in]) and cu_seqlens.
+    Weights N(0, 0.02); norm gains 1 + N(0, 0.02); x N(0, 1)."""
+    import torch
+    lens = seq_lengths(cfg)
+    cu = cu_seqlens(lens)
+    M = int(cu[-1])
+    H, F, dt, s = cfg.hidden, cfg.ffn, cfg.dtype, cfg.seed
+    return {
+        "lengths": lens,
+        "cu_seqlens_host": cu,
+        "cu_seqlens": torch.from_numpy(cu).to(device),
+        "M": M,
+        "x": device_normal((M, H), s, "x", dt, device=device),
+        "w_norm1": device_normal((H,), s, "w_norm", dt, std=0.02, mean=1.0, device=device),
+        "w_norm2": device_normal((H,), s + 1, "w_norm", dt, std=0.02, mean=1.0, device=device),
+        "w_qkv": device_normal((cfg.qkv_out, H), s, "w_qkv", dt, std=0.02, device=device),
+        "w_o": device_normal((H, cfg.n_q_heads * cfg.head_dim), s, "w_o", dt, std=0.02, device=device),
+        "w_gate_up": device_normal((2 * F, H), s, "w_gate_up", dt, std=0.02, device=device),
+        "w_down": device_normal((H, F), s, "w_down", dt, std=0.02, device=device),
+    }
+
+
+def decode_inputs(cfg: LayerConfig, device: str = "cuda"):
+    """Full-size decode-attention inputs on the GPU: q [B, Hq, D], the paged
+    K/V caches [num_blocks, block_size, Hkv, D] (N(0, 1)), a shuffled block
+    table and the context lengths."""
+    import torch
+    ctx = seq_lengths(cfg)
+    table, nb = paged_cache_layout(ctx, cfg.block_size, rng_for(cfg, "block_table"))
+    B, dt, s = len(ctx), cfg.dtype, cfg.seed
+    shape = (nb, cfg.block_size, cfg.n_kv_heads, cfg.head_dim)
+    return {
+        "context_lens_host": ctx,
+        "block_table_host": table,
+        "context_lens": torch.from_numpy(ctx.astype(np.int32)).to(device),
+        "block_table": torch.from_numpy(table).to(device),
+        "num_blocks": nb,
+        "max_context_len": int(ctx.max()),
+        "q": device_normal((B, cfg.n_q_heads, cfg.head_dim), s, "q", dt, device=device),
+        "k_cache": device_normal(shape, s, "k_cache", dt, device=device),
+        "v_cache": device_normal(shape, s, "v_cache", dt, device=device),
+    }
