@@ -159,8 +159,10 @@ def _closed_forms():
 
 def cpu_baseline(budget_s: float = 20.0):
     """Time the fp64 CPU oracle on a bounded sample of the same prefill layer
-    and extrapolate to the full batch (rows scale linearly; attention by the
-    causal pair count).  Reported as a baseline only."""
+    and extrapolate to the full batch: the per-row operators on `rows` token
+    rows (linears on `cols` output columns, scaled by N / cols), attention on
+    whole prompts, shortest first, scaled by the causal key-query pair count.
+    Reported as a baseline only."""
     import numpy as np
 
     import oracle
@@ -169,36 +171,32 @@ def cpu_baseline(budget_s: float = 20.0):
     lens = wl.seq_lengths(cfg)
     M, H, F = int(lens.sum()), cfg.hidden, cfg.ffn
     Hq, Hkv, D = cfg.n_q_heads, cfg.n_kv_heads, cfg.head_dim
-    rows = 256
+    rows, cols = 256, 1024
     g = lambda tag, shape, std=1.0, mean=0.0: wl.normal(wl.rng_for(cfg, tag), shape, std, mean).astype(np.float64)
     x = g("x", (rows, H))
     wn = g("w_norm", (H,), 0.02, 1.0)
-    Ws = {"qkv": g("w_qkv", (cfg.qkv_out, H), 0.02), "o": g("w_o", (H, Hq * D), 0.02),
-          "gate_up": g("w_gate_up", (2 * F, H), 0.02), "down": g("w_down", (H, F), 0.02)}
-    t = {}
+    # (N, K) of each linear and a `cols`-row slice of its weight
+    shapes = {"qkv": (cfg.qkv_out, H), "o": (H, Hq * D), "gate_up": (2 * F, H), "down": (H, F)}
+    Ws = {k: g("w_" + k, (cols, K), 0.02) for k, (N, K) in shapes.items()}
+    xs = {"qkv": x, "o": x[:, : Hq * D], "gate_up": x, "down": g("ffn_act", (rows, F))}
     t0 = time.perf_counter()
-    h = oracle.rmsnorm(x, wn, cfg.eps)
-    t["rmsnorm"] = 2 * (time.perf_counter() - t0)
+    oracle.rmsnorm(x, wn, cfg.eps)
+    t_rows = 2 * (time.perf_counter() - t0)
+    t_lin = 0.0
+    for k, (N, K) in shapes.items():
+        t0 = time.perf_counter()
+        oracle.linear(xs[k], Ws[k])
+        t_lin += (time.perf_counter() - t0) * N / cols
+    u = g("gate_up", (rows, 2 * F))
     t0 = time.perf_counter()
-    qkv = oracle.linear(h, Ws["qkv"])
-    o = oracle.linear(x[:, : Hq * D], Ws["o"])
-    gu = oracle.linear(h, Ws["gate_up"])
-    t["linears_a"] = time.perf_counter() - t0
-    t0 = time.perf_counter()
-    act = oracle.swiglu(gu)
-    t["swiglu"] = time.perf_counter() - t0
-    t0 = time.perf_counter()
-    oracle.linear(act, Ws["down"])
-    t["linears_b"] = time.perf_counter() - t0
-    per_row = sum(t.values()) / rows
-    # attention: whole prompts, shortest first, until the budget share is used
+    oracle.swiglu(u)
+    t_rows += time.perf_counter() - t0
+    per_row = (t_rows + t_lin) / rows
     order = np.argsort(lens)
     done_pairs, att_s, used = 0, 0.0, []
     for b in order:
         L = int(lens[b])
-        q = g("q", (L, Hq, D))
-        k = g("k", (L, Hkv, D))
-        v = g("v", (L, Hkv, D))
+        q, k, v = g("q", (L, Hq, D)), g("k", (L, Hkv, D)), g("v", (L, Hkv, D))
         t0 = time.perf_counter()
         oracle.attn_prefill(q, k, v, [0, L], 1 / math.sqrt(D), True)
         att_s += time.perf_counter() - t0
@@ -214,10 +212,10 @@ def cpu_baseline(budget_s: float = 20.0):
     except Exception:  # pragma: no cover
         cores = len(os.sched_getaffinity(0))
     return {"value": M / total_s, "unit": "tokens/s", "cores": int(cores), "kind": "oracle",
-            "sample": f"fp64 NumPy oracle on {rows} token rows of every per-row operator (RMSNorm, 4 linears, "
-                      f"SwiGLU) and {len(used)} whole prompts of attention (lengths {used}), "
-                      f"extrapolated to the {M}-token batch by rows and causal key-query pairs; "
-                      f"decode attention not included; measured {sum(t.values()) + att_s:.1f} s"}
+            "sample": f"fp64 NumPy oracle: RMSNorm and SwiGLU on {rows} token rows, the 4 linears on {rows} rows x "
+                      f"{cols} output columns, attention on {len(used)} whole prompts (lengths {used}); "
+                      f"extrapolated to the {M}-token batch by rows, columns and causal key-query pairs; "
+                      f"decode attention not included"}
 
 
 def main():
