@@ -121,6 +121,7 @@ opscale_status opscale_swiglu(const void* gate_up, void* out, int64_t M, int64_t
  *   cu_seqlens[B] = total_tokens.  Zero-length prompts are allowed.
  * max_seqlen: an upper bound on the prompt lengths, used to size the launch;
  *   the result does not depend on it being tight (it must be >= 1).
+ * scale must be finite and > 0 (1/sqrt(D) for standard attention).
  * D must be 64 or 128; Hkv must divide Hq.  bf16: QK^T and PV on MFMA, fp32
  *   online softmax, probabilities rounded to bf16 for the PV product.
  */
@@ -155,8 +156,8 @@ size_t opscale_attn_decode_workspace_size(int32_t B, int32_t Hq, int32_t D,
  * workspace: DEVICE scratch of at least opscale_attn_decode_workspace_size(B,
  *   Hq, D, max_context_len) bytes, else OPSCALE_ERR_WORKSPACE.  Contents on
  *   entry are ignored.  Calls sharing a workspace must be stream-ordered.
- * block_size must be a power of two in [1, 1024]; D 64 or 128; Hkv | Hq and
- *   Hq / Hkv <= 16.
+ * scale must be finite and > 0.  block_size must be a power of two in
+ *   [1, 1024]; D 64 or 128; Hkv | Hq; on the bf16 path Hq / Hkv is 1, 2, 4 or 8.
  */
 opscale_status opscale_attn_decode(const void* q, const void* k_cache, const void* v_cache,
                                    const int32_t* block_table, const int32_t* context_lens,

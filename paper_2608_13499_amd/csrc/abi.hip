@@ -197,7 +197,8 @@ opscale_status check_prefill(const void* q, const void* k, const void* v, int64_
     return fail(OPSCALE_ERR_INVALID_ARG, "attn_prefill: bad sizes B=%d T=%lld Hq=%d Hkv=%d", B, (long long)T, Hq, Hkv);
   if (Hq % Hkv) return fail(OPSCALE_ERR_INVALID_ARG, "attn_prefill: Hkv=%d does not divide Hq=%d", Hkv, Hq);
   if (D != 64 && D != 128) return fail(OPSCALE_ERR_UNSUPPORTED, "attn_prefill: head_dim %d (supported: 64, 128)", D);
-  if (!std::isfinite(scale)) return fail(OPSCALE_ERR_INVALID_ARG, "attn_prefill: scale must be finite");
+  if (!(scale > 0.f) || !std::isfinite(scale))
+    return fail(OPSCALE_ERR_INVALID_ARG, "attn_prefill: scale must be finite and > 0");
   if (B == 0 || T == 0) return OPSCALE_OK;
   if (max_seqlen < 1) return fail(OPSCALE_ERR_INVALID_ARG, "attn_prefill: max_seqlen must be >= 1");
   const int vec = 16 / esize(dt);
@@ -225,7 +226,8 @@ opscale_status check_decode(const void* q, const void* kc, const void* vc, const
     return fail(OPSCALE_ERR_UNSUPPORTED, "attn_decode: bf16 supports Hq/Hkv in {1, 2, 4, 8}, got %d", G);
   if (bs < 1 || bs > 1024 || (bs & (bs - 1)))
     return fail(OPSCALE_ERR_INVALID_ARG, "attn_decode: block_size %d must be a power of two in [1, 1024]", bs);
-  if (!std::isfinite(scale)) return fail(OPSCALE_ERR_INVALID_ARG, "attn_decode: scale must be finite");
+  if (!(scale > 0.f) || !std::isfinite(scale))
+    return fail(OPSCALE_ERR_INVALID_ARG, "attn_decode: scale must be finite and > 0");
   if (B == 0) return OPSCALE_OK;
   if (max_blocks < 1 || (int64_t)max_blocks * bs >= kMaxDim || num_blocks < 1 || max_ctx < 1)
     return fail(OPSCALE_ERR_INVALID_ARG, "attn_decode: max_blocks_per_seq=%d num_blocks=%lld max_context_len=%d",

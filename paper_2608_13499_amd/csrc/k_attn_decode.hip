@@ -28,8 +28,10 @@ namespace opscale {
 
 namespace {
 constexpr float kLog2e = 1.4426950408889634f;
-constexpr int kChunk = 512;  // nominal keys per split
+constexpr int kChunk = 512;  // nominal keys per split, and keys per page window
 constexpr int kTile = 32;    // keys per wave step
+// Page ids of one window of kChunk keys (any block size >= 1) fit in here.
+constexpr int kMaxPages = kChunk + 1;
 
 struct SplitPlan {
   int n, splits, chunk;
@@ -62,8 +64,10 @@ __global__ __launch_bounds__(256) void attn_decode_split_kernel(
     int log2bs, int max_blocks, int64_t num_blocks, int max_splits, float scale_log2,
     float* __restrict__ ws_o, float* __restrict__ ws_ml) {
   constexpr int CPR = D / 8;        // 16-byte chunks per cache row
-  constexpr int RPI = 64 / CPR;     // rows per wave load instruction
+  constexpr int RPI = 64 / CPR;     // rows per wave load instruction (V layout)
   constexpr int KSTEPS = D / 32;    // MFMA k-steps over the head dim
+  constexpr int NV = kTile / RPI;   // V loads per lane per tile
+  __shared__ int32_t pages[kMaxPages];  // physical blocks of the current key window
   __shared__ float p_lds[4][G][kTile];
   __shared__ float red_m[4][G], red_l[4][G];
   __shared__ float red_o[4][G][D];
@@ -79,7 +83,21 @@ __global__ __launch_bounds__(256) void attn_decode_split_kernel(
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int col = lane & 15, grp = lane >> 4;
   const int64_t row_elems = (int64_t)Hkv * D;
+
+  // Page ids are looked up once per window of kChunk keys (normally the whole
+  // split) and kept in LDS, so the per-tile K/V loads do not wait on a
+  // dependent block-table load.  Invalid ids become -1 (rows of zeros).
   const int32_t* trow = table + (int64_t)b * max_blocks;
+  int p_first = 0, w_end = 0;
+  auto load_pages = [&](int w0) {
+    w_end = min(k_end, w0 + kChunk);
+    p_first = w0 >> log2bs;
+    const int p_count = ((w_end - 1) >> log2bs) - p_first + 1;
+    for (int i = threadIdx.x; i < p_count; i += 256) {
+      const int blk = trow[p_first + i];
+      pages[i] = (uint32_t)blk < (uint64_t)num_blocks ? blk : -1;
+    }
+  };
 
   // Query heads of this group as the MFMA B operand (column = head).
   bf16x8 qf[KSTEPS];
@@ -94,10 +112,34 @@ __global__ __launch_bounds__(256) void attn_decode_split_kernel(
     }
   }
 
-  auto cache_row = [&](const __bf16* cache, int j, bool& ok) -> const __bf16* {
-    const int blk = trow[j >> log2bs];
-    ok = (uint32_t)blk < (uint64_t)num_blocks;
-    return cache + ((int64_t)(ok ? blk : 0) * bs + (j & (bs - 1))) * row_elems + (int64_t)g * D;
+  // address of cache row j (absolute key index) for this KV head, or null
+  auto row_ptr = [&](const __bf16* cache, int j) -> const __bf16* {
+    if (j >= w_end) return nullptr;
+    const int blk = pages[(j >> log2bs) - p_first];
+    if (blk < 0) return nullptr;
+    return cache + ((int64_t)blk * bs + (j & (bs - 1))) * row_elems + (int64_t)g * D;
+  };
+
+  // K in MFMA A-operand layout (lane: key col, 8 head-dim values at 32*s + 8*grp)
+  // and V in row layout (lane: key vrow + RPI*i, 8 head-dim values at 8*vchunk).
+  const int vrow = lane / CPR, vchunk = lane % CPR;
+  struct TileRegs {
+    u32x4 k[2][KSTEPS];
+    u32x4 v[NV];
+  };
+  auto load_tile = [&](int t0, TileRegs& r) {
+#pragma unroll
+    for (int sub = 0; sub < 2; ++sub) {
+      const __bf16* kr = row_ptr(kc, t0 + sub * 16 + col);
+#pragma unroll
+      for (int s = 0; s < KSTEPS; ++s)
+        r.k[sub][s] = kr ? *reinterpret_cast<const u32x4*>(kr + s * 32 + grp * 8) : u32x4{0u, 0u, 0u, 0u};
+    }
+#pragma unroll
+    for (int i = 0; i < NV; ++i) {
+      const __bf16* vr = row_ptr(vc, t0 + i * RPI + vrow);
+      r.v[i] = vr ? *reinterpret_cast<const u32x4*>(vr + vchunk * 8) : u32x4{0u, 0u, 0u, 0u};
+    }
   };
 
   float m_run = -INFINITY, l_run = 0.f;  // for head `col` (lanes col < G meaningful)
@@ -107,50 +149,25 @@ __global__ __launch_bounds__(256) void attn_decode_split_kernel(
 #pragma unroll
     for (int e = 0; e < 8; ++e) acc[hh][e] = 0.f;
 
-  const int vrow = lane / CPR, vchunk = lane % CPR;
-  for (int t0 = k_begin + wave * kTile; t0 < k_end; t0 += 4 * kTile) {
-    // ---- issue K (operand layout) and V (row layout) loads for 32 keys
-    u32x4 kf[2][KSTEPS];
-#pragma unroll
-    for (int sub = 0; sub < 2; ++sub) {
-      const int j = t0 + sub * 16 + col;
-      bool ok = false;
-      const __bf16* kr = j < k_end ? cache_row(kc, j, ok) : kc;
-#pragma unroll
-      for (int s = 0; s < KSTEPS; ++s) {
-        u32x4 w = {0u, 0u, 0u, 0u};
-        if (j < k_end && ok) w = *reinterpret_cast<const u32x4*>(kr + s * 32 + grp * 8);
-        kf[sub][s] = w;
-      }
-    }
-    u32x4 vv[kTile / RPI];
-#pragma unroll
-    for (int i = 0; i < kTile / RPI; ++i) {
-      const int j = t0 + i * RPI + vrow;
-      bool ok = false;
-      const __bf16* vr = j < k_end ? cache_row(vc, j, ok) : vc;
-      u32x4 w = {0u, 0u, 0u, 0u};
-      if (j < k_end && ok) w = *reinterpret_cast<const u32x4*>(vr + vchunk * 8);
-      vv[i] = w;
-    }
-    // ---- scores S^T[key][head]: lane holds head `col`, keys 4*grp + r (+16 sub)
+  auto compute_tile = [&](int t0, const TileRegs& r) {
+    // scores S^T[key][head]: lane holds head `col`, keys t0 + 16*sub + 4*grp + rr
     f32x4 st[2];
 #pragma unroll
     for (int sub = 0; sub < 2; ++sub) {
       st[sub] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int s = 0; s < KSTEPS; ++s)
-        st[sub] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, kf[sub][s]),
-                                                          qf[s], st[sub], 0, 0, 0);
+        st[sub] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, r.k[sub][s]), qf[s],
+                                                          st[sub], 0, 0, 0);
     }
     float tmax = -INFINITY;
 #pragma unroll
     for (int sub = 0; sub < 2; ++sub)
 #pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int j = t0 + sub * 16 + grp * 4 + r;
-        const float sv = j < k_end ? st[sub][r] * scale_log2 : -INFINITY;
-        st[sub][r] = sv;
+      for (int rr = 0; rr < 4; ++rr) {
+        const int j = t0 + sub * 16 + grp * 4 + rr;
+        const float sv = j < w_end ? st[sub][rr] * scale_log2 : -INFINITY;
+        st[sub][rr] = sv;
         tmax = fmaxf(tmax, sv);
       }
     tmax = fmaxf(tmax, __shfl_xor(tmax, 16, 64));
@@ -163,15 +180,14 @@ __global__ __launch_bounds__(256) void attn_decode_split_kernel(
 #pragma unroll
     for (int sub = 0; sub < 2; ++sub)
 #pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const float p = fast_exp2(st[sub][r] - m_use);
+      for (int rr = 0; rr < 4; ++rr) {
+        const float p = fast_exp2(st[sub][rr] - m_use);
         psum += p;
-        if (col < G) p_lds[wave][col][sub * 16 + grp * 4 + r] = p;
+        if (col < G) p_lds[wave][col][sub * 16 + grp * 4 + rr] = p;
       }
     psum += __shfl_xor(psum, 16, 64);
     psum += __shfl_xor(psum, 32, 64);
     l_run = l_run * alpha + psum;
-    // ---- values: acc[hh][e] += p[hh][key] * v[key][vchunk*8 + e]
 #pragma unroll
     for (int hh = 0; hh < G; ++hh) {
       const float a = __shfl(alpha, hh, 64);
@@ -181,15 +197,15 @@ __global__ __launch_bounds__(256) void attn_decode_split_kernel(
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
     __builtin_amdgcn_wave_barrier();
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    // values: acc[hh][e] += p[hh][key] * v[key][vchunk*8 + e]
 #pragma unroll
-    for (int i = 0; i < kTile / RPI; ++i) {
+    for (int i = 0; i < NV; ++i) {
       const int kl = i * RPI + vrow;
-      const uint32_t w[4] = {vv[i][0], vv[i][1], vv[i][2], vv[i][3]};
       float vf[8];
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
-        vf[2 * e] = bf_lo(w[e]);
-        vf[2 * e + 1] = bf_hi(w[e]);
+        vf[2 * e] = bf_lo(r.v[i][e]);
+        vf[2 * e + 1] = bf_hi(r.v[i][e]);
       }
 #pragma unroll
       for (int hh = 0; hh < G; ++hh) {
@@ -201,6 +217,24 @@ __global__ __launch_bounds__(256) void attn_decode_split_kernel(
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
     __builtin_amdgcn_wave_barrier();
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+  };
+
+  // Software pipeline: the loads of the wave's next tile are in flight while
+  // the current one is scored and accumulated.
+  TileRegs cur, nxt;
+  for (int w0 = k_begin; w0 < k_end; w0 += kChunk) {
+    if (w0 != k_begin) __syncthreads();  // every wave is done with the previous window
+    load_pages(w0);
+    __syncthreads();
+    int t0 = w0 + wave * kTile;
+    if (t0 < w_end) load_tile(t0, cur);
+    while (t0 < w_end) {
+      const int t1 = t0 + 4 * kTile;
+      if (t1 < w_end) load_tile(t1, nxt);
+      compute_tile(t0, cur);
+      cur = nxt;
+      t0 = t1;
+    }
   }
 
   // ---- merge the lanes that hold different keys of the same columns

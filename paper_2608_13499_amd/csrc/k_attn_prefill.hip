@@ -39,19 +39,34 @@ constexpr int kBKV = 64;  // keys per K/V tile
 
 template <int D>
 struct PrefillSmem {
-  // K tile: 64 rows of D bf16, 16-byte chunk c of row r at chunk c ^ (r % CPR)
-  // where CPR = D/8 chunks per row.  V^T tile: D rows of 64 keys (128 B), the
-  // 8-byte chunk kc of row d at kc ^ (d % 16).
+  // One stage holds a 64-key K tile and a 64-key V tile, both row-major (D
+  // bf16 per row) and both filled by buffer_load ... lds.  The 16-byte chunk c
+  // of K row r sits at chunk c ^ k_swz(r); of V row r at chunk c ^ v_swz(r).
   static constexpr int kRowBytes = D * 2;
-  static constexpr int kKBytes = kBKV * kRowBytes;
-  static constexpr int kVBytes = D * kBKV * 2;
-  static constexpr int kStage = kKBytes + kVBytes;
+  static constexpr int kTileBytes = kBKV * kRowBytes;
+  static constexpr int kStage = 2 * kTileBytes;
   static constexpr int kTotal = 2 * kStage;
 };
 
+// K is read as the MFMA A operand: 32 consecutive rows at one chunk.  Any 8
+// (and 16) consecutive rows must hit distinct 16-byte bank groups.
 template <int D>
 __device__ __forceinline__ int k_swz(int r) {
   return D == 128 ? (r & 15) : ((r ^ (r >> 3)) & 7);
+}
+// V is read with ds_read_b64_tr_b16: a 16-lane group reads 4 consecutive rows
+// x 32 bytes (two 16-byte chunks), so rows r..r+3 must land in distinct bank
+// groups for both chunks: XOR the chunk with 2*(r mod 4).
+__device__ __forceinline__ int v_swz(int r) { return (r & 3) << 1; }
+
+typedef short s16x4 __attribute__((ext_vector_type(4)));
+
+// Transposed LDS read (gfx950 ds_read_b64_tr_b16).  Within each group of 16
+// lanes, lane i receives element i % 4 of the 8-byte chunks addressed by
+// lanes 4e + i / 4 of its group, for e = 0..3.
+__device__ __forceinline__ u32x2 lds_read_tr16(const OPS_LDS char* p) {
+  const s16x4 v = __builtin_amdgcn_ds_read_tr16_b64_v4i16((OPS_LDS s16x4*)p);
+  return __builtin_bit_cast(u32x2, v);
 }
 
 template <int D>
@@ -63,6 +78,11 @@ __global__ __launch_bounds__(256, 2) void attn_prefill_bf16_kernel(
   constexpr int CPR = D / 8;          // 16-byte chunks per row
   constexpr int DSTEPS = D / 16;      // MFMA k-steps over the head dim
   constexpr int DT = D / 32;          // 32-wide output tiles over the head dim
+  // Lazy rescaling: the running max only moves when a tile's max exceeds it by
+  // more than this (log2 units), so probabilities stay <= 2^kLazy and the
+  // output rescale is skipped on most tiles.  Exact: numerator and
+  // denominator use the same reference.
+  constexpr float kLazy = 8.f;
   __shared__ __attribute__((aligned(16))) char smem_raw[S::kTotal];
   OPS_LDS char* smem = (OPS_LDS char*)smem_raw;
 
@@ -78,10 +98,14 @@ __global__ __launch_bounds__(256, 2) void attn_prefill_bf16_kernel(
   const int L = cu[b + 1] - seq0;
   const int ntiles = (L + BQ - 1) / BQ;
 
-  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
   const int h = g * G + hb * hpb + wave % hpb;
   const int qs = wave / hpb;
   const int fr = lane & 31, fh = lane >> 5;
+  // lane roles in the transposed V reads: 16-lane group tg, member tc
+  const int tg = lane >> 4, tc = lane & 15;
+  const int tr_key = 4 * (tg >> 1) + (tc >> 2);               // + 16 s (+ 8 for the upper half)
+  const int tr_col = 16 * (tg & 1) + 4 * (tc & 3);            // + 32 dt
 
   for (int t = gridDim.y - 1 - blockIdx.y; t < ntiles; t += gridDim.y) {
     const int q_lo = t * BQ + qs * 32;          // first query of this wave
@@ -107,144 +131,104 @@ __global__ __launch_bounds__(256, 2) void attn_prefill_bf16_kernel(
     f32x16 acc[DT];
 #pragma unroll
     for (int i = 0; i < DT; ++i) acc[i] = f32x16{};
-    float m_run = -INFINITY, l_part = 0.f;
+    float m_run = -INFINITY, l_part = 0.f;  // running max (log2 units) and partial sum
 
-    // K tile loader (LDS DMA) and V tile loader (registers, written transposed).
-    auto kv_rsrc = [&](const __bf16* base, int kv0) {
+    // K and V tiles: LDS DMA, rows past the prompt read as zeros.
+    auto load_kv = [&](int kv0, int stage) {
       const int rows = min(kBKV, L - kv0);
-      return make_rsrc(base + (int64_t)(seq0 + kv0) * kv_stride + (int64_t)g * D,
-                       (uint32_t)(((int64_t)(rows - 1) * kv_stride + D) * 2));
-    };
-    auto load_k = [&](int kv0, int stage) {
-      const __amdgpu_buffer_rsrc_t kr = kv_rsrc(k, kv0);
-      OPS_LDS char* dst = smem + stage * S::kStage;
+      const uint32_t nrec = (uint32_t)(((int64_t)(rows - 1) * kv_stride + D) * 2);
+      const int64_t off = (int64_t)(seq0 + kv0) * kv_stride + (int64_t)g * D;
+      const __amdgpu_buffer_rsrc_t kr = make_rsrc(k + off, nrec);
+      const __amdgpu_buffer_rsrc_t vr = make_rsrc(v + off, nrec);
+      OPS_LDS char* dk = smem + stage * S::kStage;
+      OPS_LDS char* dv = dk + S::kTileBytes;
       constexpr int ROWS_PER_LOAD = 64 / CPR;  // rows covered by one 1 KB wave load
+      constexpr int LOADS = kBKV / ROWS_PER_LOAD / 4;
 #pragma unroll
-      for (int grp = wave; grp < kBKV / ROWS_PER_LOAD; grp += 4) {
+      for (int i = 0; i < LOADS; ++i) {
+        const int grp = i * 4 + wave;
         const int r = grp * ROWS_PER_LOAD + lane / CPR;
-        const int c = (lane % CPR) ^ k_swz<D>(r);
-        buffer_load16_lds(kr, dst + grp * 1024, (uint32_t)(((int64_t)r * kv_stride + c * 8) * 2));
-      }
-    };
-    // V: thread -> (key pair kp = 0..31, chunk c), 2*CPR*32/256 items per thread.
-    constexpr int VITEMS = 32 * CPR / 256;  // items (key pair x chunk) per thread
-    u32x4 vreg[VITEMS][2];
-    auto load_v = [&](int kv0) {
-      const __amdgpu_buffer_rsrc_t vr = kv_rsrc(v, kv0);
-#pragma unroll
-      for (int it = 0; it < VITEMS; ++it) {
-        const int item = threadIdx.x + it * 256;
-        const int kp = item & 31, c = item >> 5;
-#pragma unroll
-        for (int e = 0; e < 2; ++e)
-          vreg[it][e] = buffer_load16(vr, (uint32_t)(((int64_t)(2 * kp + e) * kv_stride + c * 8) * 2));
-      }
-    };
-    auto store_vt = [&](int stage) {
-      OPS_LDS char* vt = smem + stage * S::kStage + S::kKBytes;
-#pragma unroll
-      for (int it = 0; it < VITEMS; ++it) {
-        const int item = threadIdx.x + it * 256;
-        const int kp = item & 31, c = item >> 5;
-        const uint32_t a[4] = {vreg[it][0][0], vreg[it][0][1], vreg[it][0][2], vreg[it][0][3]};
-        const uint32_t bb[4] = {vreg[it][1][0], vreg[it][1][1], vreg[it][1][2], vreg[it][1][3]};
-#pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          const int d = c * 8 + e;
-          const uint32_t lo = (e & 1) ? (a[e >> 1] >> 16) : (a[e >> 1] & 0xffffu);
-          const uint32_t hi = (e & 1) ? (bb[e >> 1] & 0xffff0000u) : (bb[e >> 1] << 16);
-          const int kc = (2 * kp) >> 2;  // 8-byte chunk of 4 keys
-          const int off = d * (kBKV * 2) + ((kc ^ (d & 15)) << 3) + ((2 * kp) & 3) * 2;
-          *reinterpret_cast<OPS_LDS uint32_t*>(vt + off) = lo | hi;
-        }
+        const int pc = lane % CPR;
+        buffer_load16_lds(kr, dk + grp * 1024, (uint32_t)(((int64_t)r * kv_stride + (pc ^ k_swz<D>(r)) * 8) * 2));
+        buffer_load16_lds(vr, dv + grp * 1024, (uint32_t)(((int64_t)r * kv_stride + (pc ^ v_swz(r)) * 8) * 2));
       }
     };
 
-    if (nkv > 0) {
-      load_k(0, 0);
-      load_v(0);
-      store_vt(0);
-    }
+    if (nkv > 0) load_kv(0, 0);
     for (int it = 0; it < nkv; ++it) {
       const int kv0 = it * kBKV;
       wait_vmem();
       __syncthreads();
-      const bool more = it + 1 < nkv;
-      if (more) {
-        load_k(kv0 + kBKV, (it + 1) & 1);
-        load_v(kv0 + kBKV);
-      }
+      if (it + 1 < nkv) load_kv(kv0 + kBKV, (it + 1) & 1);
       const OPS_LDS char* ks = smem + (it & 1) * S::kStage;
-      const OPS_LDS char* vts = ks + S::kKBytes;
+      const OPS_LDS char* vs = ks + S::kTileBytes;
       // Skip tiles that are entirely in this wave's causal future.
       const bool active = !(causal && kv0 > q_lo + 31) && q_lo < L;
-      if (active) {
-        f32x16 st[2];
+      if (!active) continue;
+      f32x16 st[2];
 #pragma unroll
-        for (int kb = 0; kb < 2; ++kb) {
-          st[kb] = f32x16{};
-          const int r = kb * 32 + fr;
+      for (int kb = 0; kb < 2; ++kb) {
+        st[kb] = f32x16{};
+        const int r = kb * 32 + fr;
 #pragma unroll
-          for (int s = 0; s < DSTEPS; ++s) {
-            const int c = 2 * s + fh;
-            const bf16x8 kf = *reinterpret_cast<const OPS_LDS bf16x8*>(
-                ks + r * S::kRowBytes + ((c ^ k_swz<D>(r)) << 4));
-            st[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[s], st[kb], 0, 0, 0);
-          }
+        for (int s = 0; s < DSTEPS; ++s) {
+          const int c = 2 * s + fh;
+          const bf16x8 kf = *reinterpret_cast<const OPS_LDS bf16x8*>(
+              ks + r * S::kRowBytes + ((c ^ k_swz<D>(r)) << 4));
+          st[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[s], st[kb], 0, 0, 0);
         }
-        // scale into the log2 domain and mask
-        const bool need_mask = (causal && kv0 + kBKV - 1 > q_lo) || (kv0 + kBKV > L);
-        float tmax = -INFINITY;
+      }
+      // mask (only tiles that reach past the diagonal or the prompt end):
+      // key kv0 + fh*4 + off is visible iff off <= lim, off a constant per element
+      if ((causal && kv0 + kBKV - 1 > q_lo) || kv0 + kBKV > L) {
+        const int lim = (causal ? min(q_pos, L - 1) : L - 1) - kv0 - fh * 4;
 #pragma unroll
         for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-          for (int e = 0; e < 16; ++e) {
-            float sv = st[kb][e] * scale_log2;
-            if (need_mask) {
-              const int key = kv0 + kb * 32 + (e >> 2) * 8 + fh * 4 + (e & 3);
-              if (key >= L || (causal && key > q_pos)) sv = -INFINITY;
-            }
-            st[kb][e] = sv;
-            tmax = fmaxf(tmax, sv);
-          }
-        tmax = fmaxf(tmax, __shfl_xor(tmax, 32, 64));
-        const float m_new = fmaxf(m_run, tmax);
-        const float m_use = m_new == -INFINITY ? 0.f : m_new;
-        const float alpha = fast_exp2(m_run - m_use);
-        m_run = m_new;
-        float psum = 0.f;
-        bf16x8 pf[4];
+          for (int e = 0; e < 16; ++e)
+            if (kb * 32 + (e >> 2) * 8 + (e & 3) > lim) st[kb][e] = -INFINITY;
+      }
+      float tmax = -INFINITY;
 #pragma unroll
-        for (int kb = 0; kb < 2; ++kb)
+      for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-          for (int e = 0; e < 16; ++e) {
-            const float p = fast_exp2(st[kb][e] - m_use);
-            psum += p;
-            pf[kb * 2 + (e >> 3)][e & 7] = (__bf16)p;
-          }
-        l_part = l_part * alpha + psum;
+        for (int e = 0; e < 16; ++e) tmax = fmaxf(tmax, st[kb][e]);
+      tmax = fmaxf(tmax, __shfl_xor(tmax, 32, 64)) * scale_log2;
+      // move the reference max only when the tile's max exceeds it by kLazy
+      if (tmax > m_run + kLazy) {
+        const float alpha = fast_exp2(m_run - tmax);  // 0 on the first tile
+        l_part *= alpha;
 #pragma unroll
         for (int i = 0; i < DT; ++i) acc[i] *= alpha;
-        // the next V tile goes to the other stage now, before the PV product,
-        // so its registers are free again for the accumulators
-        if (more) store_vt((it + 1) & 1);
-        // O^T[d][i] += sum_key V^T[d][key] P^T[key][i]
+        m_run = tmax;
+      }
+      const float m_use = m_run == -INFINITY ? 0.f : m_run;
+      float psum = 0.f;
+      bf16x8 pf[4];
 #pragma unroll
-        for (int dt = 0; dt < DT; ++dt) {
-          const int d = dt * 32 + fr;
-          const OPS_LDS char* row = vts + d * (kBKV * 2);
+      for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-          for (int s = 0; s < 4; ++s) {
-            const int kc0 = 4 * s + fh, kc1 = 4 * s + 2 + fh;
-            const u32x2 lo = *reinterpret_cast<const OPS_LDS u32x2*>(row + ((kc0 ^ (d & 15)) << 3));
-            const u32x2 hi = *reinterpret_cast<const OPS_LDS u32x2*>(row + ((kc1 ^ (d & 15)) << 3));
-            const u32x4 w = {lo[0], lo[1], hi[0], hi[1]};
-            acc[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, w), pf[s],
-                                                             acc[dt], 0, 0, 0);
-          }
+        for (int e = 0; e < 16; ++e) {
+          const float p = fast_exp2(fmaf(st[kb][e], scale_log2, -m_use));
+          psum += p;
+          pf[kb * 2 + (e >> 3)][e & 7] = (__bf16)p;
         }
-      } else if (more) {
-        store_vt((it + 1) & 1);
+      l_part += psum;
+      // O^T[d][i] += sum_key V^T[d][key] P^T[key][i]; the A operand (V^T, lane:
+      // d = 32 dt + fr, keys 16 s + 8 (e/4) + 4 fh + e%4) comes from two
+      // transposed reads of the row-major V tile.
+#pragma unroll
+      for (int dt = 0; dt < DT; ++dt) {
+#pragma unroll
+        for (int s = 0; s < 4; ++s) {
+          const int r0 = 16 * s + tr_key, r1 = r0 + 8;
+          const int cc = 32 * dt + tr_col;  // head-dim column of this lane's 8-byte chunk
+          const int c16 = cc >> 3, half = (cc >> 2) & 1;
+          const u32x2 lo = lds_read_tr16(vs + r0 * S::kRowBytes + ((c16 ^ v_swz(r0)) << 4) + half * 8);
+          const u32x2 hi = lds_read_tr16(vs + r1 * S::kRowBytes + ((c16 ^ v_swz(r1)) << 4) + half * 8);
+          const bf16x8 vf = __builtin_bit_cast(bf16x8, u32x4{lo[0], lo[1], hi[0], hi[1]});
+          acc[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf[s], acc[dt], 0, 0, 0);
+        }
       }
     }
 

@@ -2,9 +2,11 @@
 // projections of the decoder layer.
 //
 // bf16 path: MFMA v_mfma_f32_32x32x16_bf16, fp32 accumulation.  A 256x256
-// block tile is staged through LDS in BK = 64 slices with two stages; the next
-// slice is fetched with buffer_load ... lds (HBM/L2 -> LDS without passing
-// through registers) while the current one feeds the matrix cores.  Rows and
+// block tile is staged through an LDS ring in BK-wide K slices; the next slices
+// are fetched with buffer_load ... lds (HBM/L2 -> LDS without passing through
+// registers) while the current one feeds the matrix cores.  Four waves own
+// 128x128 sub-tiles each, so every 16-byte LDS fragment read feeds four
+// MFMAs (LDS read traffic is half that of 128x64 wave tiles).  Rows and
 // K columns beyond the matrix read as zeros through the buffer descriptor's
 // range check, so ragged M, N and K need no separate code path.
 //
@@ -21,53 +23,97 @@ namespace opscale {
 
 namespace {
 
-constexpr int kBM = 256, kBN = 256, kBK = 64;
-constexpr int kWM = 128, kWN = 64;                           // wave tile (m x n)
-constexpr int kWavesM = kBM / kWM, kWavesN = kBN / kWN;      // 2 x 4
-constexpr int kThreads = kWavesM * kWavesN * 64;             // 512
-constexpr int kRowBytes = kBK * 2;                           // 128 B per LDS row
-constexpr int kStageBytes = (kBM + kBN) * kRowBytes;         // 64 KB
-constexpr int kGroupM = 8;                                   // tile rows per L2 group
+// Tile configuration: BM x BN block tile, K in slices of BK, WGM x WGN waves
+// (each owns a (BM/WGM) x (BN/WGN) sub-tile), STAGES-deep LDS ring.
+template <int BM_, int BN_, int BK_, int WGM_, int WGN_, int STAGES_, bool INTERLEAVE_ = false>
+struct GemmCfg {
+  static constexpr int BM = BM_, BN = BN_, BK = BK_, WGM = WGM_, WGN = WGN_, STAGES = STAGES_;
+  static constexpr bool INTERLEAVE = INTERLEAVE_;
+  static constexpr int WM = BM / WGM, WN = BN / WGN;  // wave tile (m x n)
+  static constexpr int kThreads = WGM * WGN * 64;
+  static constexpr int kWaves = WGM * WGN;
+  static constexpr int kRowBytes = BK * 2;              // one LDS row = BK bf16
+  static constexpr int kCPR = BK / 8;                   // 16-byte chunks per row
+  static constexpr int kRowsPerLoad = 64 / kCPR;        // rows one 1 KB wave load covers
+  static constexpr int kStageBytes = (BM + BN) * kRowBytes;
+  static constexpr int kLdsBytes = STAGES * kStageBytes;
+  static constexpr int kLoadsPerTile = (BM + BN) / kRowsPerLoad / kWaves;  // per wave
+  static_assert(BM % (kRowsPerLoad * kWaves) == 0 && BN % (kRowsPerLoad * kWaves) == 0,
+                "each operand's rows must split evenly over the waves");
+  static_assert(BK % 32 == 0, "an even number of 16-wide k-steps per slice");
+  static_assert(kLoadsPerTile * (STAGES - 2 > 0 ? STAGES - 2 : 0) <= 63, "vmcnt range");
+};
 
-// 16-byte chunk c of LDS row r lives at physical chunk c ^ swz(r).  For any 8
-// consecutive rows (32-bank view) and any 16 consecutive rows (64-bank view)
-// the same logical chunk lands in distinct bank groups, so the per-lane
-// 16-byte fragment reads below are conflict-free.
-__device__ __forceinline__ int swz(int r) { return (r ^ (r >> 3)) & 7; }
+using CfgBig = GemmCfg<256, 256, 64, 2, 2, 2>;     // 4 waves of 128x128, 2 x 64 KB stages
+using CfgBig8 = GemmCfg<256, 256, 64, 2, 4, 2>;    // 8 waves of 128x64, 2 x 64 KB stages
+using CfgDeep = GemmCfg<256, 256, 32, 2, 2, 4>;    // 4 waves of 128x128, 4 x 32 KB stages
+using CfgDeep8 = GemmCfg<256, 256, 32, 2, 4, 4>;   // 8 waves of 128x64, 4 x 32 KB stages
+using CfgDeepI = GemmCfg<256, 256, 32, 2, 2, 4, true>;
+using CfgDeep8I = GemmCfg<256, 256, 32, 2, 4, 4, true>;
+using CfgMid = GemmCfg<256, 128, 64, 2, 2, 3>;     // 4 waves of 128x64, 3 x 48 KB stages
+using CfgMidI = GemmCfg<256, 128, 64, 2, 2, 3, true>;
 
-// Loads rows [0, rows) x k-slice [k0, k0 + 64) of a K-contiguous bf16 matrix
-// (descriptor based at the tile's first row) into one LDS stage region.
-// Wave w handles 8-row groups w, w + 8, ...; lane p of a group writes LDS
-// bytes [p*16, p*16+16) of the group, i.e. row p/8, physical chunk p%8.
-template <int ROWS>
-__device__ __forceinline__ void load_tile(__amdgpu_buffer_rsrc_t rsrc, OPS_LDS char* lds, int K, int k0,
-                                          int wave, int lane) {
-  const int rl = lane >> 3, pc = lane & 7;
+constexpr int kGroupM = 8;  // tile rows per L2 group
+
+// 16-byte chunk c of LDS row r is stored at physical chunk c ^ swz(r).  For
+// any 8 consecutive rows (a 32-bank view of LDS) and any 16 consecutive rows
+// (a 64-bank view) the same logical chunk lands in distinct 16-byte bank
+// groups, so the per-lane fragment reads are conflict-free.  swz depends only
+// on r mod 32, i.e. on the lane, so one per-lane offset per K step serves every
+// 32-row fragment of a wave (the rest is an immediate offset).
+template <int CPR>
+__device__ __forceinline__ int swz(int r) {
+  if constexpr (CPR == 8) return (r ^ ((r >> 3) & 1)) & 7;  // 128-byte rows
+  else return ((r >> 1) ^ (r >> 3)) & 3;                    // 64-byte rows
+}
+
+// s_waitcnt with only the vector-memory counter constrained (gfx9 encoding:
+// vmcnt in bits [3:0] and [15:14], expcnt [6:4], lgkmcnt [11:8]).
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N <= 63, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
+}
+
+// One BK-wide slice of ROWS rows of a K-contiguous bf16 matrix (descriptor
+// based at the tile's first row) into an LDS stage region.  Wave w issues
+// loads w, w + waves, ...; lane p of a load writes LDS bytes [p*16, p*16+16)
+// of its 1 KB group: row p / CPR, physical chunk p % CPR.
+template <class C, int ROWS>
+__device__ __forceinline__ void load_slice(__amdgpu_buffer_rsrc_t rsrc, OPS_LDS char* lds, int K, int k0,
+                                           int wave, int lane) {
+  const int rl = lane / C::kCPR, pc = lane % C::kCPR;
+  constexpr int kPerWave = ROWS / C::kRowsPerLoad / C::kWaves;
 #pragma unroll
-  for (int grp = wave; grp < ROWS / 8; grp += kThreads / 64) {
-    const int r = grp * 8 + rl;
-    const int c = pc ^ swz(r);
+  for (int g = 0; g < kPerWave; ++g) {
+    const int grp = g * C::kWaves + wave;
+    const int r = grp * C::kRowsPerLoad + rl;
+    const int c = pc ^ swz<C::kCPR>(r);
     const int k = k0 + c * 8;
     const uint32_t voff = k < K ? (uint32_t)(((int64_t)r * K + k) * 2) : kOobOffset;
-    buffer_load16_lds(rsrc, lds + grp * 8 * kRowBytes, voff);
+    buffer_load16_lds(rsrc, lds + grp * 1024, voff);
   }
 }
 
-__device__ __forceinline__ bf16x8 lds_frag(const OPS_LDS char* base, int r, int c) {
-  return *reinterpret_cast<const OPS_LDS bf16x8*>(base + r * kRowBytes + ((c ^ swz(r)) << 4));
+template <class C>
+__device__ __forceinline__ bf16x8 lds_frag(const OPS_LDS char* p) {
+  return *reinterpret_cast<const OPS_LDS bf16x8*>(p);
 }
 
 }  // namespace
 
-__global__ __launch_bounds__(kThreads, 1) void gemm_bf16_kernel(const __bf16* __restrict__ x,
-                                                                const __bf16* __restrict__ W,
-                                                                const __bf16* __restrict__ bias,
-                                                                __bf16* __restrict__ y, int M, int N,
-                                                                int K) {
+template <class C>
+__global__ __launch_bounds__(C::kThreads, 1) void gemm_bf16_kernel(const __bf16* __restrict__ x,
+                                                                   const __bf16* __restrict__ W,
+                                                                   const __bf16* __restrict__ bias,
+                                                                   __bf16* __restrict__ y, int M, int N,
+                                                                   int K) {
   extern __shared__ __attribute__((aligned(16))) char smem_raw[];
   OPS_LDS char* smem = (OPS_LDS char*)smem_raw;
+  constexpr int BM = C::BM, BN = C::BN, BK = C::BK, WM = C::WM, WN = C::WN, S = C::STAGES;
+  constexpr int TM = WM / 32, TN = WN / 32;  // 32x32 MFMA tiles per wave
 
-  const int tiles_m = (M + kBM - 1) / kBM, tiles_n = (N + kBN - 1) / kBN;
+  const int tiles_m = (M + BM - 1) / BM, tiles_n = (N + BN - 1) / BN;
   const uint32_t tid = xcd_remap(blockIdx.x, (uint32_t)(tiles_m * tiles_n));
   // grouped order: kGroupM tile-rows sweep the tile-columns together
   const int group = tid / (kGroupM * tiles_n);
@@ -75,67 +121,123 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_bf16_kernel(const __bf16* __
   const int gsize = min(tiles_m - first_m, kGroupM);
   const int in_group = tid % (kGroupM * tiles_n);
   const int tm = first_m + in_group % gsize, tn = in_group / gsize;
-  const int m0 = tm * kBM, n0 = tn * kBN;
+  const int m0 = tm * BM, n0 = tn * BN;
 
-  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  const int wm = wave % kWavesM, wn = wave / kWavesM;
+  // wave index as a scalar: the LDS destinations of the loads are then
+  // wave-uniform without a readfirstlane per load
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
+  const int wm = wave % C::WGM, wn = wave / C::WGM;
 
-  const __amdgpu_buffer_rsrc_t xr =
-      make_rsrc(x + (int64_t)m0 * K, (uint32_t)(min(kBM, M - m0) * K * 2));
-  const __amdgpu_buffer_rsrc_t wr =
-      make_rsrc(W + (int64_t)n0 * K, (uint32_t)(min(kBN, N - n0) * K * 2));
+  const __amdgpu_buffer_rsrc_t xr = make_rsrc(x + (int64_t)m0 * K, (uint32_t)(min(BM, M - m0) * K * 2));
+  const __amdgpu_buffer_rsrc_t wr = make_rsrc(W + (int64_t)n0 * K, (uint32_t)(min(BN, N - n0) * K * 2));
 
-  f32x16 acc[kWN / 32][kWM / 32];
+  f32x16 acc[TN][TM];
 #pragma unroll
-  for (int i = 0; i < kWN / 32; ++i)
+  for (int i = 0; i < TN; ++i)
 #pragma unroll
-    for (int j = 0; j < kWM / 32; ++j) acc[i][j] = f32x16{};
+    for (int j = 0; j < TM; ++j) acc[i][j] = f32x16{};
 
-  const int nk = (K + kBK - 1) / kBK;
-  auto stage_x = [&](int s) { return smem + s * kStageBytes; };
-  auto stage_w = [&](int s) { return smem + s * kStageBytes + kBM * kRowBytes; };
+  const int nk = (K + BK - 1) / BK;
+  auto stage_x = [&](int s) { return smem + s * C::kStageBytes; };
+  auto stage_w = [&](int s) { return smem + s * C::kStageBytes + BM * C::kRowBytes; };
+  auto load = [&](int kt) {
+    load_slice<C, BM>(xr, stage_x(kt % S), K, kt * BK, wave, lane);
+    load_slice<C, BN>(wr, stage_w(kt % S), K, kt * BK, wave, lane);
+  };
 
-  load_tile<kBM>(xr, stage_x(0), K, 0, wave, lane);
-  load_tile<kBN>(wr, stage_w(0), K, 0, wave, lane);
+#pragma unroll
+  for (int s = 0; s < S - 1; ++s)
+    if (s < nk) load(s);
 
   const int fr = lane & 31, fh = lane >> 5;
-  for (int kt = 0; kt < nk; ++kt) {
-    wait_vmem();
-    __syncthreads();
-    if (kt + 1 < nk) {
-      load_tile<kBM>(xr, stage_x((kt + 1) & 1), K, (kt + 1) * kBK, wave, lane);
-      load_tile<kBN>(wr, stage_w((kt + 1) & 1), K, (kt + 1) * kBK, wave, lane);
+  constexpr int KS = BK / 16;  // MFMA k-steps per slice
+  // per-lane byte offset of this lane's 16-byte fragment row in k-step ks
+  int lane_off[KS];
+#pragma unroll
+  for (int ks = 0; ks < KS; ++ks) lane_off[ks] = fr * C::kRowBytes + (((2 * ks + fh) ^ swz<C::kCPR>(fr)) << 4);
+  // the x slice sits first in a stage, the W slice after it
+  const int x_row0 = wm * WM * C::kRowBytes, w_row0 = BM * C::kRowBytes + wn * WN * C::kRowBytes;
+
+  bf16x8 a[2][TN], b[2][TM];
+  auto frags = [&](const OPS_LDS char* st, int ks, int buf) {
+#pragma unroll
+    for (int i = 0; i < TN; ++i) a[buf][i] = lds_frag<C>(st + w_row0 + i * 32 * C::kRowBytes + lane_off[ks]);
+#pragma unroll
+    for (int j = 0; j < TM; ++j) b[buf][j] = lds_frag<C>(st + x_row0 + j * 32 * C::kRowBytes + lane_off[ks]);
+  };
+  auto mfmas = [&](int buf) {
+#pragma unroll
+    for (int i = 0; i < TN; ++i)
+#pragma unroll
+      for (int j = 0; j < TM; ++j)
+        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[buf][i], b[buf][j], acc[i][j], 0, 0, 0);
+  };
+  // Interleave the next fragment reads between this step's MFMAs (one read
+  // after each MFMA until the reads run out, then the remaining MFMAs).
+  auto schedule = [&]() {
+    if constexpr (C::INTERLEAVE) {
+      constexpr int R = TN + TM, MF = TN * TM;
+#pragma unroll
+      for (int i = 0; i < (R < MF ? R : MF); ++i) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // MFMA
+        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // DS read
+      }
+      if constexpr (MF > R) __builtin_amdgcn_sched_group_barrier(0x008, MF - R, 0);
     }
-    const OPS_LDS char* sx = stage_x(kt & 1);
-    const OPS_LDS char* sw = stage_w(kt & 1);
+  };
+
+  if constexpr (S == 2) {
+    for (int kt = 0; kt < nk; ++kt) {
+      wait_vmcnt<0>();
+      __syncthreads();
+      if (kt + 1 < nk) load(kt + 1);
+      const OPS_LDS char* st = smem + (kt % S) * C::kStageBytes;
+      frags(st, 0, 0);
 #pragma unroll
-    for (int ks = 0; ks < kBK / 16; ++ks) {
-      const int c = ks * 2 + fh;
-      bf16x8 a[kWN / 32], b[kWM / 32];
+      for (int ks = 0; ks < KS; ++ks) {
+        if (ks + 1 < KS) frags(st, ks + 1, (ks + 1) & 1);
+        mfmas(ks & 1);
+        schedule();
+      }
+    }
+  } else {
+    // Look-ahead pipeline: at the top of iteration kt slice kt + 1 is made
+    // visible, so the last k-step of slice kt already reads slice kt + 1's
+    // first fragments and the matrix cores never wait on the barrier.
+    if (S > 2 && nk > S - 2) wait_vmcnt<C::kLoadsPerTile * (S > 2 ? S - 2 : 0)>();
+    else wait_vmcnt<0>();
+    __syncthreads();
+    frags(smem, 0, 0);
+    for (int kt = 0; kt < nk; ++kt) {
+      if (S > 3 && kt + S - 2 < nk) wait_vmcnt<C::kLoadsPerTile * (S > 3 ? S - 3 : 0)>();
+      else wait_vmcnt<0>();
+      __syncthreads();
+      if (kt + S - 1 < nk) load(kt + S - 1);
+      const OPS_LDS char* st = smem + (kt % S) * C::kStageBytes;
+      const OPS_LDS char* st_next = smem + ((kt + 1) % S) * C::kStageBytes;
 #pragma unroll
-      for (int i = 0; i < kWN / 32; ++i) a[i] = lds_frag(sw, wn * kWN + i * 32 + fr, c);
-#pragma unroll
-      for (int j = 0; j < kWM / 32; ++j) b[j] = lds_frag(sx, wm * kWM + j * 32 + fr, c);
-#pragma unroll
-      for (int i = 0; i < kWN / 32; ++i)
-#pragma unroll
-        for (int j = 0; j < kWM / 32; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
+      for (int ks = 0; ks < KS; ++ks) {
+        const int nb = (ks + 1) & 1;
+        if (ks + 1 < KS) frags(st, ks + 1, nb);
+        else if (kt + 1 < nk) frags(st_next, 0, nb);
+        mfmas(ks & 1);
+        schedule();
+      }
     }
   }
 
-  // Epilogue.  acc[i][j] element e: n = n0 + wn*64 + i*32 + (e/4)*8 + fh*4 + e%4,
-  // m = m0 + wm*128 + j*32 + fr.  Four consecutive n per lane -> one 8-byte store.
+  // Epilogue.  acc[i][j] element e: n = n0 + wn*WN + i*32 + (e/4)*8 + fh*4 + e%4,
+  // m = m0 + wm*WM + j*32 + fr.  Four consecutive n per lane -> one 8-byte store.
 #pragma unroll
-  for (int j = 0; j < kWM / 32; ++j) {
-    const int m = m0 + wm * kWM + j * 32 + fr;
+  for (int j = 0; j < TM; ++j) {
+    const int m = m0 + wm * WM + j * 32 + fr;
     if (m >= M) continue;
     __bf16* yrow = y + (int64_t)m * N;
 #pragma unroll
-    for (int i = 0; i < kWN / 32; ++i) {
+    for (int i = 0; i < TN; ++i) {
 #pragma unroll
       for (int g = 0; g < 4; ++g) {
-        const int n = n0 + wn * kWN + i * 32 + g * 8 + fh * 4;
+        const int n = n0 + wn * WN + i * 32 + g * 8 + fh * 4;
         if (n >= N) continue;
         float v0 = acc[i][j][g * 4 + 0], v1 = acc[i][j][g * 4 + 1];
         float v2 = acc[i][j][g * 4 + 2], v3 = acc[i][j][g * 4 + 3];
@@ -202,26 +304,39 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(const float* __restrict__
   }
 }
 
+template <class C>
+static hipError_t launch_gemm_bf16(const void* x, const void* W, const void* bias, void* y, int64_t M,
+                                   int64_t N, int64_t K, hipStream_t s) {
+  // More than 64 KB of dynamic LDS per workgroup needs the limit raised once
+  // per process (a host-side function attribute, no allocation).
+  static const hipError_t attr = hipFuncSetAttribute(
+      reinterpret_cast<const void*>(gemm_bf16_kernel<C>), hipFuncAttributeMaxDynamicSharedMemorySize,
+      C::kLdsBytes);
+  if (attr != hipSuccess) return attr;
+  const int64_t tiles = ((M + C::BM - 1) / C::BM) * ((N + C::BN - 1) / C::BN);
+  hipLaunchKernelGGL((gemm_bf16_kernel<C>), dim3((unsigned)tiles), dim3(C::kThreads), C::kLdsBytes, s,
+                     static_cast<const __bf16*>(x), static_cast<const __bf16*>(W),
+                     static_cast<const __bf16*>(bias), static_cast<__bf16*>(y), (int)M, (int)N, (int)K);
+  return hipGetLastError();
+}
+
 hipError_t launch_linear(const void* x, const void* W, const void* bias, void* y, int64_t M,
                          int64_t N, int64_t K, bool bf16, hipStream_t s) {
+#ifdef OPSCALE_GEMM_CFG
+  if (bf16) return launch_gemm_bf16<OPSCALE_GEMM_CFG>(x, W, bias, y, M, N, K, s);
+#else
   if (bf16) {
-    // 128 KB of dynamic LDS per workgroup exceeds the default limit: raise it
-    // once per process (a host-side attribute, no allocation).
-    static const hipError_t attr = hipFuncSetAttribute(
-        reinterpret_cast<const void*>(gemm_bf16_kernel), hipFuncAttributeMaxDynamicSharedMemorySize,
-        2 * kStageBytes);
-    if (attr != hipSuccess) return attr;
-    const int64_t tiles = ((M + kBM - 1) / kBM) * ((N + kBN - 1) / kBN);
-    hipLaunchKernelGGL(gemm_bf16_kernel, dim3((unsigned)tiles), dim3(kThreads), 2 * kStageBytes, s,
-                       static_cast<const __bf16*>(x), static_cast<const __bf16*>(W),
-                       static_cast<const __bf16*>(bias), static_cast<__bf16*>(y), (int)M, (int)N,
-                       (int)K);
-  } else {
-    const dim3 grid((unsigned)((N + 63) / 64), (unsigned)((M + 63) / 64));
-    hipLaunchKernelGGL(gemm_f32_kernel, grid, dim3(256), 0, s, static_cast<const float*>(x),
-                       static_cast<const float*>(W), static_cast<const float*>(bias),
-                       static_cast<float*>(y), (int)M, (int)N, (int)K);
+    // 256x256 tiles when they fill the 256 CUs; otherwise the 256x128 tile
+    // doubles the number of workgroups (decode-sized M).
+    const int64_t big_tiles = ((M + 255) / 256) * ((N + 255) / 256);
+    if (big_tiles >= 256) return launch_gemm_bf16<CfgBig8>(x, W, bias, y, M, N, K, s);
+    return launch_gemm_bf16<CfgMid>(x, W, bias, y, M, N, K, s);
   }
+#endif
+  const dim3 grid((unsigned)((N + 63) / 64), (unsigned)((M + 63) / 64));
+  hipLaunchKernelGGL(gemm_f32_kernel, grid, dim3(256), 0, s, static_cast<const float*>(x),
+                     static_cast<const float*>(W), static_cast<const float*>(bias),
+                     static_cast<float*>(y), (int)M, (int)N, (int)K);
   return hipGetLastError();
 }
 

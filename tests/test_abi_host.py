@@ -96,6 +96,7 @@ def test_prefill_validation(lib):
     assert call(ms=0) == 1
     assert call(cu=None) == 1
     assert call(scale=float("nan")) == 1
+    assert call(scale=-0.5) == 1 and call(scale=0.0) == 1
     assert call(q=A16 + 8) == 1            # misaligned
     assert call(T=0) == 0 and call(B=0) == 0
 

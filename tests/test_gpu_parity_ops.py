@@ -154,7 +154,7 @@ def test_attn_prefill_single_key_returns_v(ops):
 
 
 # --------------------------------------------------------- decode attention --
-def _decode_case(ops, dtype, ctx, Hq, Hkv, D, bs, seed=51, bad_block=False):
+def _decode_case(ops, dtype, ctx, Hq, Hkv, D, bs, seed=51, bad_block=False, max_context_len=None):
     import torch
     ctx = np.asarray(ctx, np.int64)
     rng = wl.rng_for(seed, "block_table")
@@ -165,7 +165,7 @@ def _decode_case(ops, dtype, ctx, Hq, Hkv, D, bs, seed=51, bad_block=False):
     vc = gen(seed, "v_cache", (nb, bs, Hkv, D), dtype)
     q = gen(seed, "q", (len(ctx), Hq, D), dtype)
     scale = 1.0 / math.sqrt(D)
-    maxc = int(max(1, ctx.max()))
+    maxc = int(max(1, ctx.max())) if max_context_len is None else max_context_len
     out = ops.opscale_attn_decode(cuda(q), cuda(kc), cuda(vc), cuda(torch.from_numpy(table)),
                                   cuda(torch.from_numpy(ctx.astype(np.int32))), maxc, scale)
     torch.cuda.synchronize()
@@ -198,3 +198,12 @@ def test_attn_decode_invalid_block_reads_zero(ops, dtype):
     say(f"attn_decode invalid block id {dtype}")
     got, ref = _decode_case(ops, dtype, [40, 20], 8, 2, 128, 16, bad_block=True)
     assert_close(got, ref, dtype, "attn_decode bad block")
+
+
+@pytest.mark.parametrize("bs", [16, 1])
+def test_attn_decode_context_beyond_launch_bound(ops, bs):
+    """max_context_len only sizes the launch: a longer context is processed in
+    several key windows by one split and the result is unchanged."""
+    say(f"attn_decode context beyond max_context_len, bs={bs}")
+    got, ref = _decode_case(ops, "bf16", [2000, 700, 3], 8, 2, 128, bs, max_context_len=100)
+    assert_close(got, ref, "bf16", "attn_decode long context")
