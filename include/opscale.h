@@ -149,8 +149,9 @@ size_t opscale_attn_decode_workspace_size(int32_t B, int32_t Hq, int32_t D,
  * q, o: [B, Hq, D]; k_cache, v_cache: [num_blocks, block_size, Hkv, D];
  * block_table: DEVICE int32 [B, max_blocks_per_seq]; context_lens: DEVICE int32 [B].
  * A context length of 0 yields a zero output row.  Lengths above
- * max_blocks_per_seq * block_size are clamped to it.  Block ids outside
- * [0, num_blocks) read as zeros (no fault).
+ * max_blocks_per_seq * block_size are clamped to it.  Keys whose block id is
+ * outside [0, num_blocks) are skipped (never read); a row whose keys are all
+ * skipped is zero.
  * max_context_len: an upper bound on context_lens used to size the split-KV
  *   launch and the workspace; results do not depend on it.
  * workspace: DEVICE scratch of at least opscale_attn_decode_workspace_size(B,

@@ -34,6 +34,12 @@ __device__ __forceinline__ void buffer_load16_lds(__amdgpu_buffer_rsrc_t r, OPS_
   __builtin_amdgcn_raw_ptr_buffer_load_lds(r, lds_wave_base, 16, voff, 0, 0, 0);
 }
 
+// 16 bytes per lane from a 64-bit global address into LDS at lds_wave_base +
+// lane * 16 (global_load_lds_dwordx4).
+__device__ __forceinline__ void global_load16_lds(const void* gptr, OPS_LDS void* lds_wave_base) {
+  __builtin_amdgcn_global_load_lds(gptr, lds_wave_base, 16, 0, 0);
+}
+
 __device__ __forceinline__ float bf_lo(uint32_t u) { return __uint_as_float(u << 16); }
 __device__ __forceinline__ float bf_hi(uint32_t u) { return __uint_as_float(u & 0xffff0000u); }
 
@@ -62,6 +68,14 @@ __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_ex
 // Wait for every outstanding vector-memory operation of this wave (including
 // buffer loads into LDS) before a barrier makes their data visible.
 __device__ __forceinline__ void wait_vmem() { __builtin_amdgcn_s_waitcnt(0); }
+
+// s_waitcnt constraining only the vector-memory counter to <= N (gfx9
+// encoding: vmcnt in bits [3:0] and [15:14], expcnt [6:4], lgkmcnt [11:8]).
+template <int N>
+__device__ __forceinline__ void wait_vmcnt_le() {
+  static_assert(N >= 0 && N <= 63, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
+}
 
 // Block id -> tile id such that the consecutive tile ids land on one XCD.
 // Workgroups are dealt round-robin to the 8 XCDs, so block b runs on XCD

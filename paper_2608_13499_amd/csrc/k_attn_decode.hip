@@ -2,21 +2,26 @@
 // cache [num_blocks, block_size, Hkv, D].
 //
 // bf16 path.  The key range of every sequence is cut into splits of about
-// kChunk keys (split-KV), so that 256 sequences x 8 KV heads give thousands of
-// independent workgroups and the long and short contexts balance.  A
-// workgroup (4 waves) owns one (split, KV head, sequence) and serves all G
-// query heads of that KV head, so each cached K/V row is read from HBM once.
-// A wave takes 32 keys at a time:
-//   * scores: S^T[key][head] = K Q^T on MFMA 16x16x32 (A = 16 cached K rows
-//     loaded straight from HBM into operand registers, B = the G query rows,
-//     zero-padded to 16 columns);
-//   * online softmax per head in the log2 domain;
-//   * values: lanes own 8 consecutive head-dim columns of one key row (16-byte
-//     coalesced loads) and accumulate p * v in fp32 for the G heads, the
-//     probabilities broadcast through LDS.
-// Each split leaves (max, sum, unnormalized output) in the caller workspace;
-// a second kernel merges the splits of a (sequence, head) in split order, so
-// the result is deterministic.
+// kChunk keys (split-KV), so 256 sequences give thousands of workgroups and
+// long and short contexts balance.  A workgroup of 8 waves owns one (split,
+// sequence, group of up to 8 KV heads): for the 8-head layer every wave takes
+// one KV head and serves all G query heads of that head, so each page of the
+// cache (block_size slots x all heads, contiguous) is streamed by one
+// workgroup in one pass and each K/V row is read from HBM exactly once.
+// Per 32 keys a wave does:
+//   * scores S^T[key][head] = K Q^T on MFMA 16x16x32: A = 16 cached K rows
+//     loaded straight from HBM into operand registers, B = the G query rows
+//     zero-padded to 16 columns;
+//   * online softmax per head in the log2 domain (lazy reference max);
+//   * O[head][d] += P V on MFMA 16x16x32: the S^T accumulator is already the
+//     A operand P (a lane holds one head and 8 keys), and V, DMA'd into LDS
+//     row-major, is read as the B operand with ds_read_b64_tr_b16.
+// The next tile's K and V loads are in flight while the current one is used.
+// Each split leaves (max, sum, unnormalized output) in the caller workspace; a
+// second kernel merges the splits of a (sequence, head) in split order, so the
+// result is deterministic.
+//
+// Keys whose page id is outside [0, num_blocks) are skipped.
 //
 // fp32 path: one wave per (sequence, head), exact expf, no workspace use.
 #include <algorithm>
@@ -30,6 +35,7 @@ namespace {
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr int kChunk = 512;  // nominal keys per split, and keys per page window
 constexpr int kTile = 32;    // keys per wave step
+constexpr int kWaves = 8;    // waves per workgroup
 // Page ids of one window of kChunk keys (any block size >= 1) fit in here.
 constexpr int kMaxPages = kChunk + 1;
 
@@ -46,6 +52,20 @@ __device__ __forceinline__ SplitPlan plan_splits(int n, int max_splits) {
   p.chunk = (per + kTile - 1) / kTile * kTile;
   return p;
 }
+
+typedef short s16x4 __attribute__((ext_vector_type(4)));
+
+// gfx950 transposed LDS read: within each 16-lane group, lane i receives
+// element i % 4 of the 8-byte chunks addressed by lanes 4e + i / 4 (e = 0..3).
+__device__ __forceinline__ u32x2 lds_read_tr16(const OPS_LDS char* p) {
+  const s16x4 v = __builtin_amdgcn_ds_read_tr16_b64_v4i16((OPS_LDS s16x4*)p);
+  return __builtin_bit_cast(u32x2, v);
+}
+
+// V rows in LDS: the 16-byte chunk c of row r sits at chunk c ^ v_swz(r), so
+// the 4 rows x 32 bytes a 16-lane group reads with one transposed read fall
+// into distinct bank groups.
+__device__ __forceinline__ int v_swz(int r) { return (r & 3) << 1; }
 }  // namespace
 
 int32_t decode_max_splits(int32_t max_context_len) {
@@ -57,22 +77,25 @@ size_t decode_workspace_bytes(int32_t B, int32_t Hq, int32_t D, int32_t max_cont
          (size_t)(D + 2);
 }
 
-template <int D, int G>
-__global__ __launch_bounds__(256) void attn_decode_split_kernel(
+// HB: KV heads per workgroup (8 / HB waves share one head's key tiles).
+template <int D, int G, int HB>
+__global__ __launch_bounds__(512) void attn_decode_split_kernel(
     const __bf16* __restrict__ q, const __bf16* __restrict__ kc, const __bf16* __restrict__ vc,
     const int32_t* __restrict__ table, const int32_t* __restrict__ ctx, int Hq, int Hkv,
     int log2bs, int max_blocks, int64_t num_blocks, int max_splits, float scale_log2,
     float* __restrict__ ws_o, float* __restrict__ ws_ml) {
-  constexpr int CPR = D / 8;        // 16-byte chunks per cache row
-  constexpr int RPI = 64 / CPR;     // rows per wave load instruction (V layout)
-  constexpr int KSTEPS = D / 32;    // MFMA k-steps over the head dim
-  constexpr int NV = kTile / RPI;   // V loads per lane per tile
-  __shared__ int32_t pages[kMaxPages];  // physical blocks of the current key window
-  __shared__ float p_lds[4][G][kTile];
-  __shared__ float red_m[4][G], red_l[4][G];
-  __shared__ float red_o[4][G][D];
+  constexpr int CPR = D / 8;             // 16-byte chunks per cache row
+  constexpr int KSTEPS = D / 32;         // MFMA k-steps over the head dim (QK)
+  constexpr int DT = D / 16;             // 16-wide output tiles over the head dim (PV)
+  constexpr int WPH = kWaves / HB;       // waves sharing one head
+  constexpr int VROWS = 64 / CPR;        // V rows per 1 KB wave load
+  constexpr int VLOADS = kTile / VROWS;  // wave loads per V tile
+  constexpr int VBYTES = kTile * D * 2;  // one V tile
+  constexpr float kLazy = 8.f;
+  __shared__ __attribute__((aligned(16))) char vbuf[kWaves][2][VBYTES];
+  __shared__ int32_t pages[kMaxPages];
 
-  const int split = blockIdx.x, g = blockIdx.y, b = blockIdx.z;
+  const int split = blockIdx.x, hg = blockIdx.y, b = blockIdx.z;
   const int bs = 1 << log2bs;
   const int n = min(ctx[b], max_blocks << log2bs);
   const SplitPlan plan = plan_splits(n, max_splits);
@@ -80,24 +103,12 @@ __global__ __launch_bounds__(256) void attn_decode_split_kernel(
   if (split >= plan.splits || k_begin >= n) return;
   const int k_end = min(n, k_begin + plan.chunk);
 
-  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
+  const int g = hg * HB + wave % HB;     // this wave's KV head
+  const int wt = wave / HB;              // its share of the head's key tiles
   const int col = lane & 15, grp = lane >> 4;
   const int64_t row_elems = (int64_t)Hkv * D;
-
-  // Page ids are looked up once per window of kChunk keys (normally the whole
-  // split) and kept in LDS, so the per-tile K/V loads do not wait on a
-  // dependent block-table load.  Invalid ids become -1 (rows of zeros).
-  const int32_t* trow = table + (int64_t)b * max_blocks;
-  int p_first = 0, w_end = 0;
-  auto load_pages = [&](int w0) {
-    w_end = min(k_end, w0 + kChunk);
-    p_first = w0 >> log2bs;
-    const int p_count = ((w_end - 1) >> log2bs) - p_first + 1;
-    for (int i = threadIdx.x; i < p_count; i += 256) {
-      const int blk = trow[p_first + i];
-      pages[i] = (uint32_t)blk < (uint64_t)num_blocks ? blk : -1;
-    }
-  };
+  OPS_LDS char* vb0 = (OPS_LDS char*)vbuf[wave][0];
 
   // Query heads of this group as the MFMA B operand (column = head).
   bf16x8 qf[KSTEPS];
@@ -112,44 +123,59 @@ __global__ __launch_bounds__(256) void attn_decode_split_kernel(
     }
   }
 
-  // address of cache row j (absolute key index) for this KV head, or null
+  // page ids of the current window (-1: not a valid block)
+  const int32_t* trow = table + (int64_t)b * max_blocks;
+  int p_first = 0, w_end = 0;
+  auto load_pages = [&](int w0) {
+    w_end = min(k_end, w0 + kChunk);
+    p_first = w0 >> log2bs;
+    const int p_count = ((w_end - 1) >> log2bs) - p_first + 1;
+    for (int i = threadIdx.x; i < p_count; i += kWaves * 64) {
+      const int blk = trow[p_first + i];
+      pages[i] = (uint32_t)blk < (uint64_t)num_blocks ? blk : -1;
+    }
+  };
+  // A key is used iff it lies in the window and its page is valid.
+  auto key_ok = [&](int j) {
+    return j < w_end && pages[(min(j, w_end - 1) >> log2bs) - p_first] >= 0;
+  };
+  // Cache row of key j for head g.  Skipped keys read the sequence's first
+  // query row instead (finite data; their probability is exactly 0), so every
+  // lane always issues every load and the vmcnt bookkeeping below is exact.
+  const __bf16* dummy = q + (int64_t)b * Hq * D;
   auto row_ptr = [&](const __bf16* cache, int j) -> const __bf16* {
-    if (j >= w_end) return nullptr;
+    if (!key_ok(j)) return dummy;
     const int blk = pages[(j >> log2bs) - p_first];
-    if (blk < 0) return nullptr;
     return cache + ((int64_t)blk * bs + (j & (bs - 1))) * row_elems + (int64_t)g * D;
   };
 
-  // K in MFMA A-operand layout (lane: key col, 8 head-dim values at 32*s + 8*grp)
-  // and V in row layout (lane: key vrow + RPI*i, 8 head-dim values at 8*vchunk).
-  const int vrow = lane / CPR, vchunk = lane % CPR;
-  struct TileRegs {
+  // K of 32 keys in MFMA A-operand layout (registers, 2*KSTEPS loads); V of
+  // the same keys DMA'd into this wave's LDS buffer `stage` (VLOADS loads).
+  struct KRegs {
     u32x4 k[2][KSTEPS];
-    u32x4 v[NV];
   };
-  auto load_tile = [&](int t0, TileRegs& r) {
+  auto load_tile = [&](int t0, KRegs& r, int stage) {
 #pragma unroll
     for (int sub = 0; sub < 2; ++sub) {
       const __bf16* kr = row_ptr(kc, t0 + sub * 16 + col);
 #pragma unroll
-      for (int s = 0; s < KSTEPS; ++s)
-        r.k[sub][s] = kr ? *reinterpret_cast<const u32x4*>(kr + s * 32 + grp * 8) : u32x4{0u, 0u, 0u, 0u};
+      for (int s = 0; s < KSTEPS; ++s) r.k[sub][s] = *reinterpret_cast<const u32x4*>(kr + s * 32 + grp * 8);
     }
+    OPS_LDS char* vb = vb0 + stage * VBYTES;
 #pragma unroll
-    for (int i = 0; i < NV; ++i) {
-      const __bf16* vr = row_ptr(vc, t0 + i * RPI + vrow);
-      r.v[i] = vr ? *reinterpret_cast<const u32x4*>(vr + vchunk * 8) : u32x4{0u, 0u, 0u, 0u};
+    for (int i = 0; i < VLOADS; ++i) {
+      const int row = i * VROWS + lane / CPR;
+      const int c = (lane % CPR) ^ v_swz(row);  // logical chunk landing at this lane's slot
+      global_load16_lds(row_ptr(vc, t0 + row) + c * 8, vb + i * 1024);
     }
   };
 
-  float m_run = -INFINITY, l_run = 0.f;  // for head `col` (lanes col < G meaningful)
-  float acc[G][8];
+  float m_run = -INFINITY, l_run = 0.f;  // softmax state of head `col` (lanes col < G)
+  f32x4 acc[DT];                          // O[head 4*grp + r][d = 16*dt + col]
 #pragma unroll
-  for (int hh = 0; hh < G; ++hh)
-#pragma unroll
-    for (int e = 0; e < 8; ++e) acc[hh][e] = 0.f;
+  for (int i = 0; i < DT; ++i) acc[i] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  auto compute_tile = [&](int t0, const TileRegs& r) {
+  auto compute_tile = [&](int t0, const KRegs& r, int stage) {
     // scores S^T[key][head]: lane holds head `col`, keys t0 + 16*sub + 4*grp + rr
     f32x4 st[2];
 #pragma unroll
@@ -166,16 +192,21 @@ __global__ __launch_bounds__(256) void attn_decode_split_kernel(
 #pragma unroll
       for (int rr = 0; rr < 4; ++rr) {
         const int j = t0 + sub * 16 + grp * 4 + rr;
-        const float sv = j < w_end ? st[sub][rr] * scale_log2 : -INFINITY;
+        const float sv = key_ok(j) ? st[sub][rr] * scale_log2 : -INFINITY;
         st[sub][rr] = sv;
         tmax = fmaxf(tmax, sv);
       }
     tmax = fmaxf(tmax, __shfl_xor(tmax, 16, 64));
     tmax = fmaxf(tmax, __shfl_xor(tmax, 32, 64));
-    const float m_new = fmaxf(m_run, tmax);
-    const float m_use = m_new == -INFINITY ? 0.f : m_new;
-    const float alpha = fast_exp2(m_run - m_use);
-    m_run = m_new;
+    // move the reference max only when the tile's max exceeds it by kLazy
+    float alpha = 1.f;
+    if (tmax > m_run + kLazy) {
+      alpha = fast_exp2(m_run - tmax);
+      m_run = tmax;
+    }
+    const float m_use = m_run == -INFINITY ? 0.f : m_run;
+    // P as the MFMA A operand: slot e of lane (col, grp) is key 4*grp + e%4 + 16*(e/4)
+    bf16x8 pa;
     float psum = 0.f;
 #pragma unroll
     for (int sub = 0; sub < 2; ++sub)
@@ -183,100 +214,113 @@ __global__ __launch_bounds__(256) void attn_decode_split_kernel(
       for (int rr = 0; rr < 4; ++rr) {
         const float p = fast_exp2(st[sub][rr] - m_use);
         psum += p;
-        if (col < G) p_lds[wave][col][sub * 16 + grp * 4 + rr] = p;
+        pa[sub * 4 + rr] = (__bf16)p;
       }
     psum += __shfl_xor(psum, 16, 64);
     psum += __shfl_xor(psum, 32, 64);
     l_run = l_run * alpha + psum;
+    // rescale O rows (heads 4*grp + r) when any head's reference moved
+    if (__builtin_amdgcn_ballot_w64(alpha != 1.f)) {
 #pragma unroll
-    for (int hh = 0; hh < G; ++hh) {
-      const float a = __shfl(alpha, hh, 64);
+      for (int rr = 0; rr < 4; ++rr) {
+        const float a = __shfl(alpha, grp * 4 + rr, 64);
 #pragma unroll
-      for (int e = 0; e < 8; ++e) acc[hh][e] *= a;
-    }
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-    __builtin_amdgcn_wave_barrier();
-    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-    // values: acc[hh][e] += p[hh][key] * v[key][vchunk*8 + e]
-#pragma unroll
-    for (int i = 0; i < NV; ++i) {
-      const int kl = i * RPI + vrow;
-      float vf[8];
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        vf[2 * e] = bf_lo(r.v[i][e]);
-        vf[2 * e + 1] = bf_hi(r.v[i][e]);
-      }
-#pragma unroll
-      for (int hh = 0; hh < G; ++hh) {
-        const float p = p_lds[wave][hh][kl];
-#pragma unroll
-        for (int e = 0; e < 8; ++e) acc[hh][e] = fmaf(p, vf[e], acc[hh][e]);
+        for (int i = 0; i < DT; ++i) acc[i][rr] *= a;
       }
     }
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-    __builtin_amdgcn_wave_barrier();
-    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    // V as the B operand: lane (d = 16*dt + col, group grp) needs keys
+    // 4*grp + e (e < 4) and 16 + 4*grp + (e - 4); one transposed read each.
+    const OPS_LDS char* vb = vb0 + stage * VBYTES;
+    const int trow0 = 4 * grp + (col >> 2);
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt) {
+      const int cc = dt * 16 + 4 * (col & 3);  // head-dim column of this lane's 8-byte chunk
+      const int c16 = cc >> 3, half = (cc >> 2) & 1;
+      const int r0 = trow0, r1 = trow0 + 16;
+      const u32x2 lo = lds_read_tr16(vb + r0 * (D * 2) + ((c16 ^ v_swz(r0)) << 4) + half * 8);
+      const u32x2 hi = lds_read_tr16(vb + r1 * (D * 2) + ((c16 ^ v_swz(r1)) << 4) + half * 8);
+      const bf16x8 vf = __builtin_bit_cast(bf16x8, u32x4{lo[0], lo[1], hi[0], hi[1]});
+      acc[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(pa, vf, acc[dt], 0, 0, 0);
+    }
   };
 
-  // Software pipeline: the loads of the wave's next tile are in flight while
-  // the current one is scored and accumulated.
-  TileRegs cur, nxt;
+  // Software pipeline over this wave's tiles of each key window.
+  KRegs cur, nxt;
+  int stage = 0;
   for (int w0 = k_begin; w0 < k_end; w0 += kChunk) {
     if (w0 != k_begin) __syncthreads();  // every wave is done with the previous window
     load_pages(w0);
     __syncthreads();
-    int t0 = w0 + wave * kTile;
-    if (t0 < w_end) load_tile(t0, cur);
+    int t0 = w0 + wt * kTile;
+    if (t0 < w_end) load_tile(t0, cur, stage);
     while (t0 < w_end) {
-      const int t1 = t0 + 4 * kTile;
-      if (t1 < w_end) load_tile(t1, nxt);
-      compute_tile(t0, cur);
+      const int t1 = t0 + WPH * kTile;
+      if (t1 < w_end) {
+        load_tile(t1, nxt, stage ^ 1);
+        wait_vmcnt_le<KSTEPS * 2 + VLOADS>();  // this tile's loads landed, the next may fly
+      } else {
+        wait_vmem();
+      }
+      compute_tile(t0, cur, stage);
       cur = nxt;
+      stage ^= 1;
       t0 = t1;
     }
   }
 
-  // ---- merge the lanes that hold different keys of the same columns
+  // ---- merge the waves sharing a head (WPH > 1) through LDS, write partials
+  // acc[dt][rr]: head 4*grp + rr, d = 16*dt + col.
+  const int64_t slot_base = (int64_t)b * Hq * max_splits + split;
+  if constexpr (WPH == 1) {
 #pragma unroll
-  for (int hh = 0; hh < G; ++hh)
+    for (int rr = 0; rr < 4; ++rr) {
+      const int hh = 4 * grp + rr;
+      if (hh < G) {
+        const int64_t slot = slot_base + (int64_t)(g * G + hh) * max_splits;
 #pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      float a = acc[hh][e];
-#pragma unroll
-      for (int off = CPR; off < 64; off <<= 1) a += __shfl_xor(a, off, 64);
-      acc[hh][e] = a;
+        for (int dt = 0; dt < DT; ++dt) ws_o[slot * D + dt * 16 + col] = acc[dt][rr];
+      }
     }
-  if (lane < CPR) {
-#pragma unroll
-    for (int hh = 0; hh < G; ++hh)
-#pragma unroll
-      for (int e = 0; e < 8; ++e) red_o[wave][hh][lane * 8 + e] = acc[hh][e];
-  }
-  if (lane < G) {
-    red_m[wave][lane] = m_run;
-    red_l[wave][lane] = l_run;
-  }
-  __syncthreads();
-  // ---- merge the 4 waves and write this split's partial result
-  for (int idx = threadIdx.x; idx < G * D; idx += 256) {
-    const int hh = idx / D, d = idx % D;
-    float M = -INFINITY;
-#pragma unroll
-    for (int w = 0; w < 4; ++w) M = fmaxf(M, red_m[w][hh]);
-    float o = 0.f, l = 0.f;
-#pragma unroll
-    for (int w = 0; w < 4; ++w) {
-      const float f = red_m[w][hh] == -INFINITY ? 0.f : fast_exp2(red_m[w][hh] - M);
-      o += f * red_o[w][hh][d];
-      l += f * red_l[w][hh];
+    if (col < G) {
+      const int64_t slot = slot_base + (int64_t)(g * G + col) * max_splits;
+      if (grp == 0) {
+        ws_ml[slot * 2 + 0] = m_run;
+        ws_ml[slot * 2 + 1] = l_run;
+      }
     }
-    const int h = g * G + hh;
-    const int64_t slot = ((int64_t)b * Hq + h) * max_splits + split;
-    ws_o[slot * D + d] = o;
-    if (d == 0) {
-      ws_ml[slot * 2 + 0] = M;
-      ws_ml[slot * 2 + 1] = l;
+  } else {
+    __syncthreads();  // the V buffers are reused for the merge
+    float* red = reinterpret_cast<float*>(vbuf);  // [wave][G][D + 2]
+    float* mine = red + wave * G * (D + 2);
+#pragma unroll
+    for (int rr = 0; rr < 4; ++rr) {
+      const int hh = 4 * grp + rr;
+      if (hh < G)
+#pragma unroll
+        for (int dt = 0; dt < DT; ++dt) mine[hh * (D + 2) + dt * 16 + col] = acc[dt][rr];
+    }
+    if (col < G && grp == 0) {
+      mine[col * (D + 2) + D] = m_run;
+      mine[col * (D + 2) + D + 1] = l_run;
+    }
+    __syncthreads();
+    for (int idx = threadIdx.x; idx < HB * G * D; idx += kWaves * 64) {
+      const int hl = idx / (G * D), hh = (idx / D) % G, d = idx % D;  // head slot, query head, column
+      float M = -INFINITY;
+      for (int w = 0; w < WPH; ++w) M = fmaxf(M, red[((w * HB + hl) * G + hh) * (D + 2) + D]);
+      float o = 0.f, l = 0.f;
+      for (int w = 0; w < WPH; ++w) {
+        const float* e = red + ((w * HB + hl) * G + hh) * (D + 2);
+        const float f = e[D] == -INFINITY ? 0.f : fast_exp2(e[D] - M);
+        o += f * e[d];
+        l += f * e[D + 1];
+      }
+      const int64_t slot = slot_base + (int64_t)((hg * HB + hl) * G + hh) * max_splits;
+      ws_o[slot * D + d] = o;
+      if (d == 0) {
+        ws_ml[slot * 2 + 0] = M;
+        ws_ml[slot * 2 + 1] = l;
+      }
     }
   }
 }
@@ -297,7 +341,9 @@ __global__ __launch_bounds__(64) void attn_decode_combine_kernel(
   float l = 0.f;
   for (int s = 0; s < plan.splits; ++s) {
     if (s * plan.chunk >= n) continue;
-    const float f = fast_exp2(ws_ml[(slot0 + s) * 2] - M);
+    const float ms = ws_ml[(slot0 + s) * 2];
+    if (ms == -INFINITY) continue;  // every key of the split was skipped
+    const float f = fast_exp2(ms - M);
     l += f * ws_ml[(slot0 + s) * 2 + 1];
 #pragma unroll
     for (int c = 0; c < D / 64; ++c) acc[c] += f * ws_o[(slot0 + s) * D + lane + c * 64];
@@ -327,21 +373,22 @@ __global__ __launch_bounds__(64) void attn_decode_f32_kernel(
   float m_run = -INFINITY, l_run = 0.f, acc[DPL] = {};
   for (int kv0 = 0; kv0 < n; kv0 += 64) {
     const int j = kv0 + lane;
-    float s = -INFINITY;
+    float s = -INFINITY;  // keys in invalid pages are skipped
     int64_t row = -1;
     if (j < n) {
       const int blk = trow[j >> log2bs];
-      if ((uint32_t)blk < (uint64_t)num_blocks)
+      if ((uint32_t)blk < (uint64_t)num_blocks) {
         row = (((int64_t)blk * bs + (j & (bs - 1))) * Hkv + g) * D;
-      float dot = 0.f;
-      if (row >= 0)
+        float dot = 0.f;
         for (int d = 0; d < D; ++d) dot = fmaf(qs[d], kc[row + d], dot);
-      s = dot * scale;
+        s = dot * scale;
+      }
     }
     rows[lane] = row;
     const float m_new = fmaxf(m_run, wave_max(s));
-    const float p = j < n ? expf(s - m_new) : 0.f;
-    const float alpha = expf(m_run - m_new);
+    const float m_use = m_new == -INFINITY ? 0.f : m_new;
+    const float p = row >= 0 ? expf(s - m_use) : 0.f;
+    const float alpha = expf(m_run - m_use);
     l_run = l_run * alpha + wave_sum(p);
     m_run = m_new;
     ps[lane] = p;
@@ -385,20 +432,28 @@ hipError_t launch_attn_decode(const void* q, const void* kcache, const void* vca
   const int max_splits = decode_max_splits(max_context_len);
   float* ws_o = static_cast<float*>(ws);
   float* ws_ml = ws_o + (size_t)B * Hq * max_splits * D;
-  const dim3 grid((unsigned)max_splits, (unsigned)Hkv, (unsigned)B);
   const float sl2 = scale * kLog2e;
   const int G = Hq / Hkv;
-#define OPS_DEC(DD, GG)                                                                          \
-  hipLaunchKernelGGL((attn_decode_split_kernel<DD, GG>), grid, dim3(256), 0, s,                  \
-                     static_cast<const __bf16*>(q), static_cast<const __bf16*>(kcache),          \
+  const int HB = Hkv >= 8 ? 8 : Hkv;  // KV heads per workgroup (Hkv in {1, 2, 4} or a multiple of 8)
+  const dim3 grid((unsigned)max_splits, (unsigned)(Hkv / HB), (unsigned)B);
+#define OPS_DEC(DD, GG, HH)                                                                     \
+  hipLaunchKernelGGL((attn_decode_split_kernel<DD, GG, HH>), grid, dim3(kWaves * 64), 0, s,     \
+                     static_cast<const __bf16*>(q), static_cast<const __bf16*>(kcache),         \
                      static_cast<const __bf16*>(vcache), table, ctx, Hq, Hkv, log2bs, max_blocks, \
                      num_blocks, max_splits, sl2, ws_o, ws_ml)
-#define OPS_DEC_G(DD)                 \
-  switch (G) {                        \
-    case 1: OPS_DEC(DD, 1); break;    \
-    case 2: OPS_DEC(DD, 2); break;    \
-    case 4: OPS_DEC(DD, 4); break;    \
-    default: OPS_DEC(DD, 8); break;   \
+#define OPS_DEC_H(DD, GG)                    \
+  switch (HB) {                              \
+    case 1: OPS_DEC(DD, GG, 1); break;       \
+    case 2: OPS_DEC(DD, GG, 2); break;       \
+    case 4: OPS_DEC(DD, GG, 4); break;       \
+    default: OPS_DEC(DD, GG, 8); break;      \
+  }
+#define OPS_DEC_G(DD)                   \
+  switch (G) {                          \
+    case 1: OPS_DEC_H(DD, 1) break;     \
+    case 2: OPS_DEC_H(DD, 2) break;     \
+    case 4: OPS_DEC_H(DD, 4) break;     \
+    default: OPS_DEC_H(DD, 8) break;    \
   }
   if (D == 128) {
     OPS_DEC_G(128)
@@ -406,6 +461,7 @@ hipError_t launch_attn_decode(const void* q, const void* kcache, const void* vca
     OPS_DEC_G(64)
   }
 #undef OPS_DEC_G
+#undef OPS_DEC_H
 #undef OPS_DEC
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
