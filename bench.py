@@ -44,16 +44,17 @@ def source_sha(kernel: str) -> str:
         return hashlib.sha256(f.read()).hexdigest()[:16]
 
 
-def measured_traffic(kernel: str, launches_per_unit=1):
-    """HBM bytes per launch from the committed counter summary, or None when
-    the kernel source changed since the counters were taken."""
+def measured_traffic(op: str, kernel: str):
+    """HBM bytes per launch of `op` (FETCH_SIZE + WRITE_SIZE, calibrated) from
+    the committed counter summary, or None when the kernel's source changed
+    since the counters were taken."""
     try:
         with open(TRAFFIC_FILE) as f:
             t = json.load(f)
     except (OSError, ValueError):
         return None
-    e = t.get(kernel)
-    if not e or e.get("source_sha") != source_sha(kernel):
+    e = t.get("ops", {}).get(op)
+    if not e or e.get("kernel") != kernel or e.get("source_sha") != source_sha(kernel):
         return None
     return e.get("bytes_per_launch")
 
@@ -285,7 +286,7 @@ def main():
     else:
         roof = {"bound": "hbm", "achieved": round(by / t_dom * 1e-9, 1), "peak": PEAK_HBM * 1e-9, "unit": "GB/s"}
     roof["frac"] = round(roof["achieved"] / roof["peak"], 4)
-    roof["traffic"] = measured_traffic(kernel)
+    roof["traffic"] = measured_traffic(dom, kernel)
     roof["kernel"] = f"{kernel} ({dom})"
     roof["work_per_launch"] = {"flops": fl, "bytes": by}
     M = layer.p["M"]

@@ -16,6 +16,8 @@
 // m and runs of 4 consecutive columns n, stored as 8-byte chunks.
 //
 // fp32 path: a plain LDS-tiled FMA kernel (exact fp32 products and sums).
+#include <algorithm>
+
 #include "common.h"
 #include "launch.h"
 
@@ -53,7 +55,6 @@ using CfgDeep8I = GemmCfg<256, 256, 32, 2, 4, 4, true>;
 using CfgMid = GemmCfg<256, 128, 64, 2, 2, 3>;     // 4 waves of 128x64, 3 x 48 KB stages
 using CfgMidI = GemmCfg<256, 128, 64, 2, 2, 3, true>;
 
-constexpr int kGroupM = 8;  // tile rows per L2 group
 
 // 16-byte chunk c of LDS row r is stored at physical chunk c ^ swz(r).  For
 // any 8 consecutive rows (a 32-bank view of LDS) and any 16 consecutive rows
@@ -107,7 +108,7 @@ __global__ __launch_bounds__(C::kThreads, 1) void gemm_bf16_kernel(const __bf16*
                                                                    const __bf16* __restrict__ W,
                                                                    const __bf16* __restrict__ bias,
                                                                    __bf16* __restrict__ y, int M, int N,
-                                                                   int K) {
+                                                                   int K, int group_m) {
   extern __shared__ __attribute__((aligned(16))) char smem_raw[];
   OPS_LDS char* smem = (OPS_LDS char*)smem_raw;
   constexpr int BM = C::BM, BN = C::BN, BK = C::BK, WM = C::WM, WN = C::WN, S = C::STAGES;
@@ -115,11 +116,13 @@ __global__ __launch_bounds__(C::kThreads, 1) void gemm_bf16_kernel(const __bf16*
 
   const int tiles_m = (M + BM - 1) / BM, tiles_n = (N + BN - 1) / BN;
   const uint32_t tid = xcd_remap(blockIdx.x, (uint32_t)(tiles_m * tiles_n));
-  // grouped order: kGroupM tile-rows sweep the tile-columns together
-  const int group = tid / (kGroupM * tiles_n);
-  const int first_m = group * kGroupM;
-  const int gsize = min(tiles_m - first_m, kGroupM);
-  const int in_group = tid % (kGroupM * tiles_n);
+  // grouped order: group_m tile-rows sweep the tile-columns together, so a
+  // W column-block is fetched once per group and reused from L2 / MALL by
+  // every tile-row of the group while the group's x rows stay cache resident
+  const int group = tid / (group_m * tiles_n);
+  const int first_m = group * group_m;
+  const int gsize = min(tiles_m - first_m, group_m);
+  const int in_group = tid % (group_m * tiles_n);
   const int tm = first_m + in_group % gsize, tn = in_group / gsize;
   const int m0 = tm * BM, n0 = tn * BN;
 
@@ -313,10 +316,18 @@ static hipError_t launch_gemm_bf16(const void* x, const void* W, const void* bia
       reinterpret_cast<const void*>(gemm_bf16_kernel<C>), hipFuncAttributeMaxDynamicSharedMemorySize,
       C::kLdsBytes);
   if (attr != hipSuccess) return attr;
-  const int64_t tiles = ((M + C::BM - 1) / C::BM) * ((N + C::BN - 1) / C::BN);
+  const int64_t tiles_m = (M + C::BM - 1) / C::BM;
+  const int64_t tiles = tiles_m * ((N + C::BN - 1) / C::BN);
+  // Tile-rows per group: as many as keep the group's x rows (BM x K bf16 each)
+  // within 16 MB, so they stay in the last-level cache while the group sweeps
+  // the tile-columns; at least one, at most all.
+  constexpr int64_t kGroupBytes = 16ll << 20;
+  const int64_t row_block_bytes = (int64_t)C::BM * K * 2;
+  const int group_m = (int)std::max<int64_t>(1, std::min<int64_t>(tiles_m, kGroupBytes / row_block_bytes));
   hipLaunchKernelGGL((gemm_bf16_kernel<C>), dim3((unsigned)tiles), dim3(C::kThreads), C::kLdsBytes, s,
                      static_cast<const __bf16*>(x), static_cast<const __bf16*>(W),
-                     static_cast<const __bf16*>(bias), static_cast<__bf16*>(y), (int)M, (int)N, (int)K);
+                     static_cast<const __bf16*>(bias), static_cast<__bf16*>(y), (int)M, (int)N, (int)K,
+                     group_m);
   return hipGetLastError();
 }
 
