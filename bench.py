@@ -31,6 +31,7 @@ TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_counters.json")
 KERNEL_SOURCES = {"gemm_bf16_kernel": "paper_2608_13499_amd/csrc/k_gemm.hip",
                   "attn_prefill_bf16_kernel": "paper_2608_13499_amd/csrc/k_attn_prefill.hip",
                   "attn_decode_split_kernel": "paper_2608_13499_amd/csrc/k_attn_decode.hip",
+                  "attn_decode_combine_kernel": "paper_2608_13499_amd/csrc/k_attn_decode.hip",
                   "rmsnorm_kernel": "paper_2608_13499_amd/csrc/k_norm_act.hip",
                   "swiglu_kernel": "paper_2608_13499_amd/csrc/k_norm_act.hip"}
 
@@ -40,8 +41,15 @@ def log(*a):
 
 
 def source_sha(kernel: str) -> str:
-    with open(os.path.join(ROOT, KERNEL_SOURCES[kernel]), "rb") as f:
-        return hashlib.sha256(f.read()).hexdigest()[:16]
+    """Hash of the kernel's source file with comments and whitespace removed,
+    so that only a change of the code itself invalidates its counters."""
+    import re
+    with open(os.path.join(ROOT, KERNEL_SOURCES[kernel])) as f:
+        src = f.read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    src = re.sub(r"//[^\n]*", "", src)
+    src = "".join(src.split())
+    return hashlib.sha256(src.encode()).hexdigest()[:16]
 
 
 def measured_traffic(op: str, kernel: str):

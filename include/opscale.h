@@ -4,7 +4,7 @@
  *
  * The paper treats an LLM as a dataflow of operators that are profiled,
  * provisioned and scaled one by one (Section 2.2 "Rethinking the Scaling
- * Unit"; Section 4 "Operator Profiling").  Each entry point below is one such
+ * Unit"; Section 4.2 "Operator Profiling").  Each entry point below is one such
  * operator of a Llama-style decoder layer: RMS Norm, the QKV / O / gate-up /
  * down linears, the fused SiLU-multiply activation, causal grouped-query
  * prefill attention over a ragged batch of prompts, and decode attention over a
@@ -12,7 +12,7 @@
  * with device events around the launches and excluding host overhead (Section
  * 2.1 "Compute Sensitivity"), together with the operator's algorithmic flops
  * and bytes, the inputs of the profiler's T_v / M_v / C_v tables (Section 3.1,
- * Section 4).
+ * Section 4.2).
  *
  * Conventions shared by every entry point
  *  - Pointers: all tensor pointers are DEVICE pointers to caller-owned memory,
@@ -169,7 +169,7 @@ opscale_status opscale_attn_decode(const void* q, const void* k_cache, const voi
                                    hipStream_t stream, opscale_timing* timing);
 
 /* ---------------------------------------------------------------------------
- * Operator profiling (Section 4 "Operator Profiling": per-operator compute
+ * Operator profiling (Section 4.2 "Operator Profiling": per-operator compute
  * time T_v and memory M_v; Appendix C "Dataflow Characteristics": the payload
  * an operator hands to the next one, the basis of C_v).
  * ------------------------------------------------------------------------- */

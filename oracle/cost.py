@@ -2,7 +2,7 @@
 
 The paper's Operator Profiler records, per operator, its compute time T_v, its
 memory M_v (weights vs. transient tensors) and its communication C_v, the
-payload handed to the next operator (Section 4, "Operator Profiling"; Section
+payload handed to the next operator (Section 4.2, "Operator Profiling"; Section
 2.1 "Memory Sensitivity"; Appendix C "Dataflow Characteristics").  The counts
 below are what each operator must compute or move at minimum: each input read
 once, each output written once, weights read once, K/V read once per KV head

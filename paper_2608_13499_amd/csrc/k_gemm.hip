@@ -4,11 +4,12 @@
 // bf16 path: MFMA v_mfma_f32_32x32x16_bf16, fp32 accumulation.  A 256x256
 // block tile is staged through an LDS ring in BK-wide K slices; the next slices
 // are fetched with buffer_load ... lds (HBM/L2 -> LDS without passing through
-// registers) while the current one feeds the matrix cores.  Four waves own
-// 128x128 sub-tiles each, so every 16-byte LDS fragment read feeds four
-// MFMAs (LDS read traffic is half that of 128x64 wave tiles).  Rows and
-// K columns beyond the matrix read as zeros through the buffer descriptor's
-// range check, so ragged M, N and K need no separate code path.
+// registers) while the current one feeds the matrix cores.  Large problems
+// use eight waves of 128x64 sub-tiles (two waves per SIMD, so one wave's LDS
+// reads overlap the other's MFMAs); problems with fewer than 256 such tiles
+// use a 256x128 tile of four waves, which doubles the workgroup count.  Rows
+// and K columns beyond the matrix read as zeros through the buffer
+// descriptor's range check, so ragged M, N and K need no separate code path.
 //
 // Both operands are K-contiguous, which is what an MFMA operand lane wants: a
 // lane holds 8 consecutive k of one row.  The W tile is the MFMA "A" operand
