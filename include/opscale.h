@@ -90,6 +90,8 @@ opscale_status opscale_rmsnorm(const void* x, const void* w, void* y, int64_t M,
  * x: [M, K]; W: [N, K] (the nn.Linear weight layout); bias: [N] or NULL;
  * y: [M, N], must not alias x or W.  bf16: MFMA with fp32 accumulation.
  * K * sizeof(dt) and N * sizeof(dt) must be multiples of 16.
+ * The bf16 block tile (256x256, 192x256 or 256x128) is chosen per shape; the
+ * environment variable OPSCALE_GEMM_TILE set to one of those names forces it.
  */
 opscale_status opscale_linear(const void* x, const void* W, const void* bias, void* y,
                               int64_t M, int64_t N, int64_t K, opscale_dtype dt,

@@ -18,6 +18,9 @@
 //
 // fp32 path: a plain LDS-tiled FMA kernel (exact fp32 products and sums).
 #include <algorithm>
+#include <cstdio>
+#include <cstdlib>
+#include <cstring>
 
 #include "common.h"
 #include "launch.h"
@@ -26,12 +29,13 @@ namespace opscale {
 
 namespace {
 
+constexpr int kNumCUs = 256;  // MI355X compute units
+
 // Tile configuration: BM x BN block tile, K in slices of BK, WGM x WGN waves
 // (each owns a (BM/WGM) x (BN/WGN) sub-tile), STAGES-deep LDS ring.
-template <int BM_, int BN_, int BK_, int WGM_, int WGN_, int STAGES_, bool INTERLEAVE_ = false>
+template <int BM_, int BN_, int BK_, int WGM_, int WGN_, int STAGES_>
 struct GemmCfg {
   static constexpr int BM = BM_, BN = BN_, BK = BK_, WGM = WGM_, WGN = WGN_, STAGES = STAGES_;
-  static constexpr bool INTERLEAVE = INTERLEAVE_;
   static constexpr int WM = BM / WGM, WN = BN / WGN;  // wave tile (m x n)
   static constexpr int kThreads = WGM * WGN * 64;
   static constexpr int kWaves = WGM * WGN;
@@ -47,14 +51,9 @@ struct GemmCfg {
   static_assert(kLoadsPerTile * (STAGES - 2 > 0 ? STAGES - 2 : 0) <= 63, "vmcnt range");
 };
 
-using CfgBig = GemmCfg<256, 256, 64, 2, 2, 2>;     // 4 waves of 128x128, 2 x 64 KB stages
 using CfgBig8 = GemmCfg<256, 256, 64, 2, 4, 2>;    // 8 waves of 128x64, 2 x 64 KB stages
-using CfgDeep = GemmCfg<256, 256, 32, 2, 2, 4>;    // 4 waves of 128x128, 4 x 32 KB stages
-using CfgDeep8 = GemmCfg<256, 256, 32, 2, 4, 4>;   // 8 waves of 128x64, 4 x 32 KB stages
-using CfgDeepI = GemmCfg<256, 256, 32, 2, 2, 4, true>;
-using CfgDeep8I = GemmCfg<256, 256, 32, 2, 4, 4, true>;
+using CfgT192 = GemmCfg<192, 256, 64, 2, 4, 2>;    // 8 waves of 96x64, 2 x 56 KB stages
 using CfgMid = GemmCfg<256, 128, 64, 2, 2, 3>;     // 4 waves of 128x64, 3 x 48 KB stages
-using CfgMidI = GemmCfg<256, 128, 64, 2, 2, 3, true>;
 
 
 // 16-byte chunk c of LDS row r is stored at physical chunk c ^ swz(r).  For
@@ -176,32 +175,32 @@ __global__ __launch_bounds__(C::kThreads, 1) void gemm_bf16_kernel(const __bf16*
       for (int j = 0; j < TM; ++j)
         acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[buf][i], b[buf][j], acc[i][j], 0, 0, 0);
   };
-  // Interleave the next fragment reads between this step's MFMAs (one read
-  // after each MFMA until the reads run out, then the remaining MFMAs).
-  auto schedule = [&]() {
-    if constexpr (C::INTERLEAVE) {
-      constexpr int R = TN + TM, MF = TN * TM;
-#pragma unroll
-      for (int i = 0; i < (R < MF ? R : MF); ++i) {
-        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // MFMA
-        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // DS read
-      }
-      if constexpr (MF > R) __builtin_amdgcn_sched_group_barrier(0x008, MF - R, 0);
-    }
-  };
 
   if constexpr (S == 2) {
+    // Slice kt + 1 is made visible before the last k-step of slice kt: that
+    // step already reads slice kt + 1's first fragments, and the MFMAs issued
+    // just before the barrier keep the matrix cores busy while the waves
+    // meet.  Slice kt + 2 is then loaded into the stage slice kt used (every
+    // wave has read its last fragments of it before the barrier).
+    wait_vmcnt<0>();
+    __syncthreads();
+    if (nk > 1) load(1);
+    frags(smem, 0, 0);
     for (int kt = 0; kt < nk; ++kt) {
-      wait_vmcnt<0>();
-      __syncthreads();
-      if (kt + 1 < nk) load(kt + 1);
-      const OPS_LDS char* st = smem + (kt % S) * C::kStageBytes;
-      frags(st, 0, 0);
+      const OPS_LDS char* st = smem + (kt & 1) * C::kStageBytes;
+      const OPS_LDS char* st_next = smem + ((kt + 1) & 1) * C::kStageBytes;
 #pragma unroll
       for (int ks = 0; ks < KS; ++ks) {
-        if (ks + 1 < KS) frags(st, ks + 1, (ks + 1) & 1);
+        const int nb = (ks + 1) & 1;
+        if (ks + 1 < KS) {
+          frags(st, ks + 1, nb);
+        } else if (kt + 1 < nk) {
+          wait_vmcnt<0>();
+          __syncthreads();
+          if (kt + 2 < nk) load(kt + 2);
+          frags(st_next, 0, nb);
+        }
         mfmas(ks & 1);
-        schedule();
       }
     }
   } else {
@@ -225,7 +224,6 @@ __global__ __launch_bounds__(C::kThreads, 1) void gemm_bf16_kernel(const __bf16*
         if (ks + 1 < KS) frags(st, ks + 1, nb);
         else if (kt + 1 < nk) frags(st_next, 0, nb);
         mfmas(ks & 1);
-        schedule();
       }
     }
   }
@@ -338,10 +336,30 @@ hipError_t launch_linear(const void* x, const void* W, const void* bias, void* y
   if (bf16) return launch_gemm_bf16<OPSCALE_GEMM_CFG>(x, W, bias, y, M, N, K, s);
 #else
   if (bf16) {
-    // 256x256 tiles when they fill the 256 CUs; otherwise the 256x128 tile
-    // doubles the number of workgroups (decode-sized M).
-    const int64_t big_tiles = ((M + 255) / 256) * ((N + 255) / 256);
-    if (big_tiles >= 256) return launch_gemm_bf16<CfgBig8>(x, W, bias, y, M, N, K, s);
+    // One workgroup per CU at a time, so a launch runs in ceil(tiles / 256)
+    // rounds.  Pick the tile whose rounds x tile area x relative per-element
+    // cost is smallest: 256x256 moves the fewest operand bytes per flop,
+    // 192x256 (about 15 % more per element) and 256x128 (about 30 % more)
+    // fill the last round better when 256x256 would leave it mostly idle.
+    struct Choice { int bm, bn; double cost; };
+    const Choice choices[] = {{256, 256, 1.0}, {192, 256, 1.15}, {256, 128, 1.3}};
+    int best = 0;
+    double best_t = 0;
+    // OPSCALE_GEMM_TILE=256x256 | 192x256 | 256x128 forces a tile (tuning
+    // and tests); anything else is ignored.
+    const char* force = getenv("OPSCALE_GEMM_TILE");
+    for (int c = 0; c < 3; ++c) {
+      if (force) {
+        char name[16];
+        snprintf(name, sizeof name, "%dx%d", choices[c].bm, choices[c].bn);
+        if (strcmp(force, name) == 0) { best = c; break; }
+      }
+      const int64_t tiles = ((M + choices[c].bm - 1) / choices[c].bm) * ((N + choices[c].bn - 1) / choices[c].bn);
+      const double t = (double)((tiles + kNumCUs - 1) / kNumCUs) * choices[c].bm * choices[c].bn * choices[c].cost;
+      if (c == 0 || t < best_t) { best = c; best_t = t; }
+    }
+    if (best == 0) return launch_gemm_bf16<CfgBig8>(x, W, bias, y, M, N, K, s);
+    if (best == 1) return launch_gemm_bf16<CfgT192>(x, W, bias, y, M, N, K, s);
     return launch_gemm_bf16<CfgMid>(x, W, bias, y, M, N, K, s);
   }
 #endif

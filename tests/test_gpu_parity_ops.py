@@ -72,6 +72,22 @@ def test_linear(ops, dtype, M, N, K, bias):
     assert_close(f64(y.cpu()), oracle.linear(f64(x), f64(W), None if b is None else f64(b)), dtype, "linear")
 
 
+@pytest.mark.parametrize("tile", ["256x256", "192x256", "256x128"])
+@pytest.mark.parametrize("M,N,K,bias", [(300, 264, 200, True), (513, 1024, 4096, False), (1, 256, 64, False),
+                                        (700, 520, 136, False)])
+def test_linear_each_tile(ops, monkeypatch, tile, M, N, K, bias):
+    """Every bf16 tile shape the dispatcher can pick, with ragged M, N and K."""
+    import torch
+    say(f"linear bf16 tile={tile} M={M} N={N} K={K} bias={bias}")
+    monkeypatch.setenv("OPSCALE_GEMM_TILE", tile)
+    x = gen(23, "x", (M, K), "bf16")
+    W = gen(23, "w_qkv", (N, K), "bf16", std=0.02)
+    b = gen(23, "bias", (N,), "bf16") if bias else None
+    y = ops.opscale_linear(cuda(x), cuda(W), None if b is None else cuda(b))
+    torch.cuda.synchronize()
+    assert_close(f64(y.cpu()), oracle.linear(f64(x), f64(W), None if b is None else f64(b)), "bf16", "linear")
+
+
 def test_linear_identity_weight(ops):
     """W = I (bf16-exact) returns x exactly: no accumulation rounding occurs."""
     import torch
