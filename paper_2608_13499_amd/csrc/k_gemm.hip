@@ -168,6 +168,35 @@ __global__ __launch_bounds__(C::kThreads, 1) void gemm_bf16_kernel(const __bf16*
 #pragma unroll
     for (int j = 0; j < TM; ++j) b[buf][j] = lds_frag<C>(st + x_row0 + j * 32 * C::kRowBytes + lane_off[ks]);
   };
+  // The MFMAs of the last k-step of slice kt with the loads of slice kt + 2
+  // interleaved, one load after each MFMA, so no wave issues its loads in one
+  // burst (the issue of a stalled load would hold back the MFMAs behind it).
+  // Past the last slice the loads are out of range (they read zeros) and go
+  // to the stage no wave reads any more.
+  auto mfmas_loading = [&](int buf, int kt) {
+    constexpr int MF = TN * TM, L = C::kLoadsPerTile, LX = BM / C::kRowsPerLoad / C::kWaves;
+    OPS_LDS char* dst = smem + ((kt + 1 < nk ? kt : kt + 1) & 1) * C::kStageBytes;
+    const int rl = lane / C::kCPR, pc = lane % C::kCPR;
+    const int k0 = (kt + 2) * BK;
+    const bool more = kt + 2 < nk;
+#pragma unroll
+    for (int q = 0; q < (MF > L ? MF : L); ++q) {
+      if (q < MF) {
+        const int i = q / TM, j = q % TM;
+        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[buf][i], b[buf][j], acc[i][j], 0, 0, 0);
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+      }
+      if (q < L) {
+        const bool isx = q < LX;
+        const int grp = (isx ? q : q - LX) * C::kWaves + wave;
+        const int r = grp * C::kRowsPerLoad + rl;
+        const int k = k0 + ((pc ^ swz<C::kCPR>(r)) << 3);
+        const uint32_t voff = (more && k < K) ? (uint32_t)(((int64_t)r * K + k) * 2) : kOobOffset;
+        buffer_load16_lds(isx ? xr : wr, dst + (isx ? 0 : BM * C::kRowBytes) + grp * 1024, voff);
+        __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
+      }
+    }
+  };
   auto mfmas = [&](int buf) {
 #pragma unroll
     for (int i = 0; i < TN; ++i)
@@ -197,10 +226,10 @@ __global__ __launch_bounds__(C::kThreads, 1) void gemm_bf16_kernel(const __bf16*
         } else if (kt + 1 < nk) {
           wait_vmcnt<0>();
           __syncthreads();
-          if (kt + 2 < nk) load(kt + 2);
           frags(st_next, 0, nb);
         }
-        mfmas(ks & 1);
+        if (ks == KS - 1) mfmas_loading(ks & 1, kt);
+        else mfmas(ks & 1);
       }
     }
   } else {
@@ -227,6 +256,8 @@ __global__ __launch_bounds__(C::kThreads, 1) void gemm_bf16_kernel(const __bf16*
       }
     }
   }
+
+  wait_vmem();  // no LDS DMA may still be in flight when the workgroup ends
 
   // Epilogue.  acc[i][j] element e: n = n0 + wn*WN + i*32 + (e/4)*8 + fh*4 + e%4,
   // m = m0 + wm*WM + j*32 + fr.  Four consecutive n per lane -> one 8-byte store.
