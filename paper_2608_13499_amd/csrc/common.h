@@ -40,6 +40,12 @@ __device__ __forceinline__ void global_load16_lds(const void* gptr, OPS_LDS void
   __builtin_amdgcn_global_load_lds(gptr, lds_wave_base, 16, 0, 0);
 }
 
+// The same with the nontemporal hint (data read once, not kept in the caches).
+__device__ __forceinline__ void global_load16_lds_nt(const void* gptr, OPS_LDS void* lds_wave_base) {
+  constexpr int kNontemporal = 2;  // cache-policy bit NT on gfx950
+  __builtin_amdgcn_global_load_lds(gptr, lds_wave_base, 16, 0, kNontemporal);
+}
+
 __device__ __forceinline__ float bf_lo(uint32_t u) { return __uint_as_float(u << 16); }
 __device__ __forceinline__ float bf_hi(uint32_t u) { return __uint_as_float(u & 0xffff0000u); }
 

@@ -16,7 +16,10 @@
 //   * O[head][d] += P V on MFMA 16x16x32: the S^T accumulator is already the
 //     A operand P (a lane holds one head and 8 keys), and V, DMA'd into LDS
 //     row-major, is read as the B operand with ds_read_b64_tr_b16.
-// The next tile's K and V loads are in flight while the current one is used.
+// A wave loads a tile and waits for it; the latency is covered by the other
+// waves of the CU: with one V buffer per wave (64 KB of LDS) and at most 128
+// VGPRs, two workgroups (16 waves) share a CU.  V is read with the
+// nontemporal hint, the cache is streamed once.
 // Each split leaves (max, sum, unnormalized output) in the caller workspace; a
 // second kernel merges the splits of a (sequence, head) in split order, so the
 // result is deterministic.
@@ -79,7 +82,7 @@ size_t decode_workspace_bytes(int32_t B, int32_t Hq, int32_t D, int32_t max_cont
 
 // HB: KV heads per workgroup (8 / HB waves share one head's key tiles).
 template <int D, int G, int HB>
-__global__ __launch_bounds__(512) void attn_decode_split_kernel(
+__global__ __launch_bounds__(512, 4) void attn_decode_split_kernel(
     const __bf16* __restrict__ q, const __bf16* __restrict__ kc, const __bf16* __restrict__ vc,
     const int32_t* __restrict__ table, const int32_t* __restrict__ ctx, int Hq, int Hkv,
     int log2bs, int max_blocks, int64_t num_blocks, int max_splits, float scale_log2,
@@ -92,7 +95,7 @@ __global__ __launch_bounds__(512) void attn_decode_split_kernel(
   constexpr int VLOADS = kTile / VROWS;  // wave loads per V tile
   constexpr int VBYTES = kTile * D * 2;  // one V tile
   constexpr float kLazy = 8.f;
-  __shared__ __attribute__((aligned(16))) char vbuf[kWaves][2][VBYTES];
+  __shared__ __attribute__((aligned(16))) char vbuf[kWaves][VBYTES];
   __shared__ int32_t pages[kMaxPages];
 
   const int split = blockIdx.x, hg = blockIdx.y, b = blockIdx.z;
@@ -108,7 +111,7 @@ __global__ __launch_bounds__(512) void attn_decode_split_kernel(
   const int wt = wave / HB;              // its share of the head's key tiles
   const int col = lane & 15, grp = lane >> 4;
   const int64_t row_elems = (int64_t)Hkv * D;
-  OPS_LDS char* vb0 = (OPS_LDS char*)vbuf[wave][0];
+  OPS_LDS char* vb = (OPS_LDS char*)vbuf[wave];
 
   // Query heads of this group as the MFMA B operand (column = head).
   bf16x8 qf[KSTEPS];
@@ -150,23 +153,24 @@ __global__ __launch_bounds__(512) void attn_decode_split_kernel(
   };
 
   // K of 32 keys in MFMA A-operand layout (registers, 2*KSTEPS loads); V of
-  // the same keys DMA'd into this wave's LDS buffer `stage` (VLOADS loads).
+  // the same keys DMA'd into this wave's LDS buffer (VLOADS loads).
   struct KRegs {
     u32x4 k[2][KSTEPS];
   };
-  auto load_tile = [&](int t0, KRegs& r, int stage) {
+  auto load_k = [&](int t0, KRegs& r) {
 #pragma unroll
     for (int sub = 0; sub < 2; ++sub) {
       const __bf16* kr = row_ptr(kc, t0 + sub * 16 + col);
 #pragma unroll
       for (int s = 0; s < KSTEPS; ++s) r.k[sub][s] = *reinterpret_cast<const u32x4*>(kr + s * 32 + grp * 8);
     }
-    OPS_LDS char* vb = vb0 + stage * VBYTES;
+  };
+  auto load_v = [&](int t0) {
 #pragma unroll
     for (int i = 0; i < VLOADS; ++i) {
       const int row = i * VROWS + lane / CPR;
       const int c = (lane % CPR) ^ v_swz(row);  // logical chunk landing at this lane's slot
-      global_load16_lds(row_ptr(vc, t0 + row) + c * 8, vb + i * 1024);
+      global_load16_lds_nt(row_ptr(vc, t0 + row) + c * 8, vb + i * 1024);
     }
   };
 
@@ -175,7 +179,8 @@ __global__ __launch_bounds__(512) void attn_decode_split_kernel(
 #pragma unroll
   for (int i = 0; i < DT; ++i) acc[i] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  auto compute_tile = [&](int t0, const KRegs& r, int stage) {
+  // Scores, softmax and P V of one tile.
+  auto compute_tile = [&](int t0, const KRegs& r) {
     // scores S^T[key][head]: lane holds head `col`, keys t0 + 16*sub + 4*grp + rr
     f32x4 st[2];
 #pragma unroll
@@ -230,7 +235,6 @@ __global__ __launch_bounds__(512) void attn_decode_split_kernel(
     }
     // V as the B operand: lane (d = 16*dt + col, group grp) needs keys
     // 4*grp + e (e < 4) and 16 + 4*grp + (e - 4); one transposed read each.
-    const OPS_LDS char* vb = vb0 + stage * VBYTES;
     const int trow0 = 4 * grp + (col >> 2);
 #pragma unroll
     for (int dt = 0; dt < DT; ++dt) {
@@ -244,27 +248,20 @@ __global__ __launch_bounds__(512) void attn_decode_split_kernel(
     }
   };
 
-  // Software pipeline over this wave's tiles of each key window.
-  KRegs cur, nxt;
-  int stage = 0;
+  // Each wave loads a tile, waits for it and uses it; latency is hidden by
+  // the other waves of the CU (two workgroups of 8 waves fit: 64 KB of LDS
+  // and at most 128 VGPRs each), not by register double buffering.  V is
+  // refilled only after the previous tile's transposed reads fed its MFMAs.
+  KRegs cur;
   for (int w0 = k_begin; w0 < k_end; w0 += kChunk) {
     if (w0 != k_begin) __syncthreads();  // every wave is done with the previous window
     load_pages(w0);
     __syncthreads();
-    int t0 = w0 + wt * kTile;
-    if (t0 < w_end) load_tile(t0, cur, stage);
-    while (t0 < w_end) {
-      const int t1 = t0 + WPH * kTile;
-      if (t1 < w_end) {
-        load_tile(t1, nxt, stage ^ 1);
-        wait_vmcnt_le<KSTEPS * 2 + VLOADS>();  // this tile's loads landed, the next may fly
-      } else {
-        wait_vmem();
-      }
-      compute_tile(t0, cur, stage);
-      cur = nxt;
-      stage ^= 1;
-      t0 = t1;
+    for (int t0 = w0 + wt * kTile; t0 < w_end; t0 += WPH * kTile) {
+      load_k(t0, cur);
+      load_v(t0);
+      wait_vmem();
+      compute_tile(t0, cur);
     }
   }
 
