@@ -7,7 +7,9 @@ Python binding never import it and share no code with it.
 Every function is the plain textbook definition of the operator the paper names
 (Section 2.1's operator characterization: RMS Norm, QKV Linear and the MLP
 linears, the fused SiLU-and-multiply activation, FlashAttention-style prefill
-attention, decode attention over a paged KV cache), evaluated in fp64 with no
+attention, decode attention over a paged KV cache) and of the operators around
+them in a full layer (rotary embedding, the paged KV-cache write, the residual
+add before each norm), evaluated in fp64 with no
 tiling, no online softmax and no split of the key range.  See `ops` for the
 per-function citations and `cost` for the algorithmic flop/byte closed forms.
 
@@ -18,5 +20,6 @@ unpinned".
 from .ops import (  # noqa: F401
     rmsnorm, linear, silu, swiglu, softmax, attn_prefill, attn_prefill_rows,
     attn_decode, attn_decode_rows, gather_paged, decoder_layer_prefill,
+    rope, reshape_and_cache, add_rmsnorm, decoder_layer_forward, decoder_layer_decode,
 )
 from . import cost  # noqa: F401

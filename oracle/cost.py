@@ -55,3 +55,24 @@ def attn_decode(context_lens, Hq: int, Hkv: int, D: int, s: int, block_size: int
     flops = 4 * D * Hq * N
     nbytes = s * (2 * Hkv * D * N + 2 * B * Hq * D) + 4 * (nblocks + B)
     return flops, nbytes
+
+
+def rope(T: int, Hq: int, Hkv: int, D: int, s: int):
+    """Rotary embedding of q and k in place: each element read and written once
+    (plus the int32 positions); 6 flops per rotated pair."""
+    flops = 3 * T * (Hq + Hkv) * D
+    nbytes = 2 * s * T * (Hq + Hkv) * D + 4 * T
+    return flops, nbytes
+
+
+def reshape_and_cache(T: int, Hkv: int, D: int, s: int):
+    """KV-cache write of T tokens (all with a valid slot): k and v read once and
+    written once, plus the int32 slot of each token."""
+    return 0, 4 * s * T * Hkv * D + 4 * T
+
+
+def add_rmsnorm(M: int, H: int, s: int):
+    """Residual add + RMS Norm: x and residual read, the sum and y written."""
+    flops = 5 * M * H
+    nbytes = s * (4 * M * H + H)
+    return flops, nbytes

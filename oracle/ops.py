@@ -29,6 +29,13 @@ READINGS = {
               "token's K/V is already in the cache; context_len 0 gives a zero output.",
     "paged": "cached key j of sequence b lives in physical block block_table[b, j // bs] "
              "at slot j % bs; cache layout [num_blocks, bs, Hkv, D].",
+    "rope": "rotate-half rotary embedding (Llama family): pair (i, i + D/2), inverse frequency "
+            "theta^(-2i/D), angle = position * frequency, no frequency scaling; applied to the "
+            "query and key heads before attention and before the cache write.",
+    "cache_write": "token t is written to physical slot slot_mapping[t] = block * bs + offset; a "
+                   "slot outside [0, num_blocks * bs) is skipped (padding).",
+    "residual": "r = x + residual feeds RMS Norm; r is also the residual of the next operator pair "
+                "(the norm of the unrounded sum).",
 }
 
 
@@ -188,6 +195,55 @@ def attn_decode_rows(q, k_cache, v_cache, block_table, context_lens, seqs, scale
                        np.asarray(block_table)[seqs], np.asarray(context_lens)[seqs], scale)
 
 
+# -------------------------------------------------------- rotary embedding ---
+def rope(x, positions, theta: float) -> np.ndarray:
+    """Rotary position embedding of query or key heads (the RoPE attention
+    operator that Section 5.6 lists among the operators shared by Llama-family
+    generations).  The paper prints no formula; this is the rotate-half form:
+    for pair i < D/2, inverse frequency f_i = theta^(-2i/D), angle a = p * f_i,
+        out[i]       = x[i] cos a - x[i + D/2] sin a
+        out[i + D/2] = x[i + D/2] cos a + x[i] sin a.
+    x: [T, H, D]; positions: [T] integer position of each token in its sequence.
+    """
+    x = _f64(x)
+    D = x.shape[-1]
+    half = D // 2
+    inv_freq = float(theta) ** (-2.0 * np.arange(half) / D)
+    ang = np.asarray(positions, np.float64)[:, None] * inv_freq[None, :]  # [T, D/2]
+    c = np.cos(ang)[:, None, :]
+    s = np.sin(ang)[:, None, :]
+    a, b = x[..., :half], x[..., half:]
+    return np.concatenate([a * c - b * s, b * c + a * s], axis=-1)
+
+
+# ------------------------------------------------------------ KV cache write --
+def reshape_and_cache(k, v, k_cache, v_cache, slot_mapping):
+    """Write the K/V rows of new tokens into the paged cache (the
+    reshape_and_cache operator of Section 2.1's memory study).  Token t goes to
+    physical slot slot_mapping[t]: block slot // bs, offset slot % bs; a slot
+    outside [0, num_blocks * bs) is skipped.
+    k, v: [T, Hkv, D]; caches: [num_blocks, bs, Hkv, D].  Returns updated
+    copies of both caches (fp64)."""
+    kc = _f64(k_cache).copy()
+    vc = _f64(v_cache).copy()
+    nb, bs = kc.shape[0], kc.shape[1]
+    k, v = _f64(k), _f64(v)
+    for t, slot in enumerate(np.asarray(slot_mapping, np.int64)):
+        if 0 <= slot < nb * bs:
+            kc[slot // bs, slot % bs] = k[t]
+            vc[slot // bs, slot % bs] = v[t]
+    return kc, vc
+
+
+# ------------------------------------------------------- residual + RMS Norm --
+def add_rmsnorm(x, residual, w, eps: float):
+    """Residual add followed by RMS Norm, the pattern each norm of a decoder
+    layer sees.  r = x + residual; y = rmsnorm(r, w, eps).  Returns (y, r); r
+    is the residual carried to the next norm."""
+    r = _f64(x) + _f64(residual)
+    return rmsnorm(r, w, eps), r
+
+
 # ----------------------------------------------------- whole decoder layer ---
 def decoder_layer_prefill(x, p, cu_seqlens, n_q_heads, n_kv_heads, head_dim, eps):
     """The layer dataflow the operators form (Section 2.2: a model is a data
@@ -212,3 +268,62 @@ def decoder_layer_prefill(x, p, cu_seqlens, n_q_heads, n_kv_heads, head_dim, eps
     act = swiglu(gu)
     y = linear(act, p["w_down"])
     return {"h1": h1, "qkv": qkv, "attn": a, "o": o, "h2": h2, "gate_up": gu, "act": act, "y": y}
+
+
+def decoder_layer_forward(x, residual, p, positions, cu_seqlens, n_q_heads, n_kv_heads, head_dim, eps,
+                          theta, k_cache, v_cache, slot_mapping):
+    """One decoder layer over a ragged prefill batch with every operator of its
+    dataflow (Section 2.2): residual + norm -> QKV -> RoPE on q and k -> cache
+    write of k and v -> causal attention -> O -> residual + norm -> gate-up ->
+    SiLU-mul -> down.  residual None means x is the layer's first input (the
+    residual is x itself).  Returns every intermediate, the layer output y, the
+    residual carried to the next layer and the updated caches (all fp64)."""
+    T, D = x.shape[0], head_dim
+    if residual is None:
+        h1, r1 = rmsnorm(x, p["w_norm1"], eps), _f64(x)
+    else:
+        h1, r1 = add_rmsnorm(x, residual, p["w_norm1"], eps)
+    qkv = linear(h1, p["w_qkv"])
+    q = rope(qkv[:, : n_q_heads * D].reshape(T, n_q_heads, D), positions, theta)
+    k = rope(qkv[:, n_q_heads * D:(n_q_heads + n_kv_heads) * D].reshape(T, n_kv_heads, D), positions, theta)
+    v = qkv[:, (n_q_heads + n_kv_heads) * D:].reshape(T, n_kv_heads, D)
+    kc, vc = reshape_and_cache(k, v, k_cache, v_cache, slot_mapping)
+    a = attn_prefill(q, k, v, cu_seqlens, 1.0 / np.sqrt(D), causal=True)
+    o = linear(a.reshape(T, n_q_heads * D), p["w_o"])
+    h2, r2 = add_rmsnorm(o, r1, p["w_norm2"], eps)
+    gu = linear(h2, p["w_gate_up"])
+    act = swiglu(gu)
+    y = linear(act, p["w_down"])
+    return {"h1": h1, "r1": r1, "qkv": qkv, "q": q, "k": k, "v": v, "attn": a, "o": o, "h2": h2, "r2": r2,
+            "gate_up": gu, "act": act, "y": y, "k_cache": kc, "v_cache": vc}
+
+
+def decoder_layer_decode(x, residual, p, context_lens, block_table, n_q_heads, n_kv_heads, head_dim, eps,
+                         theta, k_cache, v_cache):
+    """One decode step of the same layer for B sequences with one new token each
+    (Section 2.1's 1-token decode phase; Appendix E): the new token of sequence
+    b sits at position context_lens[b] - 1, its k and v are written to that
+    position's cache slot before decode attention reads the whole context."""
+    B, D = x.shape[0], head_dim
+    ctx = np.asarray(context_lens, np.int64)
+    bt = np.asarray(block_table, np.int64)
+    bs = np.asarray(k_cache).shape[1]
+    pos = ctx - 1
+    slots = np.array([bt[b, pos[b] // bs] * bs + pos[b] % bs if pos[b] >= 0 else -1 for b in range(B)], np.int64)
+    if residual is None:
+        h1, r1 = rmsnorm(x, p["w_norm1"], eps), _f64(x)
+    else:
+        h1, r1 = add_rmsnorm(x, residual, p["w_norm1"], eps)
+    qkv = linear(h1, p["w_qkv"])
+    q = rope(qkv[:, : n_q_heads * D].reshape(B, n_q_heads, D), pos, theta)
+    k = rope(qkv[:, n_q_heads * D:(n_q_heads + n_kv_heads) * D].reshape(B, n_kv_heads, D), pos, theta)
+    v = qkv[:, (n_q_heads + n_kv_heads) * D:].reshape(B, n_kv_heads, D)
+    kc, vc = reshape_and_cache(k, v, k_cache, v_cache, slots)
+    a = attn_decode(q, kc, vc, bt, ctx, 1.0 / np.sqrt(D))
+    o = linear(a.reshape(B, n_q_heads * D), p["w_o"])
+    h2, r2 = add_rmsnorm(o, r1, p["w_norm2"], eps)
+    gu = linear(h2, p["w_gate_up"])
+    act = swiglu(gu)
+    y = linear(act, p["w_down"])
+    return {"h1": h1, "r1": r1, "qkv": qkv, "q": q, "k": k, "v": v, "slots": slots, "attn": a, "o": o,
+            "h2": h2, "r2": r2, "gate_up": gu, "act": act, "y": y, "k_cache": kc, "v_cache": vc}

@@ -269,6 +269,131 @@ def check_attn_decode(impl):
     np.testing.assert_allclose(dec[0], pre[n - 1], rtol=1e-13)
 
 
+def check_rope(impl):
+    rng = np.random.default_rng(7)
+    T, H, D, theta = 6, 3, 16, 10000.0
+    x = rng.standard_normal((T, H, D))
+    pos = np.array([0, 1, 2, 7, 100, 33000])
+    out = impl.rope(x, pos, theta)
+    # position 0 is the identity
+    assert np.array_equal(out[0], x[0])
+    # unit vectors: e_i rotates into (cos a_i, sin a_i) on the pair (i, i + D/2)
+    # with a_i = p * theta^(-2i/D); e_{i+D/2} into (-sin a_i, cos a_i)
+    half = D // 2
+    for i in range(half):
+        for p_ in (1, 5, 1000):
+            a = p_ * theta ** (-2.0 * i / D)
+            e = np.zeros((1, 1, D))
+            e[0, 0, i] = 1.0
+            r = impl.rope(e, [p_], theta)[0, 0]
+            want = np.zeros(D)
+            want[i], want[i + half] = math.cos(a), math.sin(a)
+            np.testing.assert_allclose(r, want, atol=1e-12)
+            e = np.zeros((1, 1, D))
+            e[0, 0, i + half] = 1.0
+            r = impl.rope(e, [p_], theta)[0, 0]
+            want = np.zeros(D)
+            want[i], want[i + half] = -math.sin(a), math.cos(a)
+            np.testing.assert_allclose(r, want, atol=1e-12)
+    # a rotation: every pair keeps its length
+    np.testing.assert_allclose(out[..., :half] ** 2 + out[..., half:] ** 2,
+                               x[..., :half] ** 2 + x[..., half:] ** 2, rtol=1e-12)
+    # the same map written as complex multiplication z * exp(i a)
+    z = (x[..., :half] + 1j * x[..., half:]) * np.exp(1j * pos[:, None, None] * theta ** (-2.0 * np.arange(half) / D))
+    np.testing.assert_allclose(out, np.concatenate([z.real, z.imag], -1), atol=1e-11)
+    # rotations compose: rope(rope(x, m), n) == rope(x, m + n)
+    m, n = np.array([3, 40, 0, 9, 1, 2]), np.array([5, 1, 77, 0, 8, 1000])
+    np.testing.assert_allclose(impl.rope(impl.rope(x, m, theta), n, theta), impl.rope(x, m + n, theta), atol=1e-11)
+    # scores depend on the position difference only
+    q, k = rng.standard_normal((1, 1, D)), rng.standard_normal((1, 1, D))
+    for (mq, nk) in [(10, 3), (200, 190), (7, 7)]:
+        lhs = float(np.sum(impl.rope(q, [mq], theta) * impl.rope(k, [nk], theta)))
+        rhs = float(np.sum(impl.rope(q, [mq - nk], theta) * k))
+        assert abs(lhs - rhs) < 1e-10 * (1 + abs(rhs))
+
+
+def check_cache_write(impl):
+    rng = np.random.default_rng(8)
+    nb, bs, Hkv, D = 6, 4, 2, 3
+    kc0 = rng.standard_normal((nb, bs, Hkv, D))
+    vc0 = rng.standard_normal((nb, bs, Hkv, D))
+    # one sequence of 7 tokens living in blocks (4, 1): slots follow the table
+    table = np.array([4, 1])
+    k = rng.standard_normal((9, Hkv, D))
+    v = rng.standard_normal((9, Hkv, D))
+    slots = np.array([table[j // bs] * bs + j % bs for j in range(7)] + [-1, nb * bs])  # two skipped
+    kc, vc = impl.reshape_and_cache(k, v, kc0, vc0, slots)
+    # reading the sequence back through the block table returns the new rows
+    np.testing.assert_array_equal(oracle.gather_paged(kc, table, 7), k[:7])
+    np.testing.assert_array_equal(oracle.gather_paged(vc, table, 7), v[:7])
+    # every slot not written (including the last block's rows) is unchanged
+    written = np.zeros((nb, bs), bool)
+    for s_ in slots[:7]:
+        written[s_ // bs, s_ % bs] = True
+    np.testing.assert_array_equal(kc[~written], kc0[~written])
+    np.testing.assert_array_equal(vc[~written], vc0[~written])
+    # the inputs are not modified
+    assert not np.shares_memory(kc, kc0)
+
+
+def check_add_rmsnorm(impl):
+    rng = np.random.default_rng(9)
+    x = rng.standard_normal((5, 12))
+    res = rng.standard_normal((5, 12))
+    w = 1 + 0.02 * rng.standard_normal(12)
+    y, r = impl.add_rmsnorm(x, res, w, 1e-5)
+    np.testing.assert_array_equal(r, x + res)
+    # unit gain, eps 0: the normalized sum has RMS 1
+    y1, _ = impl.add_rmsnorm(x, res, np.ones(12), 0.0)
+    np.testing.assert_allclose(np.sqrt(np.mean(y1 * y1, -1)), 1.0, rtol=1e-13)
+    # the sum, not x alone, is normalized: a constant sum c gives c / sqrt(c^2 + eps) * w
+    c = 0.7
+    yc, _ = impl.add_rmsnorm(np.full((1, 12), c) - res[:1], res[:1], w, 0.5)
+    np.testing.assert_allclose(yc[0], c / math.sqrt(c * c + 0.5) * w, rtol=1e-12)
+    # residual = -x: the sum is zero and so is the output (eps > 0)
+    y0, r0 = impl.add_rmsnorm(x, -x, w, 1e-5)
+    assert np.all(r0 == 0) and np.all(y0 == 0)
+
+
+def check_layer(impl):
+    """Prefill of L tokens then one decode step equals prefill of L + 1 tokens:
+    RoPE positions, cache slots, attention and the residual path agree."""
+    rng = np.random.default_rng(10)
+    H, Hq, Hkv, D, F, eps, theta, bs = 16, 4, 2, 4, 24, 1e-5, 10000.0, 2
+    p = {"w_norm1": 1 + 0.02 * rng.standard_normal(H), "w_qkv": 0.3 * rng.standard_normal(((Hq + 2 * Hkv) * D, H)),
+         "w_o": 0.3 * rng.standard_normal((H, Hq * D)), "w_norm2": 1 + 0.02 * rng.standard_normal(H),
+         "w_gate_up": 0.3 * rng.standard_normal((2 * F, H)), "w_down": 0.3 * rng.standard_normal((H, F))}
+    lens = [5, 3]
+    x_all = [rng.standard_normal((L + 1, H)) for L in lens]
+    res_all = [rng.standard_normal((L + 1, H)) for L in lens]
+    nb = 8
+    table = np.array([[6, 1, 3], [0, 5, 2]])
+    kc0, vc0 = np.zeros((nb, bs, Hkv, D)), np.zeros((nb, bs, Hkv, D))
+    # prefill of the first L tokens of both sequences
+    x = np.concatenate([a[:L] for a, L in zip(x_all, lens)])
+    res = np.concatenate([a[:L] for a, L in zip(res_all, lens)])
+    pos = np.concatenate([np.arange(L) for L in lens])
+    slots = np.concatenate([[table[b, j // bs] * bs + j % bs for j in range(L)] for b, L in enumerate(lens)])
+    cu = np.concatenate([[0], np.cumsum(lens)])
+    pre = impl.decoder_layer_forward(x, res, p, pos, cu, Hq, Hkv, D, eps, theta, kc0, vc0, slots)
+    # one decode step with token L of each sequence
+    xd = np.stack([a[L] for a, L in zip(x_all, lens)])
+    rd = np.stack([a[L] for a, L in zip(res_all, lens)])
+    dec = impl.decoder_layer_decode(xd, rd, p, np.array(lens) + 1, table, Hq, Hkv, D, eps, theta,
+                                    pre["k_cache"], pre["v_cache"])
+    for b, L in enumerate(lens):
+        full = impl.decoder_layer_forward(x_all[b], res_all[b], p, np.arange(L + 1), [0, L + 1], Hq, Hkv, D, eps,
+                                          theta, kc0, vc0, [-1] * (L + 1))
+        for key in ("y", "r2", "attn", "q", "k"):
+            np.testing.assert_allclose(dec[key][b], full[key][L], rtol=1e-10, atol=1e-11)
+    # the decode step wrote its k and v where the prefill of L + 1 tokens would have
+    assert list(dec["slots"]) == [table[b, L // bs] * bs + L % bs for b, L in enumerate(lens)]
+    # no residual means the input itself is the residual
+    a = impl.decoder_layer_forward(x, None, p, pos, cu, Hq, Hkv, D, eps, theta, kc0, vc0, slots)
+    b_ = impl.decoder_layer_forward(x, np.zeros_like(x), p, pos, cu, Hq, Hkv, D, eps, theta, kc0, vc0, slots)
+    np.testing.assert_allclose(a["y"], b_["y"], rtol=1e-13)
+
+
 def check_cost(c):
     # causal visible pairs counted by a loop
     lens = [1, 2, 5, 0, 9]
@@ -287,9 +412,16 @@ def check_cost(c):
     f, b = c.attn_decode(ctx, 8, 2, 4, 2, 16)
     assert f == 4 * 4 * 8 * 34
     assert b == 2 * (2 * 2 * 4 * 34 + 2 * 4 * 8 * 4) + 4 * ((1 + 1 + 2 + 0) + 4)
+    # rope: q and k elements read and written once, 3 flops per element (6 per pair)
+    assert c.rope(5, 4, 2, 8, 2) == (3 * 5 * 6 * 8, 2 * 2 * 5 * 6 * 8 + 4 * 5)
+    # cache write: k and v read and written, plus one int32 slot per token
+    assert c.reshape_and_cache(5, 2, 8, 2) == (0, 4 * 2 * 5 * 2 * 8 + 4 * 5)
+    # residual + norm: x, residual read; sum and output written; gain read once
+    assert c.add_rmsnorm(4, 8, 2) == (5 * 32, 2 * (4 * 32 + 8))
 
 
-CHECKS = [check_linear, check_rmsnorm, check_swiglu, check_softmax, check_attn_prefill, check_attn_decode]
+CHECKS = [check_linear, check_rmsnorm, check_swiglu, check_softmax, check_attn_prefill, check_attn_decode,
+          check_rope, check_cache_write, check_add_rmsnorm, check_layer]
 
 
 @pytest.mark.parametrize("check", CHECKS, ids=lambda f: f.__name__)
@@ -333,6 +465,45 @@ def _mut_attn(kv_map=None, causal_strict=False, drop_scale=False, no_max=False):
     return f
 
 
+def _mut_rope(interleaved=False, sign=1.0, exp_scale=2.0):
+    def f(x, positions, theta):
+        x = np.asarray(x, float)
+        D = x.shape[-1]
+        half = D // 2
+        ang = np.asarray(positions, float)[:, None] * float(theta) ** (-exp_scale * np.arange(half) / D)
+        c, s = np.cos(ang)[:, None, :], sign * np.sin(ang)[:, None, :]
+        if interleaved:
+            a, b = x[..., 0::2], x[..., 1::2]
+            out = np.empty_like(x)
+            out[..., 0::2], out[..., 1::2] = a * c - b * s, b * c + a * s
+            return out
+        a, b = x[..., :half], x[..., half:]
+        return np.concatenate([a * c - b * s, b * c + a * s], axis=-1)
+    return f
+
+
+def _mut_cache(skip_check=True, swap=False):
+    def f(k, v, kc, vc, slots):
+        kc, vc = np.array(kc, float), np.array(vc, float)
+        nb, bs = kc.shape[:2]
+        for t, s_ in enumerate(slots):
+            if skip_check and not 0 <= s_ < nb * bs:
+                continue
+            if not skip_check and s_ >= nb * bs:
+                continue
+            blk, off = (s_ % nb, s_ // nb) if swap else (s_ // bs, s_ % bs)
+            kc[blk, off], vc[blk, off] = k[t], v[t]
+        return kc, vc
+    return f
+
+
+def _mut_layer_decode_pos(x, res, p, ctx, bt, Hq, Hkv, D, eps, theta, kc, vc):
+    """decode step that rotates the new token by position context_len instead of
+    context_len - 1 (and writes it one slot later)."""
+    return oracle.decoder_layer_decode(x, res, p, np.asarray(ctx) + 1, np.concatenate([bt, bt[:, -1:]], 1),
+                                       Hq, Hkv, D, eps, theta, kc, vc)
+
+
 MUTANTS = {
     "linear_k_reversed": (check_linear, dict(linear=lambda x, W, b=None: np.asarray(x, float) @ np.asarray(W, float)[:, ::-1].T + (0 if b is None else b))),
     "linear_bias_dropped": (check_linear, dict(linear=lambda x, W, b=None: np.asarray(x, float) @ np.asarray(W, float).T)),
@@ -348,6 +519,14 @@ MUTANTS = {
     "attn_scale_dropped": (check_attn_prefill, dict(attn_prefill=_mut_attn(drop_scale=True))),
     "decode_slot_index": (check_attn_decode, dict(attn_decode=lambda q, kc, vc, bt, n, scale: oracle.attn_decode(q, kc[:, ::-1], vc[:, ::-1], bt, n, scale))),
     "decode_gqa_modulo": (check_attn_decode, dict(attn_decode=lambda q, kc, vc, bt, n, scale: oracle.attn_decode(q, np.asarray(kc)[:, :, ::-1], np.asarray(vc)[:, :, ::-1], bt, n, scale))),
+    "rope_interleaved_pairs": (check_rope, dict(rope=_mut_rope(interleaved=True))),
+    "rope_sign": (check_rope, dict(rope=_mut_rope(sign=-1.0))),
+    "rope_exponent": (check_rope, dict(rope=_mut_rope(exp_scale=1.0))),
+    "rope_position_off_by_one": (check_rope, dict(rope=lambda x, pos, th: oracle.rope(x, np.asarray(pos) + 1, th))),
+    "cache_negative_slot_wraps": (check_cache_write, dict(reshape_and_cache=_mut_cache(skip_check=False))),
+    "cache_block_offset_swapped": (check_cache_write, dict(reshape_and_cache=_mut_cache(swap=True))),
+    "add_rmsnorm_norms_x": (check_add_rmsnorm, dict(add_rmsnorm=lambda x, r, w, eps: (oracle.rmsnorm(x, w, eps), np.asarray(x) + r))),
+    "layer_decode_position_is_len": (check_layer, dict(decoder_layer_decode=_mut_layer_decode_pos)),
 }
 
 
@@ -360,10 +539,12 @@ def test_planted_mistake_is_caught(name):
 
 @pytest.mark.parametrize("name,mut", [
     ("causal_pairs_strict", dict(attn_prefill=lambda L, Hq, Hkv, D, s, causal=True: (4 * D * Hq * int(sum(l * (l - 1) // 2 for l in L)), 0))),
+    ("rope_q_only", dict(rope=lambda T, Hq, Hkv, D, s: (3 * T * Hq * D, 2 * s * T * Hq * D + 4 * T))),
     ("decode_blocks_floor", dict(attn_decode=lambda n, Hq, Hkv, D, s, bs: (4 * D * Hq * sum(n), s * (2 * Hkv * D * sum(n) + 2 * len(n) * Hq * D) + 4 * (sum(x // bs for x in n) + len(n))))),
 ])
 def test_planted_cost_mistake_is_caught(name, mut):
-    c = types.SimpleNamespace(**{k: getattr(ocost, k) for k in ("linear", "rmsnorm", "swiglu", "attn_prefill", "attn_decode")})
+    c = types.SimpleNamespace(**{k: getattr(ocost, k) for k in ("linear", "rmsnorm", "swiglu", "attn_prefill", "attn_decode",
+                                                                "rope", "reshape_and_cache", "add_rmsnorm")})
     for k, v in mut.items():
         setattr(c, k, v)
     with pytest.raises(AssertionError):

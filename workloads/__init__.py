@@ -52,6 +52,7 @@ class LayerConfig:
     mode: str = "prefill"  # "prefill" or "decode"
     block_size: int = 16   # paged KV cache (decode)
     seed: int = 0
+    rope_theta: float = 500000.0  # rotary base of the Llama-3 family
 
     @property
     def qkv_out(self) -> int:
@@ -84,7 +85,7 @@ def _lognormal_until(rng, total, median, sigma, lo, hi) -> np.ndarray:
 
 
 # The five workloads.  Names describe the layer and batch they model.
-C1 = LayerConfig("tiny_f32_prefill", "f32", 256, 4, 4, 64, 688)
+C1 = LayerConfig("tiny_f32_prefill", "f32", 256, 4, 4, 64, 688, rope_theta=10000.0)
 C2 = LayerConfig("llama8b_prefill_ragged16", "bf16", 4096, 32, 8, 128, 14336)
 C3 = LayerConfig("llama8b_decode_b256", "bf16", 4096, 32, 8, 128, 14336, mode="decode")
 C4 = LayerConfig("llama70b_prefill_16k", "bf16", 8192, 64, 8, 128, 28672)
