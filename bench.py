@@ -29,6 +29,9 @@ PEAK_BF16 = 2.5e15     # dense bf16 MFMA, FLOP/s
 PEAK_HBM = 8.0e12      # HBM3E, B/s
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_counters.json")
 KERNEL_SOURCES = {"gemm_bf16_kernel": "paper_2608_13499_amd/csrc/k_gemm.hip",
+                  "rope_kernel": "paper_2608_13499_amd/csrc/k_layer_ops.hip",
+                  "cache_write_kernel": "paper_2608_13499_amd/csrc/k_layer_ops.hip",
+                  "add_rmsnorm_kernel": "paper_2608_13499_amd/csrc/k_layer_ops.hip",
                   "attn_prefill_bf16_kernel": "paper_2608_13499_amd/csrc/k_attn_prefill.hip",
                   "attn_decode_split_kernel": "paper_2608_13499_amd/csrc/k_attn_decode.hip",
                   "attn_decode_combine_kernel": "paper_2608_13499_amd/csrc/k_attn_decode.hip",
@@ -116,6 +119,41 @@ class Layer:
         ops.opscale_linear(self.act, p["w_down"], y=self.y); mark(8)
         ops.opscale_attn_decode(d["q"], d["k_cache"], d["v_cache"], d["block_table"], d["context_lens"],
                                 d["max_context_len"], self.scale, workspace=self.ws, out=self.dout); mark(9)
+
+    def setup_extras(self):
+        """Operands of the operators around attention at the same shape: RoPE on
+        the packed QKV output, the write of every token's k / v into a shuffled
+        paged cache, and the residual add + norm of the O projection output."""
+        import numpy as np
+        import workloads as wl
+        torch, pc = self.torch, self.pc
+        lens = self.p["lengths"]
+        bs = pc.block_size
+        table, nb = wl.paged_cache_layout(lens, bs, wl.rng_for(pc, "block_table"))
+        slots = np.concatenate([[table[b, j // bs] * bs + j % bs for j in range(L)] for b, L in enumerate(lens)])
+        self.slots = torch.from_numpy(slots.astype(np.int32)).cuda()
+        self.pos = torch.from_numpy(np.concatenate([np.arange(L) for L in lens]).astype(np.int32)).cuda()
+        self.kc = torch.zeros(nb, bs, pc.n_kv_heads, pc.head_dim, dtype=torch.bfloat16, device="cuda")
+        self.vc = torch.zeros_like(self.kc)
+        self.res = wl.device_normal((self.p["M"], pc.hidden), pc.seed, "attn_out", "bf16")
+        self.extra_names = ["rope", "reshape_and_cache", "add_rmsnorm"]
+
+    def extra(self, i):
+        ops, pc = self.ops, self.pc
+        if i == 0:
+            ops.opscale_rope(self.q, self.k, self.pos, pc.rope_theta)
+        elif i == 1:
+            ops.opscale_reshape_and_cache(self.k, self.v, self.kc, self.vc, self.slots)
+        else:
+            ops.opscale_add_rmsnorm(self.o, self.res, self.p["w_norm2"], y=self.h2, eps=pc.eps)
+
+    def extra_work(self):
+        pc = self.pc
+        M, H = self.p["M"], pc.hidden
+        Hq, Hkv, D = pc.n_q_heads, pc.n_kv_heads, pc.head_dim
+        return {"rope": (3 * M * (Hq + Hkv) * D, 2 * 2 * M * (Hq + Hkv) * D + 4 * M, "hbm", M, "tokens/s"),
+                "reshape_and_cache": (0, 4 * 2 * M * Hkv * D + 4 * M, "hbm", M, "tokens/s"),
+                "add_rmsnorm": (5 * M * H, 2 * (4 * M * H + H), "hbm", M, "tokens/s")}
 
     def work(self):
         """Algorithmic (flops, bytes, bound, units, unit-name) per operator."""
@@ -230,8 +268,8 @@ def cpu_baseline(budget_s: float = 20.0):
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=10)
-    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--calibrate-copy-mib", type=int, default=0,
                     help="run one device copy of this many MiB before the steps (counter calibration)")
@@ -297,6 +335,24 @@ def main():
     roof["traffic"] = measured_traffic(dom, kernel)
     roof["kernel"] = f"{kernel} ({dom})"
     roof["work_per_launch"] = {"flops": fl, "bytes": by}
+    # The operators around attention of a full layer (RoPE, cache write,
+    # residual + norm), timed separately: they are not part of the step.
+    layer.setup_extras()
+    extra_ops = {}
+    for i, nm in enumerate(layer.extra_names):
+        for _ in range(a.warmup):
+            layer.extra(i)
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(2 * a.steps)]
+        for j in range(a.steps):
+            ev[2 * j].record()
+            layer.extra(i)
+            ev[2 * j + 1].record()
+        torch.cuda.synchronize()
+        us = sum(ev[2 * j].elapsed_time(ev[2 * j + 1]) for j in range(a.steps)) * 1e3 / a.steps
+        fl, by, bound, units, unit = layer.extra_work()[nm]
+        t_s = us * 1e-6
+        extra_ops[nm] = {"us": round(us, 2), unit: round(units / t_s, 1), "gbps": round(by / t_s * 1e-9, 1),
+                         "bound": bound, "roofline_frac": round(by / t_s / PEAK_HBM, 4)}
     M = layer.p["M"]
     out = {
         "metric": "per-operator prefill tokens/s + % of MFMA/HBM roofline, Llama-8B-shaped layer",
@@ -311,6 +367,7 @@ def main():
                    "global_batch": M, "seq_len": int(layer.p["lengths"].max()), "parallelism": "none"},
         "roofline": roof,
         "per_op": per_op,
+        "extra_ops": extra_ops,
     }
     if not a.no_cpu_baseline:
         log("cpu baseline (oracle) ...")

@@ -148,7 +148,9 @@ size_t opscale_attn_decode_workspace_size(int32_t B, int32_t Hq, int32_t D,
  *   o[b, h, :] = sum_{j < n_b} softmax_j(scale * q[b, h, :] . K_b[j, g, :]) V_b[j, g, :]
  * with n_b = context_lens[b] (already including the new token, whose K/V were
  * written to the cache beforehand) and K_b[j] = k_cache[block_table[b, j / bs], j % bs].
- * q, o: [B, Hq, D]; k_cache, v_cache: [num_blocks, block_size, Hkv, D];
+ * q: [B, Hq, D] rows of q_row_stride elements (>= Hq * D, a multiple of 16
+ * bytes; a view into the QKV linear's output is fine); o: [B, Hq, D] dense;
+ * k_cache, v_cache: [num_blocks, block_size, Hkv, D];
  * block_table: DEVICE int32 [B, max_blocks_per_seq]; context_lens: DEVICE int32 [B].
  * A context length of 0 yields a zero output row.  Lengths above
  * max_blocks_per_seq * block_size are clamped to it.  Keys whose block id is
@@ -162,13 +164,60 @@ size_t opscale_attn_decode_workspace_size(int32_t B, int32_t Hq, int32_t D,
  * scale must be finite and > 0.  block_size must be a power of two in
  *   [1, 1024]; D 64 or 128; Hkv | Hq; on the bf16 path Hq / Hkv is 1, 2, 4 or 8.
  */
-opscale_status opscale_attn_decode(const void* q, const void* k_cache, const void* v_cache,
+opscale_status opscale_attn_decode(const void* q, int64_t q_row_stride, const void* k_cache, const void* v_cache,
                                    const int32_t* block_table, const int32_t* context_lens,
                                    void* o, int32_t B, int32_t Hq, int32_t Hkv, int32_t D,
                                    int32_t block_size, int32_t max_blocks_per_seq,
                                    int64_t num_blocks, int32_t max_context_len, float scale,
                                    opscale_dtype dt, void* workspace, size_t workspace_bytes,
                                    hipStream_t stream, opscale_timing* timing);
+
+/* ---------------------------------------------------------------------------
+ * The operators around attention in a full decoder layer.
+ * ------------------------------------------------------------------------- */
+
+/*
+ * Rotary position embedding of the query and key heads, in place (the RoPE
+ * attention operator that Section 5.6 lists among those shared by Llama-family
+ * models), rotate-half form.  For token t at position p = positions[t] and
+ * pair i < D/2 of every head, with inverse frequency f_i = theta^(-2i/D) and
+ * angle a = p * f_i:
+ *   x[i] <- x[i] cos a - x[i + D/2] sin a,   x[i + D/2] <- x[i + D/2] cos a + x[i] sin a.
+ * q: [T, Hq, D] rows of q_row_stride elements; k: [T, Hkv, D] rows of
+ * k_row_stride elements (both may be views into the QKV linear's output);
+ * positions: device int32 [T].  The angle is formed and reduced modulo 2 pi
+ * in fp64.  D 64 or 128; theta finite and > 0; q and k must not share heads.
+ * 16-byte aligned q and k, strides multiples of 16 bytes.
+ */
+opscale_status opscale_rope(void* q, void* k, int64_t q_row_stride, int64_t k_row_stride,
+                            const int32_t* positions, int64_t T, int32_t Hq, int32_t Hkv, int32_t D,
+                            double theta, opscale_dtype dt, hipStream_t stream, opscale_timing* timing);
+
+/*
+ * Paged KV-cache write (the reshape_and_cache operator of Section 2.1's
+ * memory study): the K and V rows of token t go to cache row
+ * slot_mapping[t], i.e. block slot / block_size, offset slot % block_size of
+ * k_cache and v_cache [num_blocks, block_size, Hkv, D].  A token whose slot is
+ * outside [0, num_blocks * block_size) is skipped (padding).
+ * k, v: [T, Hkv, D] rows of kv_row_stride elements (views into the QKV output
+ * are fine); slot_mapping: device int32 [T]; num_blocks * block_size < 2^31.
+ * The caches must not overlap k or v.  Tokens sharing a slot race.
+ */
+opscale_status opscale_reshape_and_cache(const void* k, const void* v, int64_t kv_row_stride, void* k_cache,
+                                         void* v_cache, const int32_t* slot_mapping, int64_t T, int32_t Hkv,
+                                         int32_t D, int32_t block_size, int64_t num_blocks, opscale_dtype dt,
+                                         hipStream_t stream, opscale_timing* timing);
+
+/*
+ * Residual add fused with RMS Norm, the form each norm of a decoder layer
+ * takes after the first: residual <- x + residual (rounded once to dt) and
+ * y <- (x + residual) / sqrt(mean((x + residual)^2) + eps) * w, the norm taken
+ * of the unrounded fp32 sum.  x, residual, y: [M, H]; w: [H].  y may be x;
+ * residual must not overlap x, y or w.  Same size rules as opscale_rmsnorm,
+ * and a row is at most 16 KB (H <= 8192 in bf16), else OPSCALE_ERR_UNSUPPORTED.
+ */
+opscale_status opscale_add_rmsnorm(const void* x, void* residual, const void* w, void* y, int64_t M, int64_t H,
+                                   float eps, opscale_dtype dt, hipStream_t stream, opscale_timing* timing);
 
 /* ---------------------------------------------------------------------------
  * Operator profiling (Section 4.2 "Operator Profiling": per-operator compute
@@ -197,7 +246,8 @@ typedef struct {
       int32_t Hq, Hkv, D; float scale; int32_t causal;
     } attn_prefill;
     struct {
-      const void *q, *k_cache, *v_cache; const int32_t *block_table, *context_lens; void* o;
+      const void* q; int64_t q_row_stride; const void *k_cache, *v_cache;
+      const int32_t *block_table, *context_lens; void* o;
       int32_t B, Hq, Hkv, D, block_size, max_blocks_per_seq; int64_t num_blocks;
       int32_t max_context_len; float scale; void* workspace; size_t workspace_bytes;
     } attn_decode;

@@ -5,6 +5,7 @@ sources (csrc/), their build script and the ctypes binding."""
 from ._lib import (  # noqa: F401
     OpscaleError, Timing, Profile, OpDesc, load, LIB_PATH, EXPORTS,
     opscale_version, opscale_rmsnorm, opscale_linear, opscale_swiglu, opscale_attn_prefill,
+    opscale_rope, opscale_reshape_and_cache, opscale_add_rmsnorm,
     opscale_attn_decode_workspace_size, opscale_attn_decode, opscale_op_profile,
     desc_rmsnorm, desc_linear, desc_swiglu, desc_attn_prefill, desc_attn_decode,
     OPSCALE_OK, OPSCALE_ERR_INVALID_ARG, OPSCALE_ERR_UNSUPPORTED, OPSCALE_ERR_WORKSPACE,

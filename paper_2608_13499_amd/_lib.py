@@ -52,7 +52,7 @@ class _PrefillArgs(ctypes.Structure):
 
 
 class _DecodeArgs(ctypes.Structure):
-    _fields_ = [("q", c_vp), ("k_cache", c_vp), ("v_cache", c_vp), ("block_table", c_vp),
+    _fields_ = [("q", c_vp), ("q_row_stride", c_i64), ("k_cache", c_vp), ("v_cache", c_vp), ("block_table", c_vp),
                 ("context_lens", c_vp), ("o", c_vp), ("B", c_i32), ("Hq", c_i32), ("Hkv", c_i32),
                 ("D", c_i32), ("block_size", c_i32), ("max_blocks_per_seq", c_i32), ("num_blocks", c_i64),
                 ("max_context_len", c_i32), ("scale", c_f32), ("workspace", c_vp), ("workspace_bytes", c_sz)]
@@ -88,11 +88,17 @@ EXPORTS = {
     "opscale_attn_prefill": (c_i32, [c_vp, c_vp, c_vp, c_i64, c_i64, c_vp, c_vp, c_i32, c_i64, c_i32,
                                      c_i32, c_i32, c_i32, c_f32, c_i32, c_i32, c_vp, ctypes.POINTER(Timing)]),
     "opscale_attn_decode_workspace_size": (c_sz, [c_i32, c_i32, c_i32, c_i32]),
-    "opscale_attn_decode": (c_i32, [c_vp, c_vp, c_vp, c_vp, c_vp, c_vp, c_i32, c_i32, c_i32, c_i32, c_i32,
+    "opscale_attn_decode": (c_i32, [c_vp, c_i64, c_vp, c_vp, c_vp, c_vp, c_vp, c_i32, c_i32, c_i32, c_i32, c_i32,
                                     c_i32, c_i64, c_i32, c_f32, c_i32, c_vp, c_sz, c_vp,
                                     ctypes.POINTER(Timing)]),
     "opscale_op_profile": (c_i32, [ctypes.POINTER(OpDesc), c_i32, c_i32, c_vp, c_sz, c_vp,
                                    ctypes.POINTER(Profile)]),
+    "opscale_rope": (c_i32, [c_vp, c_vp, c_i64, c_i64, c_vp, c_i64, c_i32, c_i32, c_i32, ctypes.c_double, c_i32,
+                             c_vp, ctypes.POINTER(Timing)]),
+    "opscale_reshape_and_cache": (c_i32, [c_vp, c_vp, c_i64, c_vp, c_vp, c_vp, c_i64, c_i32, c_i32, c_i32, c_i64,
+                                          c_i32, c_vp, ctypes.POINTER(Timing)]),
+    "opscale_add_rmsnorm": (c_i32, [c_vp, c_vp, c_vp, c_vp, c_i64, c_i64, c_f32, c_i32, c_vp,
+                                    ctypes.POINTER(Timing)]),
 }
 
 _lib = None
@@ -156,6 +162,11 @@ def _contig(name, t):
 
 
 # --------------------------------------------------------------- operators --
+def _heads_view(name, t_, H, D):
+    if t_.dim() != 3 or t_.shape[1] != H or t_.shape[2] != D or t_.stride(2) != 1 or t_.stride(1) != D:
+        raise OpscaleError(OPSCALE_ERR_INVALID_ARG, f"{name} must be [T, {H}, {D}] with contiguous heads")
+
+
 def opscale_version() -> str:
     return load().opscale_version().decode()
 
@@ -251,28 +262,95 @@ def opscale_attn_decode_workspace_size(B: int, Hq: int, D: int, max_context_len:
 def opscale_attn_decode(q, k_cache, v_cache, block_table, context_lens, max_context_len: int,
                         scale: float, workspace=None, out=None, stream=None, timed: bool = False):
     """Decode attention over a paged cache [num_blocks, block_size, Hkv, D].
-    block_table int32 [B, max_blocks]; context_lens int32 [B].  `workspace`
-    (a uint8 GPU tensor) is allocated by torch when not given."""
+    q [B, Hq, D] may be strided in its first dimension (a view into the QKV
+    output).  block_table int32 [B, max_blocks]; context_lens int32 [B].
+    `workspace` (a uint8 GPU tensor) is allocated by torch when not given."""
     import torch
     lib = load()
     _dev(q, k_cache, v_cache, block_table, context_lens, workspace, out)
-    for n, t_ in (("q", q), ("k_cache", k_cache), ("v_cache", v_cache), ("block_table", block_table),
+    for n, t_ in (("k_cache", k_cache), ("v_cache", v_cache), ("block_table", block_table),
                   ("context_lens", context_lens)):
         _contig(n, t_)
     B, Hq, D = q.shape
+    _heads_view("q", q, Hq, D)
     num_blocks, bs, Hkv, _ = k_cache.shape
     need = opscale_attn_decode_workspace_size(B, Hq, D, max_context_len)
     if workspace is None:
         workspace = torch.empty(need, dtype=torch.uint8, device=q.device)
     if out is None:
-        out = torch.empty_like(q)
+        out = torch.empty(B, Hq, D, dtype=q.dtype, device=q.device)
+    _contig("out", out)
     t = Timing() if timed else None
-    _check(lib.opscale_attn_decode(_ptr(q), _ptr(k_cache), _ptr(v_cache), _ptr(block_table),
+    _check(lib.opscale_attn_decode(_ptr(q), q.stride(0), _ptr(k_cache), _ptr(v_cache), _ptr(block_table),
                                    _ptr(context_lens), _ptr(out), B, Hq, Hkv, D, bs, block_table.shape[1],
                                    num_blocks, max_context_len, scale, _dt(q), _ptr(workspace),
                                    workspace.numel() * workspace.element_size(), _stream(stream),
                                    ctypes.byref(t) if t else None))
     return (out, t) if timed else out
+
+
+def opscale_rope(q, k, positions, theta: float, stream=None, timed: bool = False):
+    """Rotary embedding of q [T, Hq, D] and k [T, Hkv, D] in place (rotate-half
+    form); the token dimension may be strided (views into the QKV output).
+    positions: int32 [T] on the GPU.  Returns (q, k)."""
+    import torch
+    lib = load()
+    _dev(q, k, positions)
+    T, Hq, D = q.shape
+    Hkv = k.shape[1]
+    _heads_view("q", q, Hq, D)
+    _heads_view("k", k, Hkv, D)
+    if k.shape[0] != T or positions.dtype != torch.int32 or positions.numel() != T:
+        raise OpscaleError(OPSCALE_ERR_INVALID_ARG, "k must have T rows and positions be int32 [T]")
+    _contig("positions", positions)
+    t = Timing() if timed else None
+    _check(lib.opscale_rope(_ptr(q), _ptr(k), q.stride(0), k.stride(0), _ptr(positions), T, Hq, Hkv, D,
+                            float(theta), _dt(q), _stream(stream), ctypes.byref(t) if t else None))
+    return ((q, k), t) if timed else (q, k)
+
+
+def opscale_reshape_and_cache(k, v, k_cache, v_cache, slot_mapping, stream=None, timed: bool = False):
+    """Write k, v [T, Hkv, D] (token dimension may be strided) into the paged
+    caches [num_blocks, block_size, Hkv, D] at the int32 slots; slots outside
+    the cache are skipped."""
+    import torch
+    lib = load()
+    _dev(k, v, k_cache, v_cache, slot_mapping)
+    T, Hkv, D = k.shape
+    _heads_view("k", k, Hkv, D)
+    _heads_view("v", v, Hkv, D)
+    if k.stride(0) != v.stride(0):
+        raise OpscaleError(OPSCALE_ERR_INVALID_ARG, "k and v must share a row stride")
+    for n, t_ in (("k_cache", k_cache), ("v_cache", v_cache), ("slot_mapping", slot_mapping)):
+        _contig(n, t_)
+    if slot_mapping.dtype != torch.int32 or slot_mapping.numel() != T:
+        raise OpscaleError(OPSCALE_ERR_INVALID_ARG, "slot_mapping must be int32 [T]")
+    nb, bs = k_cache.shape[0], k_cache.shape[1]
+    if tuple(k_cache.shape) != (nb, bs, Hkv, D) or tuple(v_cache.shape) != tuple(k_cache.shape):
+        raise OpscaleError(OPSCALE_ERR_INVALID_ARG, f"caches must be [num_blocks, block_size, {Hkv}, {D}]")
+    t = Timing() if timed else None
+    _check(lib.opscale_reshape_and_cache(_ptr(k), _ptr(v), k.stride(0), _ptr(k_cache), _ptr(v_cache),
+                                         _ptr(slot_mapping), T, Hkv, D, bs, nb, _dt(k), _stream(stream),
+                                         ctypes.byref(t) if t else None))
+    return t if timed else None
+
+
+def opscale_add_rmsnorm(x, residual, w, y=None, eps: float = 1e-5, stream=None, timed: bool = False):
+    """residual <- x + residual; y = rmsnorm(residual) * w.  Returns y."""
+    import torch
+    lib = load()
+    _dev(x, residual, w, y)
+    for n, t_ in (("x", x), ("residual", residual), ("w", w)):
+        _contig(n, t_)
+    if y is None:
+        y = torch.empty_like(x)
+    _contig("y", y)
+    H = x.shape[-1]
+    M = x.numel() // H if H else 0
+    t = Timing() if timed else None
+    _check(lib.opscale_add_rmsnorm(_ptr(x), _ptr(residual), _ptr(w), _ptr(y), M, H, eps, _dt(x), _stream(stream),
+                                   ctypes.byref(t) if t else None))
+    return (y, t) if timed else y
 
 
 def opscale_op_profile(desc: OpDesc, warmup: int = 5, iters: int = 20, flush=None, stream=None) -> Profile:
@@ -321,7 +399,8 @@ def desc_attn_decode(q, k_cache, v_cache, block_table, context_lens, out, max_co
     d = OpDesc(op=OP_ATTN_DECODE, dt=_dt(q))
     B, Hq, D = q.shape
     nb, bs, Hkv, _ = k_cache.shape
-    d.u.attn_decode = _DecodeArgs(_ptr(q), _ptr(k_cache), _ptr(v_cache), _ptr(block_table),
+    _heads_view("q", q, Hq, D)
+    d.u.attn_decode = _DecodeArgs(_ptr(q), q.stride(0), _ptr(k_cache), _ptr(v_cache), _ptr(block_table),
                                   _ptr(context_lens), _ptr(out), B, Hq, Hkv, D, bs, block_table.shape[1],
                                   nb, max_context_len, scale, _ptr(workspace),
                                   workspace.numel() * workspace.element_size())

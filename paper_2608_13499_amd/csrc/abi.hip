@@ -127,6 +127,16 @@ Work work_decode(const std::vector<int32_t>& ctx, int64_t Hq, int64_t Hkv, int64
   return {4.0 * D * Hq * N, by, 0, (int64_t)by, s * B * Hq * D};
 }
 
+Work work_rope(int64_t T, int64_t Hq, int64_t Hkv, int64_t D, int s) {
+  return {3.0 * T * (Hq + Hkv) * D, 2.0 * s * T * (Hq + Hkv) * D + 4.0 * T};
+}
+Work work_cache_write(int64_t T, int64_t Hkv, int64_t D, int s) {
+  return {0.0, 4.0 * s * T * Hkv * D + 4.0 * T};
+}
+Work work_add_rmsnorm(int64_t M, int64_t H, int s) {
+  return {5.0 * M * H, (double)s * (4.0 * M * H + H)};
+}
+
 opscale_status copy_ints(std::vector<int32_t>& dst, const int32_t* src, int64_t n, hipStream_t s) {
   dst.resize((size_t)n);
   if (n == 0) return OPSCALE_OK;
@@ -212,7 +222,7 @@ opscale_status check_prefill(const void* q, const void* k, const void* v, int64_
   return OPSCALE_OK;
 }
 
-opscale_status check_decode(const void* q, const void* kc, const void* vc, const int32_t* table,
+opscale_status check_decode(const void* q, int64_t qs, const void* kc, const void* vc, const int32_t* table,
                             const int32_t* ctx, void* o, int32_t B, int32_t Hq, int32_t Hkv, int32_t D,
                             int32_t bs, int32_t max_blocks, int64_t num_blocks, int32_t max_ctx,
                             float scale, opscale_dtype dt, void* ws, size_t ws_bytes) {
@@ -232,6 +242,9 @@ opscale_status check_decode(const void* q, const void* kc, const void* vc, const
   if (max_blocks < 1 || (int64_t)max_blocks * bs >= kMaxDim || num_blocks < 1 || max_ctx < 1)
     return fail(OPSCALE_ERR_INVALID_ARG, "attn_decode: max_blocks_per_seq=%d num_blocks=%lld max_context_len=%d",
                 max_blocks, (long long)num_blocks, max_ctx);
+  if (qs < (int64_t)Hq * D || qs % (16 / esize(dt)) || qs > (1 << 24))
+    return fail(OPSCALE_ERR_INVALID_ARG, "attn_decode: q_row_stride=%lld must cover the heads, be a multiple of 16 bytes and <= 2^24",
+                (long long)qs);
   if (!q || !kc || !vc || !table || !ctx || !o) return fail(OPSCALE_ERR_INVALID_ARG, "attn_decode: null pointer");
   if (!aligned16(q) || !aligned16(kc) || !aligned16(vc) || !aligned16(o) ||
       (reinterpret_cast<uintptr_t>(table) & 3) || (reinterpret_cast<uintptr_t>(ctx) & 3))
@@ -240,6 +253,64 @@ opscale_status check_decode(const void* q, const void* kc, const void* vc, const
   if (dt == OPSCALE_BF16 && (!ws || ws_bytes < need || !aligned16(ws)))
     return fail(OPSCALE_ERR_WORKSPACE, "attn_decode: workspace of %zu bytes (16-byte aligned) needed, got %zu",
                 need, ws ? ws_bytes : (size_t)0);
+  return OPSCALE_OK;
+}
+
+opscale_status check_rope(void* q, void* k, int64_t qs, int64_t ks, const int32_t* pos, int64_t T, int32_t Hq,
+                          int32_t Hkv, int32_t D, double theta, opscale_dtype dt) {
+  if (!dtype_ok(dt)) return fail(OPSCALE_ERR_INVALID_ARG, "rope: unknown dtype %d", (int)dt);
+  if (T < 0 || T >= kMaxDim || Hq <= 0 || Hkv <= 0 || Hq > 65535 || Hkv > 65535)
+    return fail(OPSCALE_ERR_INVALID_ARG, "rope: bad sizes T=%lld Hq=%d Hkv=%d", (long long)T, Hq, Hkv);
+  if (D != 64 && D != 128) return fail(OPSCALE_ERR_UNSUPPORTED, "rope: head_dim %d (supported: 64, 128)", D);
+  if (!(theta > 0.0) || !std::isfinite(theta)) return fail(OPSCALE_ERR_INVALID_ARG, "rope: theta must be finite and > 0");
+  if (T == 0) return OPSCALE_OK;
+  const int vec = 16 / esize(dt);
+  if (qs < (int64_t)Hq * D || ks < (int64_t)Hkv * D || qs % vec || ks % vec)
+    return fail(OPSCALE_ERR_INVALID_ARG, "rope: row strides q=%lld k=%lld must cover the heads and be multiples of %d",
+                (long long)qs, (long long)ks, vec);
+  if (!q || !k || !pos) return fail(OPSCALE_ERR_INVALID_ARG, "rope: null pointer");
+  if (!aligned16(q) || !aligned16(k) || (reinterpret_cast<uintptr_t>(pos) & 3))
+    return fail(OPSCALE_ERR_INVALID_ARG, "rope: q, k must be 16-byte aligned, positions 4-byte");
+  return OPSCALE_OK;
+}
+
+opscale_status check_cache_write(const void* k, const void* v, int64_t kvs, void* kc, void* vc, const int32_t* slots,
+                                 int64_t T, int32_t Hkv, int32_t D, int32_t bs, int64_t nb, opscale_dtype dt) {
+  if (!dtype_ok(dt)) return fail(OPSCALE_ERR_INVALID_ARG, "reshape_and_cache: unknown dtype %d", (int)dt);
+  if (T < 0 || T >= kMaxDim || Hkv <= 0 || D <= 0 || (int64_t)Hkv * D > (1 << 20))
+    return fail(OPSCALE_ERR_INVALID_ARG, "reshape_and_cache: bad sizes T=%lld Hkv=%d D=%d", (long long)T, Hkv, D);
+  const int s = esize(dt);
+  if (((int64_t)Hkv * D * s) % 16)
+    return fail(OPSCALE_ERR_INVALID_ARG, "reshape_and_cache: a row (Hkv*D*sizeof(dt)) must be a multiple of 16 bytes");
+  if (bs < 1 || nb < 1 || nb * bs >= ((int64_t)1 << 31))
+    return fail(OPSCALE_ERR_INVALID_ARG, "reshape_and_cache: block_size=%d num_blocks=%lld", bs, (long long)nb);
+  if (T == 0) return OPSCALE_OK;
+  if (kvs < (int64_t)Hkv * D || (kvs * s) % 16)
+    return fail(OPSCALE_ERR_INVALID_ARG, "reshape_and_cache: kv_row_stride=%lld must cover the heads and be a multiple of 16 bytes",
+                (long long)kvs);
+  if (!k || !v || !kc || !vc || !slots) return fail(OPSCALE_ERR_INVALID_ARG, "reshape_and_cache: null pointer");
+  if (!aligned16(k) || !aligned16(v) || !aligned16(kc) || !aligned16(vc) || (reinterpret_cast<uintptr_t>(slots) & 3))
+    return fail(OPSCALE_ERR_INVALID_ARG, "reshape_and_cache: tensors must be 16-byte aligned, slots 4-byte");
+  const int64_t cache_bytes = nb * bs * Hkv * D * s, in_bytes = ((T - 1) * kvs + (int64_t)Hkv * D) * s;
+  if (overlap(kc, cache_bytes, k, in_bytes) || overlap(kc, cache_bytes, v, in_bytes) ||
+      overlap(vc, cache_bytes, k, in_bytes) || overlap(vc, cache_bytes, v, in_bytes) ||
+      overlap(kc, cache_bytes, vc, cache_bytes))
+    return fail(OPSCALE_ERR_INVALID_ARG, "reshape_and_cache: the caches must not overlap k, v or each other");
+  return OPSCALE_OK;
+}
+
+opscale_status check_add_rmsnorm(const void* x, void* res, const void* w, void* y, int64_t M, int64_t H, float eps,
+                                 opscale_dtype dt) {
+  opscale_status st = check_rmsnorm(x, w, y, M, H, eps, dt);
+  if (st != OPSCALE_OK || M == 0) return st;
+  if (H * esize(dt) > 16384)
+    return fail(OPSCALE_ERR_UNSUPPORTED, "add_rmsnorm: rows of up to 16 KB (H*sizeof(dt)), got %lld bytes",
+                (long long)(H * esize(dt)));
+  if (!res) return fail(OPSCALE_ERR_INVALID_ARG, "add_rmsnorm: null residual");
+  if (!aligned16(res)) return fail(OPSCALE_ERR_INVALID_ARG, "add_rmsnorm: residual must be 16-byte aligned");
+  const int64_t nb = M * H * esize(dt);
+  if (overlap(res, nb, x, nb) || overlap(res, nb, y, nb) || overlap(res, nb, w, H * esize(dt)))
+    return fail(OPSCALE_ERR_INVALID_ARG, "add_rmsnorm: residual must not overlap x, y or w");
   return OPSCALE_OK;
 }
 
@@ -345,21 +416,21 @@ size_t opscale_attn_decode_workspace_size(int32_t B, int32_t Hq, int32_t D, int3
   return opscale::decode_workspace_bytes(B, Hq, D, std::max<int32_t>(1, max_context_len));
 }
 
-opscale_status opscale_attn_decode(const void* q, const void* k_cache, const void* v_cache,
+opscale_status opscale_attn_decode(const void* q, int64_t q_row_stride, const void* k_cache, const void* v_cache,
                                    const int32_t* block_table, const int32_t* context_lens, void* o,
                                    int32_t B, int32_t Hq, int32_t Hkv, int32_t D, int32_t block_size,
                                    int32_t max_blocks_per_seq, int64_t num_blocks,
                                    int32_t max_context_len, float scale, opscale_dtype dt,
                                    void* workspace, size_t workspace_bytes, hipStream_t stream,
                                    opscale_timing* timing) {
-  opscale_status st = check_decode(q, k_cache, v_cache, block_table, context_lens, o, B, Hq, Hkv, D,
+  opscale_status st = check_decode(q, q_row_stride, k_cache, v_cache, block_table, context_lens, o, B, Hq, Hkv, D,
                                    block_size, max_blocks_per_seq, num_blocks, max_context_len,
                                    scale, dt, workspace, workspace_bytes);
   if (st != OPSCALE_OK) return st;
   zero_timing(timing);
   if (B == 0) return OPSCALE_OK;
   st = run_timed(stream, timing, "attn_decode launch", [&] {
-    return opscale::launch_attn_decode(q, k_cache, v_cache, block_table, context_lens, o, B, Hq, Hkv,
+    return opscale::launch_attn_decode(q, q_row_stride, k_cache, v_cache, block_table, context_lens, o, B, Hq, Hkv,
                                        D, block_size, max_blocks_per_seq, num_blocks,
                                        max_context_len, scale, dt == OPSCALE_BF16, workspace, stream);
   });
@@ -368,6 +439,63 @@ opscale_status opscale_attn_decode(const void* q, const void* k_cache, const voi
     st = copy_ints(ctx, context_lens, B, stream);
     if (st != OPSCALE_OK) return st;
     const Work wk = work_decode(ctx, Hq, Hkv, D, esize(dt), block_size, max_blocks_per_seq);
+    timing->alg_flops = wk.flops;
+    timing->alg_bytes = wk.bytes;
+  }
+  return st;
+}
+
+opscale_status opscale_rope(void* q, void* k, int64_t q_row_stride, int64_t k_row_stride,
+                            const int32_t* positions, int64_t T, int32_t Hq, int32_t Hkv, int32_t D,
+                            double theta, opscale_dtype dt, hipStream_t stream, opscale_timing* timing) {
+  opscale_status st = check_rope(q, k, q_row_stride, k_row_stride, positions, T, Hq, Hkv, D, theta, dt);
+  if (st != OPSCALE_OK) return st;
+  zero_timing(timing);
+  if (T == 0) return OPSCALE_OK;
+  st = run_timed(stream, timing, "rope launch", [&] {
+    return opscale::launch_rope(q, k, q_row_stride, k_row_stride, positions, T, Hq, Hkv, D, theta,
+                                dt == OPSCALE_BF16, stream);
+  });
+  if (st == OPSCALE_OK && timing) {
+    const Work wk = work_rope(T, Hq, Hkv, D, esize(dt));
+    timing->alg_flops = wk.flops;
+    timing->alg_bytes = wk.bytes;
+  }
+  return st;
+}
+
+opscale_status opscale_reshape_and_cache(const void* k, const void* v, int64_t kv_row_stride, void* k_cache,
+                                         void* v_cache, const int32_t* slot_mapping, int64_t T, int32_t Hkv,
+                                         int32_t D, int32_t block_size, int64_t num_blocks, opscale_dtype dt,
+                                         hipStream_t stream, opscale_timing* timing) {
+  opscale_status st = check_cache_write(k, v, kv_row_stride, k_cache, v_cache, slot_mapping, T, Hkv, D, block_size,
+                                        num_blocks, dt);
+  if (st != OPSCALE_OK) return st;
+  zero_timing(timing);
+  if (T == 0) return OPSCALE_OK;
+  st = run_timed(stream, timing, "reshape_and_cache launch", [&] {
+    return opscale::launch_cache_write(k, v, kv_row_stride, k_cache, v_cache, slot_mapping, T, Hkv, D,
+                                       num_blocks * block_size, dt == OPSCALE_BF16, stream);
+  });
+  if (st == OPSCALE_OK && timing) {
+    const Work wk = work_cache_write(T, Hkv, D, esize(dt));
+    timing->alg_flops = wk.flops;
+    timing->alg_bytes = wk.bytes;
+  }
+  return st;
+}
+
+opscale_status opscale_add_rmsnorm(const void* x, void* residual, const void* w, void* y, int64_t M, int64_t H,
+                                   float eps, opscale_dtype dt, hipStream_t stream, opscale_timing* timing) {
+  opscale_status st = check_add_rmsnorm(x, residual, w, y, M, H, eps, dt);
+  if (st != OPSCALE_OK) return st;
+  zero_timing(timing);
+  if (M == 0) return OPSCALE_OK;
+  st = run_timed(stream, timing, "add_rmsnorm launch", [&] {
+    return opscale::launch_add_rmsnorm(x, residual, w, y, M, H, eps, dt == OPSCALE_BF16, stream);
+  });
+  if (st == OPSCALE_OK && timing) {
+    const Work wk = work_add_rmsnorm(M, H, esize(dt));
     timing->alg_flops = wk.flops;
     timing->alg_bytes = wk.bytes;
   }
@@ -433,13 +561,13 @@ opscale_status opscale_op_profile(const opscale_op_desc* d, int32_t warmup, int3
     }
     case OPSCALE_OP_ATTN_DECODE: {
       const auto& a = d->u.attn_decode;
-      st = check_decode(a.q, a.k_cache, a.v_cache, a.block_table, a.context_lens, a.o, a.B, a.Hq,
+      st = check_decode(a.q, a.q_row_stride, a.k_cache, a.v_cache, a.block_table, a.context_lens, a.o, a.B, a.Hq,
                         a.Hkv, a.D, a.block_size, a.max_blocks_per_seq, a.num_blocks,
                         a.max_context_len, a.scale, dt, a.workspace, a.workspace_bytes);
       if (st != OPSCALE_OK) return st;
       if (a.B == 0) return fail(OPSCALE_ERR_INVALID_ARG, "op_profile: empty problem");
       launch = [=] {
-        return opscale::launch_attn_decode(a.q, a.k_cache, a.v_cache, a.block_table, a.context_lens,
+        return opscale::launch_attn_decode(a.q, a.q_row_stride, a.k_cache, a.v_cache, a.block_table, a.context_lens,
                                            a.o, a.B, a.Hq, a.Hkv, a.D, a.block_size,
                                            a.max_blocks_per_seq, a.num_blocks, a.max_context_len,
                                            a.scale, bf16, a.workspace, stream);

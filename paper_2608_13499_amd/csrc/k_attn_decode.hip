@@ -83,7 +83,7 @@ size_t decode_workspace_bytes(int32_t B, int32_t Hq, int32_t D, int32_t max_cont
 // HB: KV heads per workgroup (8 / HB waves share one head's key tiles).
 template <int D, int G, int HB>
 __global__ __launch_bounds__(512, 4) void attn_decode_split_kernel(
-    const __bf16* __restrict__ q, const __bf16* __restrict__ kc, const __bf16* __restrict__ vc,
+    const __bf16* __restrict__ q, int64_t q_stride, const __bf16* __restrict__ kc, const __bf16* __restrict__ vc,
     const int32_t* __restrict__ table, const int32_t* __restrict__ ctx, int Hq, int Hkv,
     int log2bs, int max_blocks, int64_t num_blocks, int max_splits, float scale_log2,
     float* __restrict__ ws_o, float* __restrict__ ws_ml) {
@@ -117,7 +117,7 @@ __global__ __launch_bounds__(512, 4) void attn_decode_split_kernel(
   bf16x8 qf[KSTEPS];
   {
     const bool has = col < G;
-    const __bf16* qrow = q + ((int64_t)b * Hq + (int64_t)g * G + (has ? col : 0)) * D;
+    const __bf16* qrow = q + (int64_t)b * q_stride + ((int64_t)g * G + (has ? col : 0)) * D;
 #pragma unroll
     for (int s = 0; s < KSTEPS; ++s) {
       u32x4 w = {0u, 0u, 0u, 0u};
@@ -145,7 +145,7 @@ __global__ __launch_bounds__(512, 4) void attn_decode_split_kernel(
   // Cache row of key j for head g.  Skipped keys read the sequence's first
   // query row instead (finite data; their probability is exactly 0), so every
   // lane always issues every load and the vmcnt bookkeeping below is exact.
-  const __bf16* dummy = q + (int64_t)b * Hq * D;
+  const __bf16* dummy = q + (int64_t)b * q_stride;
   auto row_ptr = [&](const __bf16* cache, int j) -> const __bf16* {
     if (!key_ok(j)) return dummy;
     const int blk = pages[(j >> log2bs) - p_first];
@@ -353,7 +353,7 @@ __global__ __launch_bounds__(64) void attn_decode_combine_kernel(
 // ------------------------------------------------------------ fp32 path ----
 template <int D>
 __global__ __launch_bounds__(64) void attn_decode_f32_kernel(
-    const float* __restrict__ q, const float* __restrict__ kc, const float* __restrict__ vc,
+    const float* __restrict__ q, int64_t q_stride, const float* __restrict__ kc, const float* __restrict__ vc,
     const int32_t* __restrict__ table, const int32_t* __restrict__ ctx, float* __restrict__ o,
     int Hq, int Hkv, int log2bs, int max_blocks, int64_t num_blocks, float scale) {
   constexpr int DPL = D / 64;
@@ -365,7 +365,7 @@ __global__ __launch_bounds__(64) void attn_decode_f32_kernel(
   const int bs = 1 << log2bs;
   const int n = min(ctx[b], max_blocks << log2bs);
   const int32_t* trow = table + (int64_t)b * max_blocks;
-  for (int d = lane; d < D; d += 64) qs[d] = q[((int64_t)b * Hq + h) * D + d];
+  for (int d = lane; d < D; d += 64) qs[d] = q[(int64_t)b * q_stride + (int64_t)h * D + d];
   __syncthreads();
   float m_run = -INFINITY, l_run = 0.f, acc[DPL] = {};
   for (int kv0 = 0; kv0 < n; kv0 += 64) {
@@ -405,7 +405,7 @@ __global__ __launch_bounds__(64) void attn_decode_f32_kernel(
   for (int c = 0; c < DPL; ++c) o[((int64_t)b * Hq + h) * D + lane + c * 64] = acc[c] * inv;
 }
 
-hipError_t launch_attn_decode(const void* q, const void* kcache, const void* vcache,
+hipError_t launch_attn_decode(const void* q, int64_t q_stride, const void* kcache, const void* vcache,
                               const int32_t* table, const int32_t* ctx, void* o, int32_t B,
                               int32_t Hq, int32_t Hkv, int32_t D, int32_t block_size,
                               int32_t max_blocks, int64_t num_blocks, int32_t max_context_len,
@@ -416,12 +416,12 @@ hipError_t launch_attn_decode(const void* q, const void* kcache, const void* vca
     const dim3 grid((unsigned)Hq, (unsigned)B);
     if (D == 128)
       hipLaunchKernelGGL((attn_decode_f32_kernel<128>), grid, dim3(64), 0, s,
-                         static_cast<const float*>(q), static_cast<const float*>(kcache),
+                         static_cast<const float*>(q), q_stride, static_cast<const float*>(kcache),
                          static_cast<const float*>(vcache), table, ctx, static_cast<float*>(o), Hq,
                          Hkv, log2bs, max_blocks, num_blocks, scale);
     else
       hipLaunchKernelGGL((attn_decode_f32_kernel<64>), grid, dim3(64), 0, s,
-                         static_cast<const float*>(q), static_cast<const float*>(kcache),
+                         static_cast<const float*>(q), q_stride, static_cast<const float*>(kcache),
                          static_cast<const float*>(vcache), table, ctx, static_cast<float*>(o), Hq,
                          Hkv, log2bs, max_blocks, num_blocks, scale);
     return hipGetLastError();
@@ -435,7 +435,7 @@ hipError_t launch_attn_decode(const void* q, const void* kcache, const void* vca
   const dim3 grid((unsigned)max_splits, (unsigned)(Hkv / HB), (unsigned)B);
 #define OPS_DEC(DD, GG, HH)                                                                     \
   hipLaunchKernelGGL((attn_decode_split_kernel<DD, GG, HH>), grid, dim3(kWaves * 64), 0, s,     \
-                     static_cast<const __bf16*>(q), static_cast<const __bf16*>(kcache),         \
+                     static_cast<const __bf16*>(q), q_stride, static_cast<const __bf16*>(kcache), \
                      static_cast<const __bf16*>(vcache), table, ctx, Hq, Hkv, log2bs, max_blocks, \
                      num_blocks, max_splits, sl2, ws_o, ws_ml)
 #define OPS_DEC_H(DD, GG)                    \

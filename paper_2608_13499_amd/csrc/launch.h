@@ -25,11 +25,25 @@ hipError_t launch_attn_prefill(const void* q, const void* k, const void* v, int6
 int32_t decode_max_splits(int32_t max_context_len);
 size_t decode_workspace_bytes(int32_t B, int32_t Hq, int32_t D, int32_t max_context_len);
 
-hipError_t launch_attn_decode(const void* q, const void* kc, const void* vc, const int32_t* table,
+hipError_t launch_attn_decode(const void* q, int64_t q_stride, const void* kc, const void* vc, const int32_t* table,
                               const int32_t* ctx, void* o, int32_t B, int32_t Hq, int32_t Hkv,
                               int32_t D, int32_t block_size, int32_t max_blocks, int64_t num_blocks,
                               int32_t max_context_len, float scale, bool bf16, void* ws,
                               hipStream_t s);
+
+// Rotary embedding of the q and k heads in place (rows of q_stride /
+// k_stride elements, token t at position pos[t]).
+hipError_t launch_rope(void* q, void* k, int64_t q_stride, int64_t k_stride, const int32_t* pos, int64_t T,
+                       int32_t Hq, int32_t Hkv, int32_t D, double theta, bool bf16, hipStream_t s);
+
+// K/V rows of T tokens to cache rows slots[t] (skipped outside [0, num_slots)).
+hipError_t launch_cache_write(const void* k, const void* v, int64_t kv_stride, void* kc, void* vc,
+                              const int32_t* slots, int64_t T, int32_t Hkv, int32_t D, int64_t num_slots,
+                              bool bf16, hipStream_t s);
+
+// residual <- x + residual; y <- rmsnorm(residual) * w.
+hipError_t launch_add_rmsnorm(const void* x, void* res, const void* w, void* y, int64_t M, int64_t H, float eps,
+                              bool bf16, hipStream_t s);
 
 // Writes a fixed pattern over `bytes` of `buf` (evicts the last-level cache
 // before a timed iteration).

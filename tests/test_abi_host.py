@@ -27,7 +27,8 @@ def test_header_declares_expected_entry_points():
     d = _declared()
     for name in ("opscale_rmsnorm", "opscale_linear", "opscale_swiglu", "opscale_attn_prefill",
                  "opscale_attn_decode", "opscale_attn_decode_workspace_size", "opscale_op_profile",
-                 "opscale_version", "opscale_status_string", "opscale_last_error"):
+                 "opscale_version", "opscale_status_string", "opscale_last_error",
+                 "opscale_rope", "opscale_reshape_and_cache", "opscale_add_rmsnorm"):
         assert name in d
 
 
@@ -105,13 +106,13 @@ def test_decode_validation_and_workspace(lib):
     f = lib.opscale_attn_decode
     need = lib.opscale_attn_decode_workspace_size(256, 32, 128, 8192)
     assert need == 4 * 256 * 32 * 16 * 130
-    ok = dict(q=A16, kc=A16, vc=A16, tab=A16, ctx=A16, o=A16 * 8, B=256, Hq=32, Hkv=8, D=128, bs=16, mb=512,
-              nb=69424, mc=8192, scale=0.08, dt=1, ws=A16 * 32, wsb=need)
+    ok = dict(q=A16, qs=32 * 128, kc=A16, vc=A16, tab=A16, ctx=A16, o=A16 * 8, B=256, Hq=32, Hkv=8, D=128, bs=16,
+              mb=512, nb=69424, mc=8192, scale=0.08, dt=1, ws=A16 * 32, wsb=need)
 
     def call(**kw):
         a = dict(ok, **kw)
-        return f(a["q"], a["kc"], a["vc"], a["tab"], a["ctx"], a["o"], a["B"], a["Hq"], a["Hkv"], a["D"], a["bs"],
-                 a["mb"], a["nb"], a["mc"], a["scale"], a["dt"], a["ws"], a["wsb"], None, None)
+        return f(a["q"], a["qs"], a["kc"], a["vc"], a["tab"], a["ctx"], a["o"], a["B"], a["Hq"], a["Hkv"], a["D"],
+                 a["bs"], a["mb"], a["nb"], a["mc"], a["scale"], a["dt"], a["ws"], a["wsb"], None, None)
 
     assert call(wsb=need - 1) == 3
     assert call(ws=None) == 3
@@ -120,4 +121,52 @@ def test_decode_validation_and_workspace(lib):
     assert call(D=256) == 2
     assert call(tab=None) == 1
     assert call(mb=0) == 1
+    assert call(qs=32 * 128 - 8) == 1      # stride smaller than the heads
+    assert call(qs=48 * 128 + 4) == 1      # not a multiple of 16 bytes
     assert call(B=0) == 0
+
+
+def test_rope_validation(lib):
+    f = lib.opscale_rope
+    ok = dict(q=A16, k=A16 * 2, qs=48 * 128, ks=48 * 128, pos=A16 * 4, T=100, Hq=32, Hkv=8, D=128, theta=5e5, dt=1)
+
+    def call(**kw):
+        a = dict(ok, **kw)
+        return f(a["q"], a["k"], a["qs"], a["ks"], a["pos"], a["T"], a["Hq"], a["Hkv"], a["D"], a["theta"], a["dt"],
+                 None, None)
+
+    assert call(D=96) == 2
+    assert call(theta=0.0) == 1 and call(theta=float("inf")) == 1
+    assert call(qs=100) == 1               # smaller than the heads
+    assert call(ks=8 * 128 + 4) == 1       # not a multiple of 16 bytes
+    assert call(pos=None) == 1
+    assert call(pos=A16 + 2) == 1          # misaligned positions
+    assert call(q=A16 + 8) == 1
+    assert call(T=0) == 0
+
+
+def test_reshape_and_cache_validation(lib):
+    f = lib.opscale_reshape_and_cache
+    ok = dict(k=A16, v=A16 * 2, kvs=48 * 128, kc=A16 * 64, vc=A16 * 128, sl=A16 * 4, T=10, Hkv=8, D=128, bs=16,
+              nb=1024, dt=1)
+
+    def call(**kw):
+        a = dict(ok, **kw)
+        return f(a["k"], a["v"], a["kvs"], a["kc"], a["vc"], a["sl"], a["T"], a["Hkv"], a["D"], a["bs"], a["nb"],
+                 a["dt"], None, None)
+
+    assert call(D=3, Hkv=1) == 1            # a row is not a multiple of 16 bytes
+    assert call(nb=1 << 27, bs=16) == 1     # slots do not fit in int32
+    assert call(kvs=100) == 1
+    assert call(sl=None) == 1
+    assert call(kc=A16 + 16 * 1024) == 1    # k_cache overlaps k
+    assert call(vc=A16 * 64 + 1024) == 1    # the caches overlap each other
+    assert call(T=0) == 0
+
+
+def test_add_rmsnorm_validation(lib):
+    f = lib.opscale_add_rmsnorm
+    assert f(A16, A16 * 4, A16 * 2, A16 * 8, 4, 16384, 1e-5, 1, None, None) == 2   # 32 KB rows
+    assert f(A16, A16 + 32, A16 * 2, A16 * 8, 4, 4096, 1e-5, 1, None, None) == 1   # residual overlaps x
+    assert f(A16, None, A16 * 2, A16 * 8, 4, 4096, 1e-5, 1, None, None) == 1
+    assert f(A16, A16 * 4, A16 * 2, A16 * 4, 4, 4096, 1e-5, 1, None, None) == 1    # y is the residual
