@@ -229,7 +229,10 @@ typedef enum {
   OPSCALE_OP_LINEAR = 1,
   OPSCALE_OP_SWIGLU = 2,
   OPSCALE_OP_ATTN_PREFILL = 3,
-  OPSCALE_OP_ATTN_DECODE = 4
+  OPSCALE_OP_ATTN_DECODE = 4,
+  OPSCALE_OP_ROPE = 5,
+  OPSCALE_OP_RESHAPE_AND_CACHE = 6,
+  OPSCALE_OP_ADD_RMSNORM = 7
 } opscale_op;
 
 /* One operator call: the argument list of the matching entry point. */
@@ -251,6 +254,15 @@ typedef struct {
       int32_t B, Hq, Hkv, D, block_size, max_blocks_per_seq; int64_t num_blocks;
       int32_t max_context_len; float scale; void* workspace; size_t workspace_bytes;
     } attn_decode;
+    struct {
+      void *q, *k; int64_t q_row_stride, k_row_stride; const int32_t* positions; int64_t T;
+      int32_t Hq, Hkv, D; double theta;
+    } rope;
+    struct {
+      const void *k, *v; int64_t kv_row_stride; void *k_cache, *v_cache; const int32_t* slot_mapping;
+      int64_t T; int32_t Hkv, D, block_size; int64_t num_blocks;
+    } reshape_and_cache;
+    struct { const void* x; void* residual; const void* w; void* y; int64_t M, H; float eps; } add_rmsnorm;
   } u;
 } opscale_op_desc;
 

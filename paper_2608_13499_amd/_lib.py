@@ -16,7 +16,8 @@ LIB_PATH = os.path.join(_HERE, "libopscale.so")
 
 OPSCALE_OK, OPSCALE_ERR_INVALID_ARG, OPSCALE_ERR_UNSUPPORTED, OPSCALE_ERR_WORKSPACE, OPSCALE_ERR_HIP = range(5)
 OPSCALE_F32, OPSCALE_BF16 = 0, 1
-OP_RMSNORM, OP_LINEAR, OP_SWIGLU, OP_ATTN_PREFILL, OP_ATTN_DECODE = range(5)
+(OP_RMSNORM, OP_LINEAR, OP_SWIGLU, OP_ATTN_PREFILL, OP_ATTN_DECODE, OP_ROPE, OP_RESHAPE_AND_CACHE,
+ OP_ADD_RMSNORM) = range(8)
 
 c_i32, c_i64, c_f32, c_f64, c_vp, c_sz = (ctypes.c_int32, ctypes.c_int64, ctypes.c_float,
                                           ctypes.c_double, ctypes.c_void_p, ctypes.c_size_t)
@@ -58,9 +59,26 @@ class _DecodeArgs(ctypes.Structure):
                 ("max_context_len", c_i32), ("scale", c_f32), ("workspace", c_vp), ("workspace_bytes", c_sz)]
 
 
+class _RopeArgs(ctypes.Structure):
+    _fields_ = [("q", c_vp), ("k", c_vp), ("q_row_stride", c_i64), ("k_row_stride", c_i64), ("positions", c_vp),
+                ("T", c_i64), ("Hq", c_i32), ("Hkv", c_i32), ("D", c_i32), ("theta", c_f64)]
+
+
+class _CacheWriteArgs(ctypes.Structure):
+    _fields_ = [("k", c_vp), ("v", c_vp), ("kv_row_stride", c_i64), ("k_cache", c_vp), ("v_cache", c_vp),
+                ("slot_mapping", c_vp), ("T", c_i64), ("Hkv", c_i32), ("D", c_i32), ("block_size", c_i32),
+                ("num_blocks", c_i64)]
+
+
+class _AddRmsnormArgs(ctypes.Structure):
+    _fields_ = [("x", c_vp), ("residual", c_vp), ("w", c_vp), ("y", c_vp), ("M", c_i64), ("H", c_i64),
+                ("eps", c_f32)]
+
+
 class _OpUnion(ctypes.Union):
     _fields_ = [("rmsnorm", _RmsnormArgs), ("linear", _LinearArgs), ("swiglu", _SwigluArgs),
-                ("attn_prefill", _PrefillArgs), ("attn_decode", _DecodeArgs)]
+                ("attn_prefill", _PrefillArgs), ("attn_decode", _DecodeArgs), ("rope", _RopeArgs),
+                ("reshape_and_cache", _CacheWriteArgs), ("add_rmsnorm", _AddRmsnormArgs)]
 
 
 class OpDesc(ctypes.Structure):
@@ -404,4 +422,30 @@ def desc_attn_decode(q, k_cache, v_cache, block_table, context_lens, out, max_co
                                   _ptr(context_lens), _ptr(out), B, Hq, Hkv, D, bs, block_table.shape[1],
                                   nb, max_context_len, scale, _ptr(workspace),
                                   workspace.numel() * workspace.element_size())
+    return d
+
+
+def desc_rope(q, k, positions, theta) -> OpDesc:
+    d = OpDesc(op=OP_ROPE, dt=_dt(q))
+    T, Hq, D = q.shape
+    _heads_view("q", q, Hq, D)
+    _heads_view("k", k, k.shape[1], D)
+    d.u.rope = _RopeArgs(_ptr(q), _ptr(k), q.stride(0), k.stride(0), _ptr(positions), T, Hq, k.shape[1], D,
+                         float(theta))
+    return d
+
+
+def desc_reshape_and_cache(k, v, k_cache, v_cache, slot_mapping) -> OpDesc:
+    d = OpDesc(op=OP_RESHAPE_AND_CACHE, dt=_dt(k))
+    T, Hkv, D = k.shape
+    nb, bs = k_cache.shape[0], k_cache.shape[1]
+    d.u.reshape_and_cache = _CacheWriteArgs(_ptr(k), _ptr(v), k.stride(0), _ptr(k_cache), _ptr(v_cache),
+                                            _ptr(slot_mapping), T, Hkv, D, bs, nb)
+    return d
+
+
+def desc_add_rmsnorm(x, residual, w, y, eps=1e-5) -> OpDesc:
+    d = OpDesc(op=OP_ADD_RMSNORM, dt=_dt(x))
+    H = x.shape[-1]
+    d.u.add_rmsnorm = _AddRmsnormArgs(_ptr(x), _ptr(residual), _ptr(w), _ptr(y), x.numel() // H, H, eps)
     return d

@@ -127,14 +127,18 @@ Work work_decode(const std::vector<int32_t>& ctx, int64_t Hq, int64_t Hkv, int64
   return {4.0 * D * Hq * N, by, 0, (int64_t)by, s * B * Hq * D};
 }
 
+// weight: parameters read; transient: activations / cache touched; io: the
+// payload handed to the next operator.
 Work work_rope(int64_t T, int64_t Hq, int64_t Hkv, int64_t D, int s) {
-  return {3.0 * T * (Hq + Hkv) * D, 2.0 * s * T * (Hq + Hkv) * D + 4.0 * T};
+  const int64_t qk = (int64_t)s * T * (Hq + Hkv) * D;
+  return {3.0 * T * (Hq + Hkv) * D, 2.0 * qk + 4.0 * T, 0, qk, qk};
 }
 Work work_cache_write(int64_t T, int64_t Hkv, int64_t D, int s) {
-  return {0.0, 4.0 * s * T * Hkv * D + 4.0 * T};
+  const int64_t kv = 2 * (int64_t)s * T * Hkv * D;
+  return {0.0, 2.0 * kv + 4.0 * T, 0, kv, 0};
 }
 Work work_add_rmsnorm(int64_t M, int64_t H, int s) {
-  return {5.0 * M * H, (double)s * (4.0 * M * H + H)};
+  return {5.0 * M * H, (double)s * (4.0 * M * H + H), s * H, s * 4 * M * H, s * 2 * M * H};
 }
 
 opscale_status copy_ints(std::vector<int32_t>& dst, const int32_t* src, int64_t n, hipStream_t s) {
@@ -576,6 +580,40 @@ opscale_status opscale_op_profile(const opscale_op_desc* d, int32_t warmup, int3
       st = copy_ints(ctx, a.context_lens, a.B, stream);
       if (st != OPSCALE_OK) return st;
       wk = work_decode(ctx, a.Hq, a.Hkv, a.D, esize(dt), a.block_size, a.max_blocks_per_seq);
+      break;
+    }
+    case OPSCALE_OP_ROPE: {
+      const auto& a = d->u.rope;
+      st = check_rope(a.q, a.k, a.q_row_stride, a.k_row_stride, a.positions, a.T, a.Hq, a.Hkv, a.D, a.theta, dt);
+      if (st != OPSCALE_OK) return st;
+      if (a.T == 0) return fail(OPSCALE_ERR_INVALID_ARG, "op_profile: empty problem");
+      launch = [=] {
+        return opscale::launch_rope(a.q, a.k, a.q_row_stride, a.k_row_stride, a.positions, a.T, a.Hq, a.Hkv, a.D,
+                                    a.theta, bf16, stream);
+      };
+      wk = work_rope(a.T, a.Hq, a.Hkv, a.D, esize(dt));
+      break;
+    }
+    case OPSCALE_OP_RESHAPE_AND_CACHE: {
+      const auto& a = d->u.reshape_and_cache;
+      st = check_cache_write(a.k, a.v, a.kv_row_stride, a.k_cache, a.v_cache, a.slot_mapping, a.T, a.Hkv, a.D,
+                             a.block_size, a.num_blocks, dt);
+      if (st != OPSCALE_OK) return st;
+      if (a.T == 0) return fail(OPSCALE_ERR_INVALID_ARG, "op_profile: empty problem");
+      launch = [=] {
+        return opscale::launch_cache_write(a.k, a.v, a.kv_row_stride, a.k_cache, a.v_cache, a.slot_mapping, a.T,
+                                           a.Hkv, a.D, a.num_blocks * a.block_size, bf16, stream);
+      };
+      wk = work_cache_write(a.T, a.Hkv, a.D, esize(dt));
+      break;
+    }
+    case OPSCALE_OP_ADD_RMSNORM: {
+      const auto& a = d->u.add_rmsnorm;
+      st = check_add_rmsnorm(a.x, a.residual, a.w, a.y, a.M, a.H, a.eps, dt);
+      if (st != OPSCALE_OK) return st;
+      if (a.M == 0) return fail(OPSCALE_ERR_INVALID_ARG, "op_profile: empty problem");
+      launch = [=] { return opscale::launch_add_rmsnorm(a.x, a.residual, a.w, a.y, a.M, a.H, a.eps, bf16, stream); };
+      wk = work_add_rmsnorm(a.M, a.H, esize(dt));
       break;
     }
     default:

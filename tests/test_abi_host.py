@@ -170,3 +170,42 @@ def test_add_rmsnorm_validation(lib):
     assert f(A16, A16 + 32, A16 * 2, A16 * 8, 4, 4096, 1e-5, 1, None, None) == 1   # residual overlaps x
     assert f(A16, None, A16 * 2, A16 * 8, 4, 4096, 1e-5, 1, None, None) == 1
     assert f(A16, A16 * 4, A16 * 2, A16 * 4, 4, 4096, 1e-5, 1, None, None) == 1    # y is the residual
+
+
+def test_profile_descriptor_layout_matches_header(tmp_path):
+    """The ctypes mirror of opscale_op_desc / opscale_profile has the C layout
+    (sizes and the offset of every union member's fields)."""
+    import shutil
+    import subprocess
+    if shutil.which("gcc") is None:
+        pytest.skip("gcc not available")
+    import paper_2608_13499_amd as ops
+    L = ops._lib
+    members = {"rmsnorm": L._RmsnormArgs, "linear": L._LinearArgs, "swiglu": L._SwigluArgs,
+               "attn_prefill": L._PrefillArgs, "attn_decode": L._DecodeArgs, "rope": L._RopeArgs,
+               "reshape_and_cache": L._CacheWriteArgs, "add_rmsnorm": L._AddRmsnormArgs}
+    lines = ['#include <stdio.h>', '#include <stddef.h>', '#include "opscale.h"', "int main(void) {",
+             'printf("desc_size %zu\\n", sizeof(opscale_op_desc));',
+             'printf("desc_u %zu\\n", offsetof(opscale_op_desc, u));',
+             'printf("profile %zu\\n", sizeof(opscale_profile));']
+    for m, cls in members.items():
+        for f, _ in cls._fields_:
+            lines.append(f'printf("{m}.{f} %zu\\n", offsetof(opscale_op_desc, u.{m}.{f}) - '
+                         f'offsetof(opscale_op_desc, u));')
+    lines.append("return 0; }")
+    src = tmp_path / "layout.c"
+    src.write_text("\n".join(lines))
+    exe = tmp_path / "layout"
+    r = subprocess.run(["gcc", "-I", HEADER.rsplit("/", 1)[0], "-I", "/opt/rocm/include", "-D__HIP_PLATFORM_AMD__",
+                        str(src), "-o", str(exe)], capture_output=True, text=True)
+    if r.returncode != 0:
+        pytest.skip("cannot compile against the HIP headers here: " + r.stderr[-200:])
+    out = dict(line.rsplit(" ", 1) for line in subprocess.run([str(exe)], capture_output=True, text=True,
+                                                               check=True).stdout.splitlines() if line)
+    import ctypes
+    assert int(out.pop("desc_size")) == ctypes.sizeof(L.OpDesc)
+    assert int(out.pop("desc_u")) == L.OpDesc.u.offset
+    assert int(out.pop("profile")) == ctypes.sizeof(L.Profile)
+    for m, cls in members.items():
+        for f, _ in cls._fields_:
+            assert int(out[f"{m}.{f}"]) == getattr(cls, f).offset, f"{m}.{f}"
