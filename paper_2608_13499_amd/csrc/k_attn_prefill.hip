@@ -26,6 +26,8 @@
 // fp32 path: one wave per (token, head), keys 64 at a time, exact expf; it
 // serves the fp32 parity configuration.
 #include <algorithm>
+#include <cstdlib>
+#include <cstring>
 
 #include "common.h"
 #include "launch.h"
@@ -69,11 +71,23 @@ __device__ __forceinline__ u32x2 lds_read_tr16(const OPS_LDS char* p) {
   return __builtin_bit_cast(u32x2, v);
 }
 
-template <int D>
+// Prompts the work-list schedule can hold in LDS (more use the grid schedule).
+constexpr int kMaxListB = 1024;
+
+// Two schedules over the same tiles (a tile: one prompt, one KV head, one
+// head block, one query-tile level), each tile computed the same way, so the
+// output does not depend on the schedule:
+//  * grid (LIST = false): blockIdx = (prompt x KV head x head block, level),
+//    highest level first; workgroups whose prompt has no tile at their level
+//    return at once.
+//  * work list (LIST = true): workgroup i takes item i of the level-major list
+//    of the tiles that exist (highest level first, then prompt, KV head and
+//    head block), so no workgroup is launched for a missing tile.
+template <int D, bool LIST>
 __global__ __launch_bounds__(256, 2) void attn_prefill_bf16_kernel(
     const __bf16* __restrict__ q, const __bf16* __restrict__ k, const __bf16* __restrict__ v,
     int64_t q_stride, int64_t kv_stride, __bf16* __restrict__ o, const int32_t* __restrict__ cu,
-    int Hq, int Hkv, int hpb, float scale_log2, int causal) {
+    int B, int Hq, int Hkv, int hpb, float scale_log2, int causal) {
   using S = PrefillSmem<D>;
   constexpr int CPR = D / 8;          // 16-byte chunks per row
   constexpr int DSTEPS = D / 16;      // MFMA k-steps over the head dim
@@ -90,16 +104,8 @@ __global__ __launch_bounds__(256, 2) void attn_prefill_bf16_kernel(
   const int nhb = G / hpb;
   const int qsub = 4 / hpb;
   const int BQ = 32 * qsub;
-  const int bx = blockIdx.x;
-  const int b = bx / (Hkv * nhb);
-  const int g = (bx / nhb) % Hkv;
-  const int hb = bx % nhb;
-  const int seq0 = cu[b];
-  const int L = cu[b + 1] - seq0;
-  const int ntiles = (L + BQ - 1) / BQ;
-
+  const int bq_shift = 5 + __builtin_ctz(qsub);
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
-  const int h = g * G + hb * hpb + wave % hpb;
   const int qs = wave / hpb;
   const int fr = lane & 31, fh = lane >> 5;
   // lane roles in the transposed V reads: 16-lane group tg, member tc
@@ -107,7 +113,9 @@ __global__ __launch_bounds__(256, 2) void attn_prefill_bf16_kernel(
   const int tr_key = 4 * (tg >> 1) + (tc >> 2);               // + 16 s (+ 8 for the upper half)
   const int tr_col = 16 * (tg & 1) + 4 * (tc & 3);            // + 32 dt
 
-  for (int t = gridDim.y - 1 - blockIdx.y; t < ntiles; t += gridDim.y) {
+  // One query tile: prompt b, KV head g, head block hb, level t.
+  auto do_tile = [&](const int b, const int g, const int hb, const int t, const int seq0, const int L) {
+    const int h = g * G + hb * hpb + wave % hpb;
     const int q_lo = t * BQ + qs * 32;          // first query of this wave
     const int q_pos = q_lo + fr;                 // this lane's query
     const int blk_q_hi = min(L, (t + 1) * BQ);   // one past the block's last query
@@ -249,6 +257,80 @@ __global__ __launch_bounds__(256, 2) void attn_prefill_bf16_kernel(
         }
     }
     __syncthreads();  // the next tile reuses the LDS stages
+  };
+
+  if constexpr (!LIST) {
+    const int bx = blockIdx.x;
+    const int b = bx / (Hkv * nhb);
+    const int g = (bx / nhb) % Hkv;
+    const int hb = bx % nhb;
+    const int seq0 = cu[b];
+    const int L = cu[b + 1] - seq0;
+    const int ntiles = (L + BQ - 1) / BQ;
+    for (int t = gridDim.y - 1 - blockIdx.y; t < ntiles; t += gridDim.y) do_tile(b, g, hb, t, seq0, L);
+  } else {
+    // n_s[b]: query tiles of prompt b.  The list holds, for every level t from
+    // the highest down, the prompts with a tile at level t (batch order), each
+    // with its HG (KV head, head block) pairs.  The tile groups at levels >= t
+    // number F(t) = sum_b max(0, n_b - t), so item group q sits at the level
+    // t with F(t + 1) <= q < F(t), found by bisection.
+    // The table (cu_s, n_s) sits in the K/V stage buffers, so it is rebuilt
+    // for every item: the tile's loads overwrite it.
+    static_assert((2 * kMaxListB + 1) * 4 <= S::kTotal, "work table does not fit the stage buffers");
+    OPS_LDS int32_t* cu_s = (OPS_LDS int32_t*)smem;
+    OPS_LDS int32_t* n_s = cu_s + kMaxListB + 1;
+    const int HG = Hkv * nhb;
+    for (int64_t i = blockIdx.x;; i += gridDim.x) {
+      for (int x = threadIdx.x; x <= B; x += 256) {
+        const int c = cu[x];
+        cu_s[x] = c;
+        if (x < B) n_s[x] = (cu[x + 1] - c + BQ - 1) >> bq_shift;
+      }
+      __syncthreads();
+      // (values below are equal in every lane and every wave; the first 64
+      // tile counts stay in a register)
+      const int n0 = lane < B ? n_s[lane] : 0;
+      auto F = [&](int t) {
+        int acc_n = max(0, n0 - t);
+        for (int b0 = 64; b0 < B; b0 += 64)
+          if (b0 + lane < B) acc_n += max(0, n_s[b0 + lane] - t);
+        return wave_sum_i(acc_n);
+      };
+      int top = n0;
+      for (int b0 = 64; b0 < B; b0 += 64)
+        if (b0 + lane < B) top = max(top, n_s[b0 + lane]);
+      top = wave_max_i(top);
+      if (i >= (int64_t)F(0) * HG) break;
+      const int qg = (int)(i / HG), r = (int)(i % HG);
+      int lo = 0, hi = top;  // F(lo) > qg >= F(hi)
+      while (hi - lo > 1) {
+        const int mid = (lo + hi) >> 1;
+        if (F(mid) > qg) lo = mid;
+        else hi = mid;
+      }
+      const int t = lo;
+      // the j-th prompt (batch order) with a tile at level t
+      int j = qg - F(t + 1);
+      int b = 0;
+      for (int b0 = 0; b0 < B; b0 += 64) {
+        const bool has = b0 == 0 ? n0 > t : (b0 + lane < B && n_s[b0 + lane] > t);
+        const uint64_t m = __builtin_amdgcn_ballot_w64(has);
+        const int pc = __builtin_popcountll(m);
+        if (j < pc) {
+          const int before = __builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0));
+          b = b0 + __builtin_ctzll(__builtin_amdgcn_ballot_w64(has && before == j));
+          break;
+        }
+        j -= pc;
+      }
+      // the values are uniform; saying so keeps the tile's buffer descriptors
+      // in scalar registers
+      const int ub = __builtin_amdgcn_readfirstlane(b);
+      const int s0 = __builtin_amdgcn_readfirstlane(cu_s[ub]);
+      const int s1 = __builtin_amdgcn_readfirstlane(cu_s[ub + 1]);
+      __syncthreads();  // every wave has read the table
+      do_tile(ub, r / nhb, r % nhb, t, s0, s1 - s0);
+    }
   }
 }
 
@@ -337,19 +419,35 @@ hipError_t launch_attn_prefill(const void* q, const void* k, const void* v, int6
   const int G = Hq / Hkv;
   const int hpb = (G % 4 == 0) ? 4 : (G % 2 == 0) ? 2 : 1;
   const int BQ = 32 * (4 / hpb);
-  const unsigned gx = (unsigned)(B * Hkv * (G / hpb));
-  const unsigned gy = (unsigned)std::min<int64_t>(65535, (max_seqlen + BQ - 1) / BQ);
   const float sl2 = scale * kLog2e;
-  if (D == 128)
-    hipLaunchKernelGGL((attn_prefill_bf16_kernel<128>), dim3(gx, gy), dim3(256), 0, s,
-                       static_cast<const __bf16*>(q), static_cast<const __bf16*>(k),
-                       static_cast<const __bf16*>(v), q_stride, kv_stride, static_cast<__bf16*>(o),
-                       cu, Hq, Hkv, hpb, sl2, (int)causal);
-  else
-    hipLaunchKernelGGL((attn_prefill_bf16_kernel<64>), dim3(gx, gy), dim3(256), 0, s,
-                       static_cast<const __bf16*>(q), static_cast<const __bf16*>(k),
-                       static_cast<const __bf16*>(v), q_stride, kv_stride, static_cast<__bf16*>(o),
-                       cu, Hq, Hkv, hpb, sl2, (int)causal);
+  // The grid launches B x ceil(max_seqlen / BQ) x HG workgroups, of which
+  // only sum_b ceil(L_b / BQ) x HG have a tile; the work list launches about
+  // that many (an upper bound: total_tokens / BQ + B tiles per HG) but pays a
+  // small fixed cost per workgroup to find its item.  Prompts that fill less
+  // than three quarters of B x max_seqlen favour the work list.
+  const int64_t max_items = (total_tokens / BQ + B) * (int64_t)Hkv * (G / hpb);
+  bool list = B <= kMaxListB && (double)total_tokens < 0.75 * (double)B * (double)max_seqlen;
+  // OPSCALE_PREFILL_SCHEDULE=grid|list overrides the choice (tuning, tests);
+  // batches of more than kMaxListB prompts always use the grid.
+  if (const char* force = std::getenv("OPSCALE_PREFILL_SCHEDULE")) {
+    if (std::strcmp(force, "grid") == 0) list = false;
+    else if (std::strcmp(force, "list") == 0) list = B <= kMaxListB;
+  }
+  const unsigned gx = list ? (unsigned)std::min<int64_t>(0x7fffffff, max_items) : (unsigned)(B * Hkv * (G / hpb));
+  const unsigned gy = list ? 1u : (unsigned)std::min<int64_t>(65535, (max_seqlen + BQ - 1) / BQ);
+#define OPS_PF(DD, P)                                                                                   \
+  hipLaunchKernelGGL((attn_prefill_bf16_kernel<DD, P>), dim3(gx, gy), dim3(256), 0, s,                  \
+                     static_cast<const __bf16*>(q), static_cast<const __bf16*>(k),                      \
+                     static_cast<const __bf16*>(v), q_stride, kv_stride, static_cast<__bf16*>(o), cu, B, \
+                     Hq, Hkv, hpb, sl2, (int)causal)
+  if (D == 128) {
+    if (list) OPS_PF(128, true);
+    else OPS_PF(128, false);
+  } else {
+    if (list) OPS_PF(64, true);
+    else OPS_PF(64, false);
+  }
+#undef OPS_PF
   return hipGetLastError();
 }
 

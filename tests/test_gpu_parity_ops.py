@@ -155,6 +155,44 @@ def test_attn_prefill(ops, dtype, lens, Hq, Hkv, D, causal, packed):
     assert_close(got, ref, dtype, "attn_prefill")
 
 
+@pytest.mark.parametrize("lens,Hq,Hkv,D", [
+    ([1, 17, 64, 65, 130, 0, 300, 33], 8, 2, 128),   # ragged, G = 4 (32-query tiles)
+    ([96, 96, 96], 4, 2, 64),                        # uniform, G = 2 (64-query tiles)
+    ([900, 5, 1, 260], 3, 3, 128),                   # G = 1 (128-query tiles)
+    ([1, 2, 3, 17] * 20 + [700], 8, 1, 64),          # 81 prompts: more than one wave of 64
+])
+def test_attn_prefill_schedules(ops, monkeypatch, lens, Hq, Hkv, D):
+    """Both schedules (grid; level-major work list) against the oracle, and
+    bitwise equal to each other (each tile is computed the same way)."""
+    outs = {}
+    for sched in ("grid", "list"):
+        monkeypatch.setenv("OPSCALE_PREFILL_SCHEDULE", sched)
+        say(f"attn_prefill bf16 schedule={sched} lens={lens} Hq={Hq} Hkv={Hkv} D={D}")
+        got, ref = _prefill_case(ops, "bf16", lens, Hq, Hkv, D, True, True)
+        assert_close(got, ref, "bf16", f"attn_prefill ({sched})")
+        outs[sched] = got
+    assert np.array_equal(outs["grid"], outs["list"])
+
+
+def test_attn_prefill_many_prompts(ops, monkeypatch):
+    """More prompts than the work list holds in LDS: the launcher takes the grid
+    even when the list is asked for."""
+    monkeypatch.setenv("OPSCALE_PREFILL_SCHEDULE", "list")
+    say("attn_prefill bf16 1101 prompts")
+    lens = ([1, 2, 3, 17] * 276)[:1101]
+    got, ref = _prefill_case(ops, "bf16", lens, 8, 2, 128, True, True)
+    assert_close(got, ref, "bf16", "attn_prefill 1101 prompts")
+
+
+def test_attn_prefill_1024_prompts_list(ops, monkeypatch):
+    """The largest batch the work list takes (1024 prompts, 16 waves of 64)."""
+    monkeypatch.setenv("OPSCALE_PREFILL_SCHEDULE", "list")
+    say("attn_prefill bf16 1024 prompts (work list)")
+    lens = ([1, 40, 3, 97, 0, 64] * 171)[:1024]
+    got, ref = _prefill_case(ops, "bf16", lens, 8, 2, 64, True, True)
+    assert_close(got, ref, "bf16", "attn_prefill 1024 prompts")
+
+
 def test_attn_prefill_single_key_returns_v(ops):
     """Prompts of length 1: softmax over one key is exactly 1, output == v."""
     import torch
