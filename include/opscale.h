@@ -293,6 +293,99 @@ opscale_status opscale_op_profile(const opscale_op_desc* desc, int32_t warmup, i
                                   void* flush_buf, size_t flush_bytes, hipStream_t stream,
                                   opscale_profile* out);
 
+/* ---------------------------------------------------------------------------
+ * Spatial sharing: operators on disjoint sets of compute units.
+ *
+ * The paper runs colocated operators on separate streams that each own a
+ * share p of the GPU's SMs (Section 2.1's SM-allocation sensitivity; the
+ * interference model of Section 4.4, Eq. 5, validated in Section 5.7,
+ * Table 2).  On MI355X the
+ * equivalent is a stream whose CU mask selects the compute units its kernels
+ * may use.  The GPU has 256 CUs in 8 XCDs, and each XCD has its own L2 and
+ * receives every 8th workgroup, so a share is laid out evenly over the XCDs.
+ * ------------------------------------------------------------------------- */
+
+/*
+ * The current device's CU count, XCD count, and how the bits of a stream's
+ * CU mask map to XCDs: interleaved = 1 when mask bit n is CU n / num_xcds of
+ * XCD n % num_xcds, 0 when it is CU n % (num_cus / num_xcds) of XCD
+ * n / (num_cus / num_xcds).  The mapping is measured once per device, at the
+ * first call, by running opscale_cu_probe on a stream masked to the first
+ * num_cus / num_xcds bits (blocking).  OPSCALE_ERR_UNSUPPORTED if the probe
+ * matches neither mapping.
+ */
+opscale_status opscale_cu_layout(int32_t* num_cus, int32_t* num_xcds, int32_t* interleaved);
+
+/*
+ * Host only (no device needed).  Mask of `count` compute units spread evenly
+ * over the XCDs: position i of the balanced order is slot i / num_xcds of XCD
+ * i % num_xcds, and the mask takes positions [first, first + count).  The
+ * ranges [0, k) and [k, num_cus) thus split the GPU into two disjoint shares
+ * whose per-XCD CU counts differ by at most one.  mask: host, mask_words
+ * uint32 words (bit n of word n / 32 is mask bit n), at least num_cus / 32;
+ * words past the CU count are zeroed.  num_cus must be a multiple of
+ * num_xcds; 1 <= count and first + count <= num_cus.
+ */
+opscale_status opscale_cu_mask_build(int32_t num_cus, int32_t num_xcds, int32_t interleaved, int32_t first,
+                                     int32_t count, uint32_t* mask, int32_t mask_words);
+
+/*
+ * A stream restricted to the CUs set in `mask` (host, mask_words uint32
+ * words, at least one bit set), at the default priority.  Kernels on it use
+ * only those CUs; the library's kernels need no particular CU count.
+ * Destroy it with opscale_cu_stream_destroy.
+ */
+opscale_status opscale_cu_stream_create(const uint32_t* mask, int32_t mask_words, hipStream_t* out);
+opscale_status opscale_cu_stream_destroy(hipStream_t stream);
+/* The CU mask the runtime holds for `stream` (host, mask_words words). */
+opscale_status opscale_cu_stream_mask(hipStream_t stream, uint32_t* mask, int32_t mask_words);
+
+/*
+ * Placement probe: launches n_workgroups workgroups of 64 lanes on `stream`;
+ * workgroup w writes out[2w] = its XCD (XCC_ID register) and out[2w + 1] =
+ * the HW_ID register (CU, shader array and shader engine in bits 8..15), then
+ * sleeps `spins` x 127 x 64 cycles so that the workgroups spread over every
+ * CU the stream may use.  out: device, 2 * n_workgroups uint32.
+ * 1 <= n_workgroups <= 65536, 0 <= spins <= 1000.  Asynchronous.
+ */
+opscale_status opscale_cu_probe(hipStream_t stream, uint32_t* out, int32_t n_workgroups, int32_t spins);
+
+/* Result of opscale_corun_profile (times in microseconds). */
+typedef struct {
+  int32_t n_a, n_b;             /* launches of each operator in the co-run   */
+  int32_t overlap_a, overlap_b; /* launches wholly inside the other's span   */
+  float a_iso_us, b_iso_us;     /* T_v(b, p): median launch, each one alone  */
+  float a_co_us, b_co_us;       /* T~_v(b, p): median of the overlapped ones */
+  double interference_a;        /* I (Eq. 5) = a_co_us / a_iso_us            */
+  double interference_b;
+} opscale_corun;
+
+/* Optional raw timestamps of opscale_corun_profile (host arrays). */
+typedef struct {
+  float *a_start, *a_end;  /* [max_launches]: launch i of a, from a common reference */
+  float *b_start, *b_end;  /* [max_launches] */
+  float *a_iso, *b_iso;    /* [iso_iters]: the isolated launch times */
+} opscale_corun_trace;
+
+/*
+ * The interference factor of Eq. 5 for two operators sharing the GPU.  Each
+ * runs on its own stream (sa, sb: normally CU-masked streams with disjoint
+ * masks, so p is the share of each).  Both are first run `warmup` times, then
+ * `iso_iters` times back to back alone on their stream, giving T_v(b, p).
+ * Then both loops run at once for a window W = max(window_ms, 4 x the slower
+ * of T_a, T_b): operator a launches ceil(W / T_a) times and b ceil(W / T_b)
+ * times (each at least 4, at most max_launches), enqueued in the order of
+ * their planned start times,
+ * with device events between launches.  Launches that lie wholly inside the
+ * other operator's active span give T~_v(b, p).  overlap_a or overlap_b is 0
+ * (and the matching time and factor 0) when no launch qualifies.  trace may
+ * be NULL.  Blocking.  1 <= iso_iters <= 4096, 4 <= max_launches <= 8192,
+ * window_ms in (0, 10000].
+ */
+opscale_status opscale_corun_profile(const opscale_op_desc* a, hipStream_t sa, const opscale_op_desc* b,
+                                     hipStream_t sb, int32_t warmup, int32_t iso_iters, float window_ms,
+                                     int32_t max_launches, const opscale_corun_trace* trace, opscale_corun* out);
+
 #ifdef __cplusplus
 }
 #endif

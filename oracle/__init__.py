@@ -11,7 +11,8 @@ attention, decode attention over a paged KV cache) and of the operators around
 them in a full layer (rotary embedding, the paged KV-cache write, the residual
 add before each norm), evaluated in fp64 with no
 tiling, no online softmax and no split of the key range.  See `ops` for the
-per-function citations and `cost` for the algorithmic flop/byte closed forms.
+per-function citations, `cost` for the algorithmic flop/byte closed forms and
+`spatial` for CU shares and the interference factor of Eq. 5.
 
 Parity status: every function here is pinned by brute force, closed forms or
 invariants in the CPU tests (tests/test_oracle_pins.py); none is "parity
@@ -23,3 +24,4 @@ from .ops import (  # noqa: F401
     rope, reshape_and_cache, add_rmsnorm, decoder_layer_forward, decoder_layer_decode,
 )
 from . import cost  # noqa: F401
+from . import spatial  # noqa: F401

@@ -3,7 +3,8 @@ ragged causal GQA prefill attention and paged decode attention, plus RoPE, the
 paged KV-cache write and residual-add RMSNorm, as hand-written HIP kernels
 behind the C ABI in include/opscale.h.  This package holds the HIP sources
 (csrc/), their build script, the ctypes binding, a layer chained from the
-entry points (layer) and the operator profiler (profiler)."""
+entry points (layer), the operator profiler (profiler) and spatial sharing
+over CU-masked streams (spatial)."""
 from ._lib import (  # noqa: F401
     OpscaleError, Timing, Profile, OpDesc, load, LIB_PATH, EXPORTS,
     opscale_version, opscale_rmsnorm, opscale_linear, opscale_swiglu, opscale_attn_prefill,
@@ -11,6 +12,8 @@ from ._lib import (  # noqa: F401
     opscale_attn_decode_workspace_size, opscale_attn_decode, opscale_op_profile,
     desc_rmsnorm, desc_linear, desc_swiglu, desc_attn_prefill, desc_attn_decode,
     desc_rope, desc_reshape_and_cache, desc_add_rmsnorm,
+    Corun, opscale_cu_layout, opscale_cu_mask_build, opscale_cu_stream_create, opscale_cu_stream_destroy,
+    opscale_cu_stream_mask, opscale_cu_probe, opscale_corun_profile,
     OPSCALE_OK, OPSCALE_ERR_INVALID_ARG, OPSCALE_ERR_UNSUPPORTED, OPSCALE_ERR_WORKSPACE,
     OPSCALE_ERR_HIP, OPSCALE_F32, OPSCALE_BF16,
 )

@@ -96,6 +96,23 @@ class Profile(ctypes.Structure):
         return {name: getattr(self, name) for name, _ in self._fields_}
 
 
+class Corun(ctypes.Structure):
+    _fields_ = [("n_a", c_i32), ("n_b", c_i32), ("overlap_a", c_i32), ("overlap_b", c_i32),
+                ("a_iso_us", c_f32), ("b_iso_us", c_f32), ("a_co_us", c_f32), ("b_co_us", c_f32),
+                ("interference_a", c_f64), ("interference_b", c_f64)]
+
+    def as_dict(self):
+        return {name: getattr(self, name) for name, _ in self._fields_}
+
+
+_PF = ctypes.POINTER(c_f32)
+
+
+class _CorunTrace(ctypes.Structure):
+    _fields_ = [("a_start", _PF), ("a_end", _PF), ("b_start", _PF), ("b_end", _PF), ("a_iso", _PF),
+                ("b_iso", _PF)]
+
+
 EXPORTS = {
     "opscale_version": (ctypes.c_char_p, []),
     "opscale_status_string": (ctypes.c_char_p, [c_i32]),
@@ -117,6 +134,14 @@ EXPORTS = {
                                           c_i32, c_vp, ctypes.POINTER(Timing)]),
     "opscale_add_rmsnorm": (c_i32, [c_vp, c_vp, c_vp, c_vp, c_i64, c_i64, c_f32, c_i32, c_vp,
                                     ctypes.POINTER(Timing)]),
+    "opscale_cu_layout": (c_i32, [ctypes.POINTER(c_i32)] * 3),
+    "opscale_cu_mask_build": (c_i32, [c_i32, c_i32, c_i32, c_i32, c_i32, ctypes.POINTER(ctypes.c_uint32), c_i32]),
+    "opscale_cu_stream_create": (c_i32, [ctypes.POINTER(ctypes.c_uint32), c_i32, ctypes.POINTER(c_vp)]),
+    "opscale_cu_stream_destroy": (c_i32, [c_vp]),
+    "opscale_cu_stream_mask": (c_i32, [c_vp, ctypes.POINTER(ctypes.c_uint32), c_i32]),
+    "opscale_cu_probe": (c_i32, [c_vp, c_vp, c_i32, c_i32]),
+    "opscale_corun_profile": (c_i32, [ctypes.POINTER(OpDesc), c_vp, ctypes.POINTER(OpDesc), c_vp, c_i32, c_i32,
+                                      c_f32, c_i32, ctypes.POINTER(_CorunTrace), ctypes.POINTER(Corun)]),
 }
 
 _lib = None
@@ -379,6 +404,76 @@ def opscale_op_profile(desc: OpDesc, warmup: int = 5, iters: int = 20, flush=Non
     _check(lib.opscale_op_profile(ctypes.byref(desc), warmup, iters, _ptr(flush), nbytes,
                                   _stream(stream), ctypes.byref(p)))
     return p
+
+
+# ---------------------------------------------------------- spatial sharing --
+def opscale_cu_layout():
+    """(num_cus, num_xcds, interleaved) of the current device."""
+    lib = load()
+    n, x, i = c_i32(), c_i32(), c_i32()
+    _check(lib.opscale_cu_layout(ctypes.byref(n), ctypes.byref(x), ctypes.byref(i)))
+    return n.value, x.value, i.value
+
+
+def opscale_cu_mask_build(num_cus: int, num_xcds: int, interleaved: int, first: int, count: int):
+    """The CU mask (list of uint32 words) of balanced positions [first, first + count)."""
+    lib = load()
+    words = (num_cus + 31) // 32
+    buf = (ctypes.c_uint32 * words)()
+    _check(lib.opscale_cu_mask_build(num_cus, num_xcds, interleaved, first, count, buf, words))
+    return list(buf)
+
+
+def opscale_cu_stream_create(mask) -> int:
+    """A CU-masked stream (an integer hipStream_t handle) for the uint32 words `mask`."""
+    lib = load()
+    buf = (ctypes.c_uint32 * len(mask))(*mask)
+    h = c_vp()
+    _check(lib.opscale_cu_stream_create(buf, len(mask), ctypes.byref(h)))
+    return h.value
+
+
+def opscale_cu_stream_destroy(stream: int):
+    _check(load().opscale_cu_stream_destroy(stream))
+
+
+def opscale_cu_stream_mask(stream: int, words: int):
+    buf = (ctypes.c_uint32 * words)()
+    _check(load().opscale_cu_stream_mask(stream, buf, words))
+    return list(buf)
+
+
+def opscale_cu_probe(out, spins: int = 4, stream=None):
+    """Launch the placement probe: out is an int32 [n, 2] GPU tensor (XCD, HW_ID per workgroup)."""
+    _dev(out)
+    if out.dim() != 2 or out.shape[1] != 2 or not out.is_contiguous() or out.element_size() != 4:
+        raise OpscaleError(OPSCALE_ERR_INVALID_ARG, "out must be a contiguous 4-byte [n, 2] tensor")
+    _check(load().opscale_cu_probe(_stream(stream), _ptr(out), out.shape[0], spins))
+    return out
+
+
+def opscale_corun_profile(desc_a: OpDesc, stream_a, desc_b: OpDesc, stream_b, warmup: int = 3,
+                          iso_iters: int = 20, window_ms: float = 20.0, max_launches: int = 2048,
+                          trace: bool = False):
+    """Eq. 5 interference factors of two operators run at once on two streams.
+    Returns a Corun (and, with trace=True, a dict of the raw launch times)."""
+    lib = load()
+    r = Corun()
+    tr = None
+    arrays = None
+    if trace:
+        arrays = {k: (c_f32 * n)() for k, n in (("a_start", max_launches), ("a_end", max_launches),
+                                                ("b_start", max_launches), ("b_end", max_launches),
+                                                ("a_iso", iso_iters), ("b_iso", iso_iters))}
+        tr = _CorunTrace(**{k: ctypes.cast(v, _PF) for k, v in arrays.items()})
+    _check(lib.opscale_corun_profile(ctypes.byref(desc_a), _stream(stream_a), ctypes.byref(desc_b),
+                                     _stream(stream_b), warmup, iso_iters, window_ms, max_launches,
+                                     ctypes.byref(tr) if tr is not None else None, ctypes.byref(r)))
+    if not trace:
+        return r
+    n = {"a_start": r.n_a, "a_end": r.n_a, "b_start": r.n_b, "b_end": r.n_b, "a_iso": iso_iters,
+         "b_iso": iso_iters}
+    return r, {k: list(v)[:n[k]] for k, v in arrays.items()}
 
 
 # descriptor builders (keep the tensors alive while the descriptor is used)

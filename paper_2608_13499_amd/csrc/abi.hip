@@ -10,8 +10,9 @@
 
 #include "launch.h"
 #include "opscale.h"
+#include "status.h"
 
-namespace {
+namespace opscale {
 
 thread_local std::string g_last_error;
 
@@ -28,6 +29,13 @@ opscale_status fail(opscale_status st, const char* fmt, ...) {
 opscale_status hip_fail(hipError_t e, const char* what) {
   return fail(OPSCALE_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
 }
+
+}  // namespace opscale
+
+namespace {
+
+using opscale::fail;
+using opscale::hip_fail;
 
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 
@@ -318,6 +326,54 @@ opscale_status check_add_rmsnorm(const void* x, void* res, const void* w, void* 
   return OPSCALE_OK;
 }
 
+// Median with linear interpolation between the two middle values (the
+// percentile rule of opscale_op_profile); 0 for an empty list.
+float median_of(std::vector<float> v) {
+  if (v.empty()) return 0.f;
+  std::sort(v.begin(), v.end());
+  const double pos = 0.5 * (double)(v.size() - 1);
+  const size_t lo = (size_t)std::floor(pos), hi = (size_t)std::ceil(pos);
+  return (float)(v[lo] + (v[hi] - v[lo]) * (pos - (double)lo));
+}
+
+// Owns a set of timing events.
+struct EventPool {
+  std::vector<hipEvent_t> ev;
+  hipError_t make(size_t n) {
+    ev.assign(n, nullptr);
+    for (auto& e : ev) {
+      const hipError_t r = hipEventCreate(&e);
+      if (r != hipSuccess) return r;
+    }
+    return hipSuccess;
+  }
+  ~EventPool() {
+    for (auto e : ev)
+      if (e) (void)hipEventDestroy(e);
+  }
+};
+
+// Per-launch times (us) of `n` back-to-back launches on s, each between two events.
+opscale_status time_loop(const std::function<hipError_t()>& launch, hipStream_t s, int n, std::vector<float>* us) {
+  EventPool pool;
+  hipError_t e = pool.make((size_t)n + 1);
+  if (e != hipSuccess) return hip_fail(e, "hipEventCreate");
+  if ((e = hipEventRecord(pool.ev[0], s)) != hipSuccess) return hip_fail(e, "hipEventRecord");
+  for (int i = 0; i < n; ++i) {
+    if ((e = launch()) != hipSuccess) return hip_fail(e, "corun launch");
+    if ((e = hipEventRecord(pool.ev[(size_t)i + 1], s)) != hipSuccess) return hip_fail(e, "hipEventRecord");
+  }
+  if ((e = hipEventSynchronize(pool.ev[(size_t)n])) != hipSuccess) return hip_fail(e, "hipEventSynchronize");
+  us->resize((size_t)n);
+  for (int i = 0; i < n; ++i) {
+    float ms = 0.f;
+    if ((e = hipEventElapsedTime(&ms, pool.ev[(size_t)i], pool.ev[(size_t)i + 1])) != hipSuccess)
+      return hip_fail(e, "hipEventElapsedTime");
+    (*us)[(size_t)i] = ms * 1000.f;
+  }
+  return OPSCALE_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -335,7 +391,7 @@ const char* opscale_status_string(opscale_status s) {
   return "unknown status";
 }
 
-const char* opscale_last_error(void) { return g_last_error.c_str(); }
+const char* opscale_last_error(void) { return opscale::g_last_error.c_str(); }
 
 opscale_status opscale_rmsnorm(const void* x, const void* w, void* y, int64_t M, int64_t H, float eps,
                                opscale_dtype dt, hipStream_t stream, opscale_timing* timing) {
@@ -506,24 +562,25 @@ opscale_status opscale_add_rmsnorm(const void* x, void* residual, const void* w,
   return st;
 }
 
-opscale_status opscale_op_profile(const opscale_op_desc* d, int32_t warmup, int32_t iters,
-                                  void* flush_buf, size_t flush_bytes, hipStream_t stream,
-                                  opscale_profile* out) {
-  if (!d || !out) return fail(OPSCALE_ERR_INVALID_ARG, "op_profile: null desc or out");
-  if (iters < 1 || warmup < 0) return fail(OPSCALE_ERR_INVALID_ARG, "op_profile: iters must be >= 1, warmup >= 0");
-  if (flush_buf && !aligned16(flush_buf)) return fail(OPSCALE_ERR_INVALID_ARG, "op_profile: flush_buf must be 16-byte aligned");
+}  // extern "C"
+
+namespace {
+
+// Validates one operator descriptor and binds its launch on `stream` (no
+// re-validation per launch); `wk` receives the algorithmic work.
+opscale_status prepare_op(const opscale_op_desc* d, hipStream_t stream, const char* who,
+                          std::function<hipError_t()>* launch_out, Work* wk_out) {
   const opscale_dtype dt = d->dt;
-  // validate once, then launch without re-validation inside the loop
   opscale_status st = OPSCALE_OK;
-  std::function<hipError_t()> launch;
-  Work wk{};
+  std::function<hipError_t()>& launch = *launch_out;
+  Work& wk = *wk_out;
   const bool bf16 = dt == OPSCALE_BF16;
   switch (d->op) {
     case OPSCALE_OP_RMSNORM: {
       const auto& a = d->u.rmsnorm;
       st = check_rmsnorm(a.x, a.w, a.y, a.M, a.H, a.eps, dt);
       if (st != OPSCALE_OK) return st;
-      if (a.M == 0) return fail(OPSCALE_ERR_INVALID_ARG, "op_profile: empty problem");
+      if (a.M == 0) return fail(OPSCALE_ERR_INVALID_ARG, "%s: empty problem", who);
       launch = [=] { return opscale::launch_rmsnorm(a.x, a.w, a.y, a.M, a.H, a.eps, bf16, stream); };
       wk = work_rmsnorm(a.M, a.H, esize(dt));
       break;
@@ -532,7 +589,7 @@ opscale_status opscale_op_profile(const opscale_op_desc* d, int32_t warmup, int3
       const auto& a = d->u.linear;
       st = check_linear(a.x, a.W, a.bias, a.y, a.M, a.N, a.K, dt);
       if (st != OPSCALE_OK) return st;
-      if (a.M == 0) return fail(OPSCALE_ERR_INVALID_ARG, "op_profile: empty problem");
+      if (a.M == 0) return fail(OPSCALE_ERR_INVALID_ARG, "%s: empty problem", who);
       launch = [=] { return opscale::launch_linear(a.x, a.W, a.bias, a.y, a.M, a.N, a.K, bf16, stream); };
       wk = work_linear(a.M, a.N, a.K, esize(dt), a.bias != nullptr);
       break;
@@ -541,7 +598,7 @@ opscale_status opscale_op_profile(const opscale_op_desc* d, int32_t warmup, int3
       const auto& a = d->u.swiglu;
       st = check_swiglu(a.gate_up, a.out, a.M, a.F, dt);
       if (st != OPSCALE_OK) return st;
-      if (a.M == 0) return fail(OPSCALE_ERR_INVALID_ARG, "op_profile: empty problem");
+      if (a.M == 0) return fail(OPSCALE_ERR_INVALID_ARG, "%s: empty problem", who);
       launch = [=] { return opscale::launch_swiglu(a.gate_up, a.out, a.M, a.F, bf16, stream); };
       wk = work_swiglu(a.M, a.F, esize(dt));
       break;
@@ -551,7 +608,7 @@ opscale_status opscale_op_profile(const opscale_op_desc* d, int32_t warmup, int3
       st = check_prefill(a.q, a.k, a.v, a.q_row_stride, a.kv_row_stride, a.o, a.cu_seqlens, a.B,
                          a.total_tokens, a.max_seqlen, a.Hq, a.Hkv, a.D, a.scale, dt);
       if (st != OPSCALE_OK) return st;
-      if (a.B == 0 || a.total_tokens == 0) return fail(OPSCALE_ERR_INVALID_ARG, "op_profile: empty problem");
+      if (a.B == 0 || a.total_tokens == 0) return fail(OPSCALE_ERR_INVALID_ARG, "%s: empty problem", who);
       launch = [=] {
         return opscale::launch_attn_prefill(a.q, a.k, a.v, a.q_row_stride, a.kv_row_stride, a.o,
                                             a.cu_seqlens, a.B, a.total_tokens, a.max_seqlen, a.Hq,
@@ -569,7 +626,7 @@ opscale_status opscale_op_profile(const opscale_op_desc* d, int32_t warmup, int3
                         a.Hkv, a.D, a.block_size, a.max_blocks_per_seq, a.num_blocks,
                         a.max_context_len, a.scale, dt, a.workspace, a.workspace_bytes);
       if (st != OPSCALE_OK) return st;
-      if (a.B == 0) return fail(OPSCALE_ERR_INVALID_ARG, "op_profile: empty problem");
+      if (a.B == 0) return fail(OPSCALE_ERR_INVALID_ARG, "%s: empty problem", who);
       launch = [=] {
         return opscale::launch_attn_decode(a.q, a.q_row_stride, a.k_cache, a.v_cache, a.block_table, a.context_lens,
                                            a.o, a.B, a.Hq, a.Hkv, a.D, a.block_size,
@@ -586,7 +643,7 @@ opscale_status opscale_op_profile(const opscale_op_desc* d, int32_t warmup, int3
       const auto& a = d->u.rope;
       st = check_rope(a.q, a.k, a.q_row_stride, a.k_row_stride, a.positions, a.T, a.Hq, a.Hkv, a.D, a.theta, dt);
       if (st != OPSCALE_OK) return st;
-      if (a.T == 0) return fail(OPSCALE_ERR_INVALID_ARG, "op_profile: empty problem");
+      if (a.T == 0) return fail(OPSCALE_ERR_INVALID_ARG, "%s: empty problem", who);
       launch = [=] {
         return opscale::launch_rope(a.q, a.k, a.q_row_stride, a.k_row_stride, a.positions, a.T, a.Hq, a.Hkv, a.D,
                                     a.theta, bf16, stream);
@@ -599,7 +656,7 @@ opscale_status opscale_op_profile(const opscale_op_desc* d, int32_t warmup, int3
       st = check_cache_write(a.k, a.v, a.kv_row_stride, a.k_cache, a.v_cache, a.slot_mapping, a.T, a.Hkv, a.D,
                              a.block_size, a.num_blocks, dt);
       if (st != OPSCALE_OK) return st;
-      if (a.T == 0) return fail(OPSCALE_ERR_INVALID_ARG, "op_profile: empty problem");
+      if (a.T == 0) return fail(OPSCALE_ERR_INVALID_ARG, "%s: empty problem", who);
       launch = [=] {
         return opscale::launch_cache_write(a.k, a.v, a.kv_row_stride, a.k_cache, a.v_cache, a.slot_mapping, a.T,
                                            a.Hkv, a.D, a.num_blocks * a.block_size, bf16, stream);
@@ -611,15 +668,33 @@ opscale_status opscale_op_profile(const opscale_op_desc* d, int32_t warmup, int3
       const auto& a = d->u.add_rmsnorm;
       st = check_add_rmsnorm(a.x, a.residual, a.w, a.y, a.M, a.H, a.eps, dt);
       if (st != OPSCALE_OK) return st;
-      if (a.M == 0) return fail(OPSCALE_ERR_INVALID_ARG, "op_profile: empty problem");
+      if (a.M == 0) return fail(OPSCALE_ERR_INVALID_ARG, "%s: empty problem", who);
       launch = [=] { return opscale::launch_add_rmsnorm(a.x, a.residual, a.w, a.y, a.M, a.H, a.eps, bf16, stream); };
       wk = work_add_rmsnorm(a.M, a.H, esize(dt));
       break;
     }
     default:
-      return fail(OPSCALE_ERR_INVALID_ARG, "op_profile: unknown op %d", (int)d->op);
+      return fail(OPSCALE_ERR_INVALID_ARG, "%s: unknown op %d", who, (int)d->op);
   }
-  if (!dtype_ok(dt)) return fail(OPSCALE_ERR_INVALID_ARG, "op_profile: unknown dtype");
+  if (!dtype_ok(dt)) return fail(OPSCALE_ERR_INVALID_ARG, "%s: unknown dtype", who);
+  return OPSCALE_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+opscale_status opscale_op_profile(const opscale_op_desc* d, int32_t warmup, int32_t iters,
+                                  void* flush_buf, size_t flush_bytes, hipStream_t stream,
+                                  opscale_profile* out) {
+  if (!d || !out) return fail(OPSCALE_ERR_INVALID_ARG, "op_profile: null desc or out");
+  if (iters < 1 || warmup < 0) return fail(OPSCALE_ERR_INVALID_ARG, "op_profile: iters must be >= 1, warmup >= 0");
+  if (flush_buf && !aligned16(flush_buf)) return fail(OPSCALE_ERR_INVALID_ARG, "op_profile: flush_buf must be 16-byte aligned");
+  std::function<hipError_t()> launch;
+  Work wk{};
+  opscale_status st = prepare_op(d, stream, "op_profile", &launch, &wk);
+  if (st != OPSCALE_OK) return st;
+  const bool bf16 = d->dt == OPSCALE_BF16;
 
   hipError_t e = g_events.init();
   if (e != hipSuccess) return hip_fail(e, "hipEventCreate");
@@ -677,6 +752,119 @@ opscale_status opscale_op_profile(const opscale_op_desc* d, int32_t warmup, int3
   p.transient_bytes = wk.transient;
   p.io_bytes = wk.io;
   *out = p;
+  return OPSCALE_OK;
+}
+
+opscale_status opscale_corun_profile(const opscale_op_desc* a, hipStream_t sa, const opscale_op_desc* b,
+                                     hipStream_t sb, int32_t warmup, int32_t iso_iters, float window_ms,
+                                     int32_t max_launches, const opscale_corun_trace* trace, opscale_corun* out) {
+  if (!a || !b || !out) return fail(OPSCALE_ERR_INVALID_ARG, "corun_profile: null desc or out");
+  if (warmup < 0 || iso_iters < 1 || iso_iters > 4096)
+    return fail(OPSCALE_ERR_INVALID_ARG, "corun_profile: warmup >= 0 and 1 <= iso_iters <= 4096 required");
+  if (max_launches < 4 || max_launches > 8192)
+    return fail(OPSCALE_ERR_INVALID_ARG, "corun_profile: max_launches %d outside [4, 8192]", max_launches);
+  if (!(window_ms > 0.f && window_ms <= 10000.f))
+    return fail(OPSCALE_ERR_INVALID_ARG, "corun_profile: window_ms must be in (0, 10000]");
+  if (sa == sb) return fail(OPSCALE_ERR_INVALID_ARG, "corun_profile: the two operators need two streams");
+  std::function<hipError_t()> la, lb;
+  Work wa{}, wb{};
+  opscale_status st = prepare_op(a, sa, "corun_profile (a)", &la, &wa);
+  if (st != OPSCALE_OK) return st;
+  if ((st = prepare_op(b, sb, "corun_profile (b)", &lb, &wb)) != OPSCALE_OK) return st;
+  hipError_t e;
+  for (int i = 0; i < warmup; ++i) {
+    if ((e = la()) != hipSuccess) return hip_fail(e, "corun warmup launch (a)");
+    if ((e = lb()) != hipSuccess) return hip_fail(e, "corun warmup launch (b)");
+  }
+  if ((e = hipStreamSynchronize(sa)) != hipSuccess) return hip_fail(e, "hipStreamSynchronize");
+  if ((e = hipStreamSynchronize(sb)) != hipSuccess) return hip_fail(e, "hipStreamSynchronize");
+
+  // T_v(b, p): each operator alone on its stream
+  std::vector<float> iso_a, iso_b;
+  if ((st = time_loop(la, sa, iso_iters, &iso_a)) != OPSCALE_OK) return st;
+  if ((st = time_loop(lb, sb, iso_iters, &iso_b)) != OPSCALE_OK) return st;
+  const float ta = median_of(iso_a), tb = median_of(iso_b);
+  // the window lasts at least four launches of the slower operator, so that
+  // launches of each fit inside the other's span
+  const double window_us = std::max((double)window_ms * 1000.0, 4.0 * (double)std::max(ta, tb));
+  auto launches = [&](float t_us) {
+    const double n = t_us > 0.f ? std::ceil(window_us / (double)t_us) : (double)max_launches;
+    return (int)std::max(4.0, std::min((double)max_launches, n));
+  };
+  const int na = launches(ta), nb = launches(tb);
+
+  // both loops at once: b waits for the reference event recorded on a, and
+  // the launches are enqueued in the order of their planned start times
+  EventPool pool;
+  if ((e = pool.make((size_t)na + (size_t)nb + 3)) != hipSuccess) return hip_fail(e, "hipEventCreate");
+  hipEvent_t ref = pool.ev[0];
+  hipEvent_t* ea = pool.ev.data() + 1;             // na + 1 events
+  hipEvent_t* eb = pool.ev.data() + 2 + (size_t)na;  // nb + 1 events
+  if ((e = hipEventRecord(ref, sa)) != hipSuccess) return hip_fail(e, "hipEventRecord");
+  if ((e = hipStreamWaitEvent(sb, ref, 0)) != hipSuccess) return hip_fail(e, "hipStreamWaitEvent");
+  if ((e = hipEventRecord(ea[0], sa)) != hipSuccess) return hip_fail(e, "hipEventRecord");
+  if ((e = hipEventRecord(eb[0], sb)) != hipSuccess) return hip_fail(e, "hipEventRecord");
+  int ia = 0, ib = 0;
+  while (ia < na || ib < nb) {
+    const bool take_a = ib >= nb || (ia < na && (double)ia * ta <= (double)ib * tb);
+    if (take_a) {
+      if ((e = la()) != hipSuccess) return hip_fail(e, "corun launch (a)");
+      if ((e = hipEventRecord(ea[++ia], sa)) != hipSuccess) return hip_fail(e, "hipEventRecord");
+    } else {
+      if ((e = lb()) != hipSuccess) return hip_fail(e, "corun launch (b)");
+      if ((e = hipEventRecord(eb[++ib], sb)) != hipSuccess) return hip_fail(e, "hipEventRecord");
+    }
+  }
+  if ((e = hipEventSynchronize(ea[na])) != hipSuccess) return hip_fail(e, "hipEventSynchronize");
+  if ((e = hipEventSynchronize(eb[nb])) != hipSuccess) return hip_fail(e, "hipEventSynchronize");
+  auto stamps = [&](hipEvent_t* ev, int n, std::vector<float>* t) {
+    t->resize((size_t)n + 1);
+    for (int i = 0; i <= n; ++i) {
+      float ms = 0.f;
+      const hipError_t r = hipEventElapsedTime(&ms, ref, ev[i]);
+      if (r != hipSuccess) return r;
+      (*t)[(size_t)i] = ms * 1000.f;
+    }
+    return hipSuccess;
+  };
+  std::vector<float> tsa, tsb;
+  if ((e = stamps(ea, na, &tsa)) != hipSuccess) return hip_fail(e, "hipEventElapsedTime");
+  if ((e = stamps(eb, nb, &tsb)) != hipSuccess) return hip_fail(e, "hipEventElapsedTime");
+  // T~_v(b, p): launches wholly inside the other operator's span
+  auto inside = [](const std::vector<float>& t, int n, float lo, float hi) {
+    std::vector<float> d;
+    for (int i = 0; i < n; ++i)
+      if (t[(size_t)i] >= lo && t[(size_t)i + 1] <= hi) d.push_back(t[(size_t)i + 1] - t[(size_t)i]);
+    return d;
+  };
+  const std::vector<float> co_a = inside(tsa, na, tsb[0], tsb[(size_t)nb]);
+  const std::vector<float> co_b = inside(tsb, nb, tsa[0], tsa[(size_t)na]);
+  opscale_corun r{};
+  r.n_a = na;
+  r.n_b = nb;
+  r.overlap_a = (int32_t)co_a.size();
+  r.overlap_b = (int32_t)co_b.size();
+  r.a_iso_us = ta;
+  r.b_iso_us = tb;
+  r.a_co_us = median_of(co_a);
+  r.b_co_us = median_of(co_b);
+  r.interference_a = co_a.empty() || ta <= 0.f ? 0.0 : (double)r.a_co_us / (double)ta;
+  r.interference_b = co_b.empty() || tb <= 0.f ? 0.0 : (double)r.b_co_us / (double)tb;
+  if (trace) {
+    for (int i = 0; i < na; ++i) {
+      if (trace->a_start) trace->a_start[i] = tsa[(size_t)i];
+      if (trace->a_end) trace->a_end[i] = tsa[(size_t)i + 1];
+    }
+    for (int i = 0; i < nb; ++i) {
+      if (trace->b_start) trace->b_start[i] = tsb[(size_t)i];
+      if (trace->b_end) trace->b_end[i] = tsb[(size_t)i + 1];
+    }
+    for (int i = 0; i < iso_iters; ++i) {
+      if (trace->a_iso) trace->a_iso[i] = iso_a[(size_t)i];
+      if (trace->b_iso) trace->b_iso[i] = iso_b[(size_t)i];
+    }
+  }
+  *out = r;
   return OPSCALE_OK;
 }
 

@@ -244,6 +244,15 @@ class Measurer:
         return t.to(torch.bfloat16 if self._dt == "bf16" else torch.float32)
 
     def __call__(self, sig: OpSignature, B: int, L_: int) -> Sample:
+        desc, keep = self.build(sig, B, L_)
+        p = self.L.opscale_op_profile(desc, self.warmup, self.iters, self.flush)
+        del keep
+        return Sample(B, L_, p.us_median, p.us_p10, p.us_p90, int(p.weight_bytes), int(p.transient_bytes),
+                      int(p.io_bytes), float(p.alg_flops), float(p.alg_bytes))
+
+    def build(self, sig: OpSignature, B: int, L_: int):
+        """The operands of `sig` at (B, L) on the GPU and its descriptor:
+        (desc, tensors to keep alive while the descriptor is used)."""
         torch, L = self.torch, self.L
         self._dt = sig.dtype
         T = B * L_ if sig.phase == PREFILL else B
@@ -318,10 +327,7 @@ class Measurer:
             desc = L.desc_attn_decode(q, kc, vc, table, ctx, o, L_, 1.0 / math.sqrt(D), ws)
         else:
             raise ValueError(f"unknown operator kind {k}")
-        p = L.opscale_op_profile(desc, self.warmup, self.iters, self.flush)
-        del keep
-        return Sample(B, L_, p.us_median, p.us_p10, p.us_p90, int(p.weight_bytes), int(p.transient_bytes),
-                      int(p.io_bytes), float(p.alg_flops), float(p.alg_bytes))
+        return desc, keep
 
 
 def domain_for(sig: OpSignature, max_prefill_tokens: int = 65536) -> Domain:

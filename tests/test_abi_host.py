@@ -28,7 +28,10 @@ def test_header_declares_expected_entry_points():
     for name in ("opscale_rmsnorm", "opscale_linear", "opscale_swiglu", "opscale_attn_prefill",
                  "opscale_attn_decode", "opscale_attn_decode_workspace_size", "opscale_op_profile",
                  "opscale_version", "opscale_status_string", "opscale_last_error",
-                 "opscale_rope", "opscale_reshape_and_cache", "opscale_add_rmsnorm"):
+                 "opscale_rope", "opscale_reshape_and_cache", "opscale_add_rmsnorm",
+                 "opscale_cu_layout", "opscale_cu_mask_build", "opscale_cu_stream_create",
+                 "opscale_cu_stream_destroy", "opscale_cu_stream_mask", "opscale_cu_probe",
+                 "opscale_corun_profile"):
         assert name in d
 
 
@@ -187,7 +190,12 @@ def test_profile_descriptor_layout_matches_header(tmp_path):
     lines = ['#include <stdio.h>', '#include <stddef.h>', '#include "opscale.h"', "int main(void) {",
              'printf("desc_size %zu\\n", sizeof(opscale_op_desc));',
              'printf("desc_u %zu\\n", offsetof(opscale_op_desc, u));',
-             'printf("profile %zu\\n", sizeof(opscale_profile));']
+             'printf("profile %zu\\n", sizeof(opscale_profile));',
+             'printf("corun %zu\\n", sizeof(opscale_corun));',
+             'printf("corun_trace %zu\\n", sizeof(opscale_corun_trace));']
+    for cname, cls in (("opscale_corun", L.Corun), ("opscale_corun_trace", L._CorunTrace)):
+        for f, _ in cls._fields_:
+            lines.append(f'printf("{cname}:{f} %zu\\n", offsetof({cname}, {f}));')
     for m, cls in members.items():
         for f, _ in cls._fields_:
             lines.append(f'printf("{m}.{f} %zu\\n", offsetof(opscale_op_desc, u.{m}.{f}) - '
@@ -206,6 +214,11 @@ def test_profile_descriptor_layout_matches_header(tmp_path):
     assert int(out.pop("desc_size")) == ctypes.sizeof(L.OpDesc)
     assert int(out.pop("desc_u")) == L.OpDesc.u.offset
     assert int(out.pop("profile")) == ctypes.sizeof(L.Profile)
+    assert int(out.pop("corun")) == ctypes.sizeof(L.Corun)
+    assert int(out.pop("corun_trace")) == ctypes.sizeof(L._CorunTrace)
+    for cname, cls in (("opscale_corun", L.Corun), ("opscale_corun_trace", L._CorunTrace)):
+        for f, _ in cls._fields_:
+            assert int(out.pop(f"{cname}:{f}")) == getattr(cls, f).offset, f"{cname}.{f}"
     for m, cls in members.items():
         for f, _ in cls._fields_:
             assert int(out[f"{m}.{f}"]) == getattr(cls, f).offset, f"{m}.{f}"
