@@ -282,8 +282,10 @@ typedef struct {
 
 /*
  * Run the described operator `warmup` times untimed, then `iters` times, each
- * preceded (when flush_buf != NULL) by a device write of flush_bytes to
- * flush_buf so that no operand is served from the 256 MB last-level cache.
+ * preceded (when flush_buf != NULL) by a device read of flush_bytes of
+ * flush_buf, so that no operand is served from L2 or the 256 MB last-level
+ * cache and no dirty line is left for the operator to write back
+ * (flush_buf's contents are don't-care).
  * Each iteration is timed alone with device events.  Fills `out` with the
  * timing distribution, the algorithmic work and the roofline fraction against
  * MI355X peaks (bf16 matrix 2.5 PFLOP/s, fp32 matrix 157.3 TFLOP/s, HBM

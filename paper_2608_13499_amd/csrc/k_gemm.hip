@@ -367,6 +367,14 @@ hipError_t launch_linear(const void* x, const void* W, const void* bias, void* y
   if (bf16) return launch_gemm_bf16<OPSCALE_GEMM_CFG>(x, W, bias, y, M, N, K, s);
 #else
   if (bf16) {
+    // Decode-sized M: the weights dominate and the tiles below would leave
+    // most CUs idle.  OPSCALE_GEMM_SKINNY=0 (or a forced tile below) turns
+    // this path off, =1 takes it wherever it is supported (tuning and tests).
+    const char* sk = getenv("OPSCALE_GEMM_SKINNY");
+    const bool sk_off = (sk && strcmp(sk, "0") == 0) || getenv("OPSCALE_GEMM_TILE");
+    const bool sk_on = sk && strcmp(sk, "1") == 0;
+    if (!sk_off && (sk_on ? skinny_linear_supported(M, N, K) : skinny_linear_preferred(M, N, K)))
+      return launch_linear_skinny(x, W, bias, y, M, N, K, s);
     // One workgroup per CU at a time, so a launch runs in ceil(tiles / 256)
     // rounds.  Pick the tile whose rounds x tile area x relative per-element
     // cost is smallest: 256x256 moves the fewest operand bytes per flop,

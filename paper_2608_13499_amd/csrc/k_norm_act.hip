@@ -164,9 +164,19 @@ hipError_t launch_swiglu(const void* gu, void* out, int64_t M, int64_t F, bool b
 }
 
 // ---------------------------------------------------------------- flush ----
+// Reads every byte of buf, so the caches then hold clean lines of buf and
+// nothing of the timed operator's operands.  (A writing flush would leave the
+// last-level cache full of dirty lines, and the next kernel would pay for
+// their write-back.)  The XOR of the data is stored only if it equals `tag`,
+// which keeps the loads alive and practically never happens.
 __global__ __launch_bounds__(256) void flush_kernel(u32x4* buf, size_t nvec, uint32_t tag) {
-  for (size_t i = (size_t)blockIdx.x * 256 + threadIdx.x; i < nvec; i += (size_t)gridDim.x * 256)
-    buf[i] = u32x4{tag, (uint32_t)i, tag, (uint32_t)(i >> 32)};
+  uint32_t h = 0;
+  for (size_t i = (size_t)blockIdx.x * 256 + threadIdx.x; i < nvec; i += (size_t)gridDim.x * 256) {
+    const u32x4 v = buf[i];  // a plain load: it allocates in L2 and the MALL
+    h ^= v[0] ^ v[1] ^ v[2] ^ v[3];
+  }
+  const size_t me = (size_t)blockIdx.x * 256 + threadIdx.x;
+  if (h == tag && me < nvec) buf[me][0] = h;
 }
 
 hipError_t launch_flush(void* buf, size_t bytes, hipStream_t s) {

@@ -16,6 +16,15 @@ hipError_t launch_swiglu(const void* gu, void* out, int64_t M, int64_t F, bool b
 hipError_t launch_linear(const void* x, const void* W, const void* bias, void* y, int64_t M,
                          int64_t N, int64_t K, bool bf16, hipStream_t s);
 
+// The small-M (decode batch) bf16 linear: all M rows per workgroup, K split
+// over its waves.  Supported for 1 <= M <= kSkinnyMaxM with K % 32 == 0;
+// preferred over the tiled GEMM where it measured faster.
+constexpr int64_t kSkinnyMaxM = 256;
+bool skinny_linear_supported(int64_t M, int64_t N, int64_t K);
+bool skinny_linear_preferred(int64_t M, int64_t N, int64_t K);
+hipError_t launch_linear_skinny(const void* x, const void* W, const void* bias, void* y, int64_t M, int64_t N,
+                                int64_t K, hipStream_t s);
+
 hipError_t launch_attn_prefill(const void* q, const void* k, const void* v, int64_t q_stride,
                                int64_t kv_stride, void* o, const int32_t* cu, int32_t B,
                                int64_t total_tokens, int32_t max_seqlen, int32_t Hq, int32_t Hkv,
@@ -45,8 +54,8 @@ hipError_t launch_cache_write(const void* k, const void* v, int64_t kv_stride, v
 hipError_t launch_add_rmsnorm(const void* x, void* res, const void* w, void* y, int64_t M, int64_t H, float eps,
                               bool bf16, hipStream_t s);
 
-// Writes a fixed pattern over `bytes` of `buf` (evicts the last-level cache
-// before a timed iteration).
+// Reads `bytes` of `buf` through the caches (evicts L2 and the last-level
+// cache, leaving only clean lines, before a timed iteration).
 hipError_t launch_flush(void* buf, size_t bytes, hipStream_t s);
 
 }  // namespace opscale

@@ -88,6 +88,31 @@ def test_linear_each_tile(ops, monkeypatch, tile, M, N, K, bias):
     assert_close(f64(y.cpu()), oracle.linear(f64(x), f64(W), None if b is None else f64(b)), "bf16", "linear")
 
 
+@pytest.mark.parametrize("M,N,K,bias", [
+    (1, 256, 64, False), (3, 40, 96, True), (16, 6144, 4096, False), (17, 520, 128, True), (33, 8, 32, False),
+    (64, 4096, 14336, False), (100, 1000, 4096, True), (129, 264, 256, False), (256, 6144, 4096, False),
+    (256, 4104, 32, True),
+])
+@pytest.mark.parametrize("ng", ["1", "2"])
+def test_linear_small_m(ops, monkeypatch, ng, M, N, K, bias):
+    """The decode-batch path (M <= 256, K % 32 == 0), forced on, with 16 and
+    32 columns per workgroup: every row-group count, N tails shorter than one
+    column group, K of one k-step per wave and fewer k-steps than waves."""
+    import torch
+    monkeypatch.delenv("OPSCALE_GEMM_TILE", raising=False)
+    monkeypatch.setenv("OPSCALE_GEMM_SKINNY", "1")
+    monkeypatch.setenv("OPSCALE_SKINNY_NG", ng)
+    say(f"linear bf16 small-M NG={ng} M={M} N={N} K={K} bias={bias}")
+    x = gen(24, "x", (M, K), "bf16")
+    W = gen(24, "w_qkv", (N, K), "bf16", std=0.02)
+    b = gen(24, "bias", (N,), "bf16") if bias else None
+    y = ops.opscale_linear(cuda(x), cuda(W), None if b is None else cuda(b))
+    y2 = ops.opscale_linear(cuda(x), cuda(W), None if b is None else cuda(b))
+    torch.cuda.synchronize()
+    assert torch.equal(y, y2)  # fixed reduction order
+    assert_close(f64(y.cpu()), oracle.linear(f64(x), f64(W), None if b is None else f64(b)), "bf16", "linear")
+
+
 def test_linear_identity_weight(ops):
     """W = I (bf16-exact) returns x exactly: no accumulation rounding occurs."""
     import torch
