@@ -1,9 +1,10 @@
 // Decode attention: one new query token per sequence against its paged KV
 // cache [num_blocks, block_size, Hkv, D].
 //
-// bf16 path.  The key range of every sequence is cut into splits of about
-// kChunk keys (split-KV), so 256 sequences give thousands of workgroups and
-// long and short contexts balance.  A workgroup of 8 waves owns one (split,
+// bf16 path.  The key range of every sequence is cut into splits (split-KV) of
+// 32 ... 512 keys, the size chosen per launch so that the batch gives about
+// 1024 workgroups: 256 sequences of thousands of keys get 512-key splits,
+// a single sequence 32-key ones, and long and short contexts balance.  A workgroup of 8 waves owns one (split,
 // sequence, group of up to 8 KV heads): for the 8-head layer every wave takes
 // one KV head and serves all G query heads of that head, so each page of the
 // cache (block_size slots x all heads, contiguous) is streamed by one
@@ -36,7 +37,9 @@ namespace opscale {
 
 namespace {
 constexpr float kLog2e = 1.4426950408889634f;
-constexpr int kChunk = 512;  // nominal keys per split, and keys per page window
+constexpr int kChunk = 512;  // the largest split, and keys per page window
+constexpr int kFillWorkgroups = 1024;  // splits are sized to give about this many
+constexpr int kMaxSplitsForFill = 64;   // ... but a sequence gets at most this many
 constexpr int kTile = 32;    // keys per wave step
 constexpr int kWaves = 8;    // waves per workgroup
 // Page ids of one window of kChunk keys (any block size >= 1) fit in here.
@@ -46,11 +49,12 @@ struct SplitPlan {
   int n, splits, chunk;
 };
 
-// Splits of one sequence: at most max_splits, each a multiple of kTile keys.
-__device__ __forceinline__ SplitPlan plan_splits(int n, int max_splits) {
+// Splits of one sequence: about chunk_keys keys each, at most max_splits,
+// each a multiple of kTile keys.
+__device__ __forceinline__ SplitPlan plan_splits(int n, int max_splits, int chunk_keys) {
   SplitPlan p;
   p.n = n;
-  p.splits = n <= 0 ? 0 : min(max_splits, (n + kChunk - 1) / kChunk);
+  p.splits = n <= 0 ? 0 : min(max_splits, (n + chunk_keys - 1) / chunk_keys);
   const int per = p.splits > 0 ? (n + p.splits - 1) / p.splits : 0;
   p.chunk = (per + kTile - 1) / kTile * kTile;
   return p;
@@ -71,12 +75,20 @@ __device__ __forceinline__ u32x2 lds_read_tr16(const OPS_LDS char* p) {
 __device__ __forceinline__ int v_swz(int r) { return (r & 3) << 1; }
 }  // namespace
 
-int32_t decode_max_splits(int32_t max_context_len) {
-  return std::max<int32_t>(1, (max_context_len + kChunk - 1) / kChunk);
+int32_t decode_chunk_keys(int32_t B, int32_t max_context_len) {
+  const int64_t ctx = std::max(1, max_context_len);
+  const int64_t per = std::max(((int64_t)std::max(1, B) * ctx + kFillWorkgroups - 1) / kFillWorkgroups,
+                               (ctx + kMaxSplitsForFill - 1) / kMaxSplitsForFill);
+  return (int32_t)std::min<int64_t>(kChunk, std::max<int64_t>(kTile, (per + kTile - 1) / kTile * kTile));
+}
+
+int32_t decode_max_splits(int32_t B, int32_t max_context_len) {
+  const int32_t c = decode_chunk_keys(B, max_context_len);
+  return std::max<int32_t>(1, (max_context_len + c - 1) / c);
 }
 
 size_t decode_workspace_bytes(int32_t B, int32_t Hq, int32_t D, int32_t max_context_len) {
-  return (size_t)4 * (size_t)B * (size_t)Hq * (size_t)decode_max_splits(max_context_len) *
+  return (size_t)4 * (size_t)B * (size_t)Hq * (size_t)decode_max_splits(B, max_context_len) *
          (size_t)(D + 2);
 }
 
@@ -85,7 +97,7 @@ template <int D, int G, int HB>
 __global__ __launch_bounds__(512, 4) void attn_decode_split_kernel(
     const __bf16* __restrict__ q, int64_t q_stride, const __bf16* __restrict__ kc, const __bf16* __restrict__ vc,
     const int32_t* __restrict__ table, const int32_t* __restrict__ ctx, int Hq, int Hkv,
-    int log2bs, int max_blocks, int64_t num_blocks, int max_splits, float scale_log2,
+    int log2bs, int max_blocks, int64_t num_blocks, int max_splits, int chunk_keys, float scale_log2,
     float* __restrict__ ws_o, float* __restrict__ ws_ml) {
   constexpr int CPR = D / 8;             // 16-byte chunks per cache row
   constexpr int KSTEPS = D / 32;         // MFMA k-steps over the head dim (QK)
@@ -101,7 +113,7 @@ __global__ __launch_bounds__(512, 4) void attn_decode_split_kernel(
   const int split = blockIdx.x, hg = blockIdx.y, b = blockIdx.z;
   const int bs = 1 << log2bs;
   const int n = min(ctx[b], max_blocks << log2bs);
-  const SplitPlan plan = plan_splits(n, max_splits);
+  const SplitPlan plan = plan_splits(n, max_splits, chunk_keys);
   const int k_begin = split * plan.chunk;
   if (split >= plan.splits || k_begin >= n) return;
   const int k_end = min(n, k_begin + plan.chunk);
@@ -322,32 +334,71 @@ __global__ __launch_bounds__(512, 4) void attn_decode_split_kernel(
   }
 }
 
-// Merge the splits of one (sequence, head); one wave per pair.
+// Merge the splits of one (sequence, head); one wave per pair.  The splits'
+// maxima and weights are taken 64 at a time across the lanes; the weighted
+// sum of their partial outputs then runs over the splits in order (lane l
+// owns output columns l + 64 c), so the result is deterministic.
 template <int D>
 __global__ __launch_bounds__(64) void attn_decode_combine_kernel(
     const float* __restrict__ ws_o, const float* __restrict__ ws_ml, const int32_t* __restrict__ ctx,
-    __bf16* __restrict__ o, int Hq, int log2bs, int max_blocks, int max_splits) {
+    __bf16* __restrict__ o, int Hq, int log2bs, int max_blocks, int max_splits, int chunk_keys) {
+  constexpr int DPL = D / 64;
+  __shared__ float fw[64];
   const int h = blockIdx.x, b = blockIdx.y, lane = threadIdx.x;
   const int n = min(ctx[b], max_blocks << log2bs);
-  const SplitPlan plan = plan_splits(n, max_splits);
+  const SplitPlan plan = plan_splits(n, max_splits, chunk_keys);
   const int64_t slot0 = ((int64_t)b * Hq + h) * max_splits;
+  auto used = [&](int sp) { return sp < plan.splits && sp * plan.chunk < n; };
   float M = -INFINITY;
-  for (int s = 0; s < plan.splits; ++s)
-    if (s * plan.chunk < n) M = fmaxf(M, ws_ml[(slot0 + s) * 2]);
-  float acc[D / 64] = {};
+  for (int sp = lane; sp < plan.splits; sp += 64)
+    if (used(sp)) M = fmaxf(M, ws_ml[(slot0 + sp) * 2]);
+  M = wave_max(M);
+  float acc[DPL] = {};
   float l = 0.f;
-  for (int s = 0; s < plan.splits; ++s) {
-    if (s * plan.chunk >= n) continue;
-    const float ms = ws_ml[(slot0 + s) * 2];
-    if (ms == -INFINITY) continue;  // every key of the split was skipped
-    const float f = fast_exp2(ms - M);
-    l += f * ws_ml[(slot0 + s) * 2 + 1];
+  for (int s0 = 0; s0 < plan.splits; s0 += 64) {
+    float f = 0.f;
+    const int sp = s0 + lane;
+    if (used(sp)) {
+      const float ms = ws_ml[(slot0 + sp) * 2];
+      if (ms != -INFINITY) {  // -inf: every key of the split was skipped
+        f = fast_exp2(ms - M);
+        l += f * ws_ml[(slot0 + sp) * 2 + 1];
+      }
+    }
+    fw[lane] = f;
+    __builtin_amdgcn_wave_barrier();
+    const int cnt = min(64, plan.splits - s0);
+    // The rows of unused splits hold stale data: they are loaded anyway (so
+    // that the loads do not wait on the weights) and dropped by the select.
+    const float* base = ws_o + (slot0 + s0) * D + lane;
+    int j = 0;
+    for (; j + 8 <= cnt; j += 8) {
+      float v[8][DPL];
 #pragma unroll
-    for (int c = 0; c < D / 64; ++c) acc[c] += f * ws_o[(slot0 + s) * D + lane + c * 64];
+      for (int u = 0; u < 8; ++u)
+#pragma unroll
+        for (int c = 0; c < DPL; ++c) v[u][c] = base[(j + u) * D + c * 64];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        const float fj = fw[j + u];
+#pragma unroll
+        for (int c = 0; c < DPL; ++c) acc[c] += fj == 0.f ? 0.f : fj * v[u][c];
+      }
+    }
+    for (; j < cnt; ++j) {
+      const float fj = fw[j];
+#pragma unroll
+      for (int c = 0; c < DPL; ++c) {
+        const float v = base[j * D + c * 64];
+        acc[c] += fj == 0.f ? 0.f : fj * v;
+      }
+    }
+    __builtin_amdgcn_wave_barrier();
   }
+  l = wave_sum(l);
   const float inv = l > 0.f ? 1.f / l : 0.f;
 #pragma unroll
-  for (int c = 0; c < D / 64; ++c) o[((int64_t)b * Hq + h) * D + lane + c * 64] = (__bf16)(acc[c] * inv);
+  for (int c = 0; c < DPL; ++c) o[((int64_t)b * Hq + h) * D + lane + c * 64] = (__bf16)(acc[c] * inv);
 }
 
 // ------------------------------------------------------------ fp32 path ----
@@ -426,7 +477,8 @@ hipError_t launch_attn_decode(const void* q, int64_t q_stride, const void* kcach
                          Hkv, log2bs, max_blocks, num_blocks, scale);
     return hipGetLastError();
   }
-  const int max_splits = decode_max_splits(max_context_len);
+  const int chunk_keys = decode_chunk_keys(B, max_context_len);
+  const int max_splits = decode_max_splits(B, max_context_len);
   float* ws_o = static_cast<float*>(ws);
   float* ws_ml = ws_o + (size_t)B * Hq * max_splits * D;
   const float sl2 = scale * kLog2e;
@@ -437,7 +489,7 @@ hipError_t launch_attn_decode(const void* q, int64_t q_stride, const void* kcach
   hipLaunchKernelGGL((attn_decode_split_kernel<DD, GG, HH>), grid, dim3(kWaves * 64), 0, s,     \
                      static_cast<const __bf16*>(q), q_stride, static_cast<const __bf16*>(kcache), \
                      static_cast<const __bf16*>(vcache), table, ctx, Hq, Hkv, log2bs, max_blocks, \
-                     num_blocks, max_splits, sl2, ws_o, ws_ml)
+                     num_blocks, max_splits, chunk_keys, sl2, ws_o, ws_ml)
 #define OPS_DEC_H(DD, GG)                    \
   switch (HB) {                              \
     case 1: OPS_DEC(DD, GG, 1); break;       \
@@ -465,10 +517,10 @@ hipError_t launch_attn_decode(const void* q, int64_t q_stride, const void* kcach
   const dim3 cgrid((unsigned)Hq, (unsigned)B);
   if (D == 128)
     hipLaunchKernelGGL((attn_decode_combine_kernel<128>), cgrid, dim3(64), 0, s, ws_o, ws_ml, ctx,
-                       static_cast<__bf16*>(o), Hq, log2bs, max_blocks, max_splits);
+                       static_cast<__bf16*>(o), Hq, log2bs, max_blocks, max_splits, chunk_keys);
   else
     hipLaunchKernelGGL((attn_decode_combine_kernel<64>), cgrid, dim3(64), 0, s, ws_o, ws_ml, ctx,
-                       static_cast<__bf16*>(o), Hq, log2bs, max_blocks, max_splits);
+                       static_cast<__bf16*>(o), Hq, log2bs, max_blocks, max_splits, chunk_keys);
   return hipGetLastError();
 }
 

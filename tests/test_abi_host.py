@@ -108,7 +108,14 @@ def test_prefill_validation(lib):
 def test_decode_validation_and_workspace(lib):
     f = lib.opscale_attn_decode
     need = lib.opscale_attn_decode_workspace_size(256, 32, 128, 8192)
-    assert need == 4 * 256 * 32 * 16 * 130
+    assert need == 4 * 256 * 32 * 16 * 130            # 512-key splits
+    # small batches get shorter splits (about 1024 workgroups, at most 64
+    # splits a sequence): one sequence of 2048 keys takes 64 splits of 32
+    # keys, of 8192 keys 64 splits of 128, 16 sequences 64 splits of 32
+    assert lib.opscale_attn_decode_workspace_size(1, 32, 128, 2048) == 4 * 1 * 32 * 64 * 130
+    assert lib.opscale_attn_decode_workspace_size(1, 32, 128, 8192) == 4 * 1 * 32 * 64 * 130
+    assert lib.opscale_attn_decode_workspace_size(16, 32, 128, 2048) == 4 * 16 * 32 * 64 * 130
+    assert lib.opscale_attn_decode_workspace_size(64, 32, 128, 2048) == 4 * 64 * 32 * 16 * 130
     ok = dict(q=A16, qs=32 * 128, kc=A16, vc=A16, tab=A16, ctx=A16, o=A16 * 8, B=256, Hq=32, Hkv=8, D=128, bs=16,
               mb=512, nb=69424, mc=8192, scale=0.08, dt=1, ws=A16 * 32, wsb=need)
 
