@@ -30,6 +30,7 @@ namespace opscale {
 namespace {
 
 constexpr int kNumCUs = 256;  // MI355X compute units
+constexpr int64_t kSplitKMaxM = 2048;  // split-K is for small M (decode batches)
 
 // Tile configuration: BM x BN block tile, K in slices of BK, WGM x WGN waves
 // (each owns a (BM/WGM) x (BN/WGN) sub-tile), STAGES-deep LDS ring.
@@ -81,8 +82,8 @@ __device__ __forceinline__ void wait_vmcnt() {
 // loads w, w + waves, ...; lane p of a load writes LDS bytes [p*16, p*16+16)
 // of its 1 KB group: row p / CPR, physical chunk p % CPR.
 template <class C, int ROWS>
-__device__ __forceinline__ void load_slice(__amdgpu_buffer_rsrc_t rsrc, OPS_LDS char* lds, int K, int k0,
-                                           int wave, int lane) {
+__device__ __forceinline__ void load_slice(__amdgpu_buffer_rsrc_t rsrc, OPS_LDS char* lds, int ld, int K,
+                                           int k0, int wave, int lane) {
   const int rl = lane / C::kCPR, pc = lane % C::kCPR;
   constexpr int kPerWave = ROWS / C::kRowsPerLoad / C::kWaves;
 #pragma unroll
@@ -91,7 +92,7 @@ __device__ __forceinline__ void load_slice(__amdgpu_buffer_rsrc_t rsrc, OPS_LDS 
     const int r = grp * C::kRowsPerLoad + rl;
     const int c = pc ^ swz<C::kCPR>(r);
     const int k = k0 + c * 8;
-    const uint32_t voff = k < K ? (uint32_t)(((int64_t)r * K + k) * 2) : kOobOffset;
+    const uint32_t voff = k < K ? (uint32_t)(((int64_t)r * ld + k) * 2) : kOobOffset;
     buffer_load16_lds(rsrc, lds + grp * 1024, voff);
   }
 }
@@ -103,19 +104,29 @@ __device__ __forceinline__ bf16x8 lds_frag(const OPS_LDS char* p) {
 
 }  // namespace
 
+// Split-K (splits > 1): workgroup blockIdx.x / tiles takes the K range
+// [split * kchunk, (split + 1) * kchunk) and writes its fp32 partial tile to
+// part[split][M][N] (no bias); a second kernel sums the splits in order.
 template <class C>
 __global__ __launch_bounds__(C::kThreads, 1) void gemm_bf16_kernel(const __bf16* __restrict__ x,
                                                                    const __bf16* __restrict__ W,
                                                                    const __bf16* __restrict__ bias,
                                                                    __bf16* __restrict__ y, int M, int N,
-                                                                   int K, int group_m) {
+                                                                   int K_total, int group_m, int kchunk,
+                                                                   float* __restrict__ part) {
   extern __shared__ __attribute__((aligned(16))) char smem_raw[];
   OPS_LDS char* smem = (OPS_LDS char*)smem_raw;
   constexpr int BM = C::BM, BN = C::BN, BK = C::BK, WM = C::WM, WN = C::WN, S = C::STAGES;
   constexpr int TM = WM / 32, TN = WN / 32;  // 32x32 MFMA tiles per wave
 
   const int tiles_m = (M + BM - 1) / BM, tiles_n = (N + BN - 1) / BN;
-  const uint32_t tid = xcd_remap(blockIdx.x, (uint32_t)(tiles_m * tiles_n));
+  const int tiles = tiles_m * tiles_n;
+  const int split = blockIdx.x / tiles;
+  const uint32_t tid = xcd_remap(blockIdx.x - split * tiles, (uint32_t)tiles);
+  // this workgroup's K range: K elements starting at k_begin, rows ld apart
+  const int ld = K_total;
+  const int k_begin = split * kchunk;
+  const int K = min(K_total - k_begin, kchunk);
   // grouped order: group_m tile-rows sweep the tile-columns together, so a
   // W column-block is fetched once per group and reused from L2 / MALL by
   // every tile-row of the group while the group's x rows stay cache resident
@@ -131,8 +142,10 @@ __global__ __launch_bounds__(C::kThreads, 1) void gemm_bf16_kernel(const __bf16*
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
   const int wm = wave % C::WGM, wn = wave / C::WGM;
 
-  const __amdgpu_buffer_rsrc_t xr = make_rsrc(x + (int64_t)m0 * K, (uint32_t)(min(BM, M - m0) * K * 2));
-  const __amdgpu_buffer_rsrc_t wr = make_rsrc(W + (int64_t)n0 * K, (uint32_t)(min(BN, N - n0) * K * 2));
+  const __amdgpu_buffer_rsrc_t xr = make_rsrc(x + (int64_t)m0 * ld + k_begin,
+                                              (uint32_t)(((int64_t)(min(BM, M - m0) - 1) * ld + K) * 2));
+  const __amdgpu_buffer_rsrc_t wr = make_rsrc(W + (int64_t)n0 * ld + k_begin,
+                                              (uint32_t)(((int64_t)(min(BN, N - n0) - 1) * ld + K) * 2));
 
   f32x16 acc[TN][TM];
 #pragma unroll
@@ -144,8 +157,8 @@ __global__ __launch_bounds__(C::kThreads, 1) void gemm_bf16_kernel(const __bf16*
   auto stage_x = [&](int s) { return smem + s * C::kStageBytes; };
   auto stage_w = [&](int s) { return smem + s * C::kStageBytes + BM * C::kRowBytes; };
   auto load = [&](int kt) {
-    load_slice<C, BM>(xr, stage_x(kt % S), K, kt * BK, wave, lane);
-    load_slice<C, BN>(wr, stage_w(kt % S), K, kt * BK, wave, lane);
+    load_slice<C, BM>(xr, stage_x(kt % S), ld, K, kt * BK, wave, lane);
+    load_slice<C, BN>(wr, stage_w(kt % S), ld, K, kt * BK, wave, lane);
   };
 
 #pragma unroll
@@ -191,7 +204,7 @@ __global__ __launch_bounds__(C::kThreads, 1) void gemm_bf16_kernel(const __bf16*
         const int grp = (isx ? q : q - LX) * C::kWaves + wave;
         const int r = grp * C::kRowsPerLoad + rl;
         const int k = k0 + ((pc ^ swz<C::kCPR>(r)) << 3);
-        const uint32_t voff = (more && k < K) ? (uint32_t)(((int64_t)r * K + k) * 2) : kOobOffset;
+        const uint32_t voff = (more && k < K) ? (uint32_t)(((int64_t)r * ld + k) * 2) : kOobOffset;
         buffer_load16_lds(isx ? xr : wr, dst + (isx ? 0 : BM * C::kRowBytes) + grp * 1024, voff);
         __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
       }
@@ -260,7 +273,26 @@ __global__ __launch_bounds__(C::kThreads, 1) void gemm_bf16_kernel(const __bf16*
   wait_vmem();  // no LDS DMA may still be in flight when the workgroup ends
 
   // Epilogue.  acc[i][j] element e: n = n0 + wn*WN + i*32 + (e/4)*8 + fh*4 + e%4,
-  // m = m0 + wm*WM + j*32 + fr.  Four consecutive n per lane -> one 8-byte store.
+  // m = m0 + wm*WM + j*32 + fr.  Four consecutive n per lane -> one 8-byte store
+  // (one 16-byte store of fp32 partials under split-K).
+  if (part) {
+    float* pbase = part + (int64_t)split * M * N;
+#pragma unroll
+    for (int j = 0; j < TM; ++j) {
+      const int m = m0 + wm * WM + j * 32 + fr;
+      if (m >= M) continue;
+#pragma unroll
+      for (int i = 0; i < TN; ++i)
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+          const int n = n0 + wn * WN + i * 32 + g * 8 + fh * 4;
+          if (n >= N) continue;
+          *reinterpret_cast<f32x4*>(pbase + (int64_t)m * N + n) =
+              f32x4{acc[i][j][g * 4 + 0], acc[i][j][g * 4 + 1], acc[i][j][g * 4 + 2], acc[i][j][g * 4 + 3]};
+        }
+    }
+    return;
+  }
 #pragma unroll
   for (int j = 0; j < TM; ++j) {
     const int m = m0 + wm * WM + j * 32 + fr;
@@ -337,9 +369,30 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(const float* __restrict__
   }
 }
 
+// y[m][n] = bf16(sum over splits s of part[s][m][n] (in split order) + bias[n]),
+// four consecutive elements per thread (N is a multiple of 8).
+__global__ __launch_bounds__(256) void splitk_reduce_kernel(const float* __restrict__ part, int splits,
+                                                            const __bf16* __restrict__ bias,
+                                                            __bf16* __restrict__ y, int64_t MN, int N) {
+  const int64_t n4 = MN / 4;
+  for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < n4; i += (int64_t)gridDim.x * 256) {
+    f32x4 a = reinterpret_cast<const f32x4*>(part)[i];
+    for (int sp = 1; sp < splits; ++sp) a += reinterpret_cast<const f32x4*>(part + (int64_t)sp * MN)[i];
+    if (bias) {
+      const int n = (int)((i * 4) % N);
+      const u32x2 bb = *reinterpret_cast<const u32x2*>(bias + n);
+      a[0] += bf_lo(bb[0]);
+      a[1] += bf_hi(bb[0]);
+      a[2] += bf_lo(bb[1]);
+      a[3] += bf_hi(bb[1]);
+    }
+    reinterpret_cast<u32x2*>(y)[i] = u32x2{pack_bf2(a[0], a[1]), pack_bf2(a[2], a[3])};
+  }
+}
+
 template <class C>
 static hipError_t launch_gemm_bf16(const void* x, const void* W, const void* bias, void* y, int64_t M,
-                                   int64_t N, int64_t K, hipStream_t s) {
+                                   int64_t N, int64_t K, hipStream_t s, int splits = 1, float* part = nullptr) {
   // More than 64 KB of dynamic LDS per workgroup needs the limit raised once
   // per process (a host-side function attribute, no allocation).
   static const hipError_t attr = hipFuncSetAttribute(
@@ -354,11 +407,31 @@ static hipError_t launch_gemm_bf16(const void* x, const void* W, const void* bia
   constexpr int64_t kGroupBytes = 16ll << 20;
   const int64_t row_block_bytes = (int64_t)C::BM * K * 2;
   const int group_m = (int)std::max<int64_t>(1, std::min<int64_t>(tiles_m, kGroupBytes / row_block_bytes));
-  hipLaunchKernelGGL((gemm_bf16_kernel<C>), dim3((unsigned)tiles), dim3(C::kThreads), C::kLdsBytes, s,
+  // K range per split: a whole number of BK slices
+  const int64_t kchunk = part ? ((K + splits - 1) / splits + C::BK - 1) / C::BK * C::BK : K;
+  const int64_t nsplit = part ? (K + kchunk - 1) / kchunk : 1;
+  hipLaunchKernelGGL((gemm_bf16_kernel<C>), dim3((unsigned)(tiles * nsplit)), dim3(C::kThreads), C::kLdsBytes, s,
                      static_cast<const __bf16*>(x), static_cast<const __bf16*>(W),
                      static_cast<const __bf16*>(bias), static_cast<__bf16*>(y), (int)M, (int)N, (int)K,
-                     group_m);
+                     group_m, (int)kchunk, part);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess || !part) return e;
+  const int64_t MN = M * N;
+  const unsigned blocks = (unsigned)std::min<int64_t>(4096, (MN / 4 + 255) / 256);
+  hipLaunchKernelGGL(splitk_reduce_kernel, dim3(blocks), dim3(256), 0, s, part, (int)nsplit,
+                     static_cast<const __bf16*>(bias), static_cast<__bf16*>(y), MN, (int)N);
   return hipGetLastError();
+}
+
+// Split-K for small M: when at most half as many 256x128 tiles as CUs exist,
+// K is cut into floor(kNumCUs / tiles) ranges (each at least 512 wide), so
+// about kNumCUs workgroups run.  (A split that only lifts 129-255 tiles a
+// little past the CU count measured slower than no split.)  0: no split.
+static int splitk_count(int64_t M, int64_t N, int64_t K) {
+  if (M > kSplitKMaxM || K < 1024) return 0;
+  const int64_t tiles = ((M + 255) / 256) * ((N + 127) / 128);
+  const int64_t s = std::min<int64_t>(kNumCUs / tiles, K / 512);
+  return s >= 2 ? (int)s : 0;
 }
 
 hipError_t launch_linear(const void* x, const void* W, const void* bias, void* y, int64_t M,
@@ -375,6 +448,19 @@ hipError_t launch_linear(const void* x, const void* W, const void* bias, void* y
     const bool sk_on = sk && strcmp(sk, "1") == 0;
     if (!sk_off && (sk_on ? skinny_linear_supported(M, N, K) : skinny_linear_preferred(M, N, K)))
       return launch_linear_skinny(x, W, bias, y, M, N, K, s);
+    // Otherwise decode-sized M splits K over workgroups (fp32 partials in
+    // stream-ordered scratch, summed in split order by a second kernel).
+    // OPSCALE_GEMM_SPLITK=0 turns this off (tuning and tests).
+    const char* spk = getenv("OPSCALE_GEMM_SPLITK");
+    const int splits = (spk && strcmp(spk, "0") == 0) || getenv("OPSCALE_GEMM_TILE") ? 0 : splitk_count(M, N, K);
+    if (splits > 1) {
+      void* part = nullptr;
+      hipError_t e = scratch_alloc((size_t)splits * M * N * sizeof(float), s, &part);
+      if (e != hipSuccess) return e;
+      e = launch_gemm_bf16<CfgMid>(x, W, bias, y, M, N, K, s, splits, static_cast<float*>(part));
+      const hipError_t f = scratch_free(part, s);
+      return e != hipSuccess ? e : f;
+    }
     // One workgroup per CU at a time, so a launch runs in ceil(tiles / 256)
     // rounds.  Pick the tile whose rounds x tile area x relative per-element
     // cost is smallest: 256x256 moves the fewest operand bytes per flop,

@@ -120,12 +120,12 @@ bool skinny_linear_supported(int64_t M, int64_t N, int64_t K) {
 }
 
 // Measured on MI355X over the 8B-layer shapes at M = 1 ... 512 (cold caches):
-// this path wins at M <= 16 for every shape, and up to M = 256 wherever the
-// tiled GEMM has few 256x256 tiles to spread over the 256 CUs (QKV, O, down:
-// 16-24 tiles); with many tiles (gate-up: 112) the tiled GEMM wins from M = 32.
+// this path wins at M <= 16 for every shape, and at M <= 32 wherever the
+// tiled GEMM has few 256x256 tiles (QKV, O, down: 16-24); beyond that the
+// split-K tiled GEMM wins (and with many tiles, gate-up's 112, the plain one).
 bool skinny_linear_preferred(int64_t M, int64_t N, int64_t K) {
   const int64_t tiles = ((M + 255) / 256) * ((N + 255) / 256);
-  return skinny_linear_supported(M, N, K) && (M <= 16 || tiles < 64);
+  return skinny_linear_supported(M, N, K) && (M <= 16 || (M <= 32 && tiles < 64));
 }
 
 hipError_t launch_linear_skinny(const void* x, const void* W, const void* bias, void* y, int64_t M, int64_t N,

@@ -57,6 +57,11 @@ hipError_t launch_cache_write(const void* k, const void* v, int64_t kv_stride, v
 hipError_t launch_add_rmsnorm(const void* x, void* res, const void* w, void* y, int64_t M, int64_t H, float eps,
                               bool bf16, hipStream_t s);
 
+// Stream-ordered scratch from a per-device pool the library keeps (freed
+// memory is reused by later calls; nothing is returned to the driver).
+hipError_t scratch_alloc(size_t bytes, hipStream_t s, void** p);
+hipError_t scratch_free(void* p, hipStream_t s);
+
 // Reads `bytes` of `buf` through the caches (evicts L2 and the last-level
 // cache, leaving only clean lines, before a timed iteration).
 hipError_t launch_flush(void* buf, size_t bytes, hipStream_t s);

@@ -113,6 +113,29 @@ def test_linear_small_m(ops, monkeypatch, ng, M, N, K, bias):
     assert_close(f64(y.cpu()), oracle.linear(f64(x), f64(W), None if b is None else f64(b)), "bf16", "linear")
 
 
+@pytest.mark.parametrize("M,N,K,bias", [
+    (256, 6144, 4096, False), (100, 520, 1032, True), (17, 4096, 14336, False), (200, 1000, 2048, True),
+    (64, 8, 1024, False), (700, 4096, 4096, True),
+])
+def test_linear_split_k(ops, monkeypatch, M, N, K, bias):
+    """Decode-sized M with K split over workgroups (fp32 partials summed in
+    split order): ragged M, N and K, a K range that does not divide evenly,
+    bias; bitwise equal across calls."""
+    import torch
+    monkeypatch.delenv("OPSCALE_GEMM_TILE", raising=False)
+    monkeypatch.delenv("OPSCALE_GEMM_SPLITK", raising=False)
+    monkeypatch.setenv("OPSCALE_GEMM_SKINNY", "0")
+    say(f"linear bf16 split-K M={M} N={N} K={K} bias={bias}")
+    x = gen(25, "x", (M, K), "bf16")
+    W = gen(25, "w_qkv", (N, K), "bf16", std=0.02)
+    b = gen(25, "bias", (N,), "bf16") if bias else None
+    y = ops.opscale_linear(cuda(x), cuda(W), None if b is None else cuda(b))
+    y2 = ops.opscale_linear(cuda(x), cuda(W), None if b is None else cuda(b))
+    torch.cuda.synchronize()
+    assert torch.equal(y, y2)
+    assert_close(f64(y.cpu()), oracle.linear(f64(x), f64(W), None if b is None else f64(b)), "bf16", "linear")
+
+
 def test_linear_identity_weight(ops):
     """W = I (bf16-exact) returns x exactly: no accumulation rounding occurs."""
     import torch
