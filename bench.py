@@ -138,6 +138,29 @@ class Layer:
         self.res = wl.device_normal((self.p["M"], pc.hidden), pc.seed, "attn_out", "bf16")
         self.extra_names = ["rope", "reshape_and_cache", "add_rmsnorm"]
 
+    def decode_linears(self):
+        """The four projections of a decode step of the same layer at the
+        decode batch (one row per sequence): descriptors for opscale_op_profile."""
+        import workloads as wl
+        pc, dc, ops = self.pc, self.dc, self.ops
+        B = len(self.d["context_lens_host"])
+        H, F, HqD = pc.hidden, pc.ffn, pc.n_q_heads * pc.head_dim
+        bf = self.torch.bfloat16
+        e = lambda *s_: self.torch.empty(*s_, dtype=bf, device="cuda")
+        xs = {"h": wl.device_normal((B, H), dc.seed, "x", "bf16"),
+              "attn": wl.device_normal((B, HqD), dc.seed, "attn_out", "bf16"),
+              "act": wl.device_normal((B, F), dc.seed, "ffn_act", "bf16")}
+        p = self.p
+        plan = [("decode_qkv_linear", "h", p["w_qkv"]), ("decode_o_linear", "attn", p["w_o"]),
+                ("decode_gate_up_linear", "h", p["w_gate_up"]), ("decode_down_linear", "act", p["w_down"])]
+        self._dec_keep = [xs]
+        out = []
+        for name, xin, W in plan:
+            y = e(B, W.shape[0])
+            self._dec_keep.append(y)
+            out.append((name, ops.desc_linear(xs[xin], W, y), B))
+        return out
+
     def extra(self, i):
         ops, pc = self.ops, self.pc
         if i == 0:
@@ -353,6 +376,16 @@ def main():
         t_s = us * 1e-6
         extra_ops[nm] = {"us": round(us, 2), unit: round(units / t_s, 1), "gbps": round(by / t_s * 1e-9, 1),
                          "bound": bound, "roofline_frac": round(by / t_s / PEAK_HBM, 4)}
+    # The decode step's projections at the decode batch (256 rows), each timed
+    # cold (after a read of 512 MB evicts L2 and the last-level cache: the
+    # layer's weights were last read a whole model step earlier).
+    flush = torch.empty(512 << 20, dtype=torch.uint8, device="cuda")
+    for nm, desc, B in layer.decode_linears():
+        pr = ops.opscale_op_profile(desc, a.warmup, a.steps, flush)
+        extra_ops[nm] = {"us": round(pr.us_median, 2), "tokens/s": round(B / (pr.us_median * 1e-6), 1),
+                         "tflops": round(pr.tflops, 1), "gbps": round(pr.gbps, 1),
+                         "bound": "mfma+hbm", "roofline_frac": round(pr.roofline_frac, 4)}
+    del flush
     M = layer.p["M"]
     out = {
         "metric": "per-operator prefill tokens/s + % of MFMA/HBM roofline, Llama-8B-shaped layer",
