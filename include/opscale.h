@@ -232,7 +232,8 @@ typedef enum {
   OPSCALE_OP_ATTN_DECODE = 4,
   OPSCALE_OP_ROPE = 5,
   OPSCALE_OP_RESHAPE_AND_CACHE = 6,
-  OPSCALE_OP_ADD_RMSNORM = 7
+  OPSCALE_OP_ADD_RMSNORM = 7,
+  OPSCALE_OP_FUSED_MOE = 8
 } opscale_op;
 
 /* One operator call: the argument list of the matching entry point. */
@@ -263,6 +264,10 @@ typedef struct {
       int64_t T; int32_t Hkv, D, block_size; int64_t num_blocks;
     } reshape_and_cache;
     struct { const void* x; void* residual; const void* w; void* y; int64_t M, H; float eps; } add_rmsnorm;
+    struct {
+      const void *x, *w1, *w2; const int32_t* topk_ids; const float* topk_weights; void* out;
+      int64_t T; int32_t H, F, E, topk; void* workspace; size_t workspace_bytes;
+    } fused_moe;
   } u;
 } opscale_op_desc;
 
@@ -294,6 +299,53 @@ typedef struct {
 opscale_status opscale_op_profile(const opscale_op_desc* desc, int32_t warmup, int32_t iters,
                                   void* flush_buf, size_t flush_bytes, hipStream_t stream,
                                   opscale_profile* out);
+
+/* ---------------------------------------------------------------------------
+ * Mixture-of-experts FFN (the FusedMoE operator of the paper's MoE models,
+ * Qwen2-57B-A14B and Mixtral-8x7B: Table 3; Section 2.1 counts it among the
+ * compute-heavy linear operators, Appendix D shows it dominating at short
+ * sequences).
+ * ------------------------------------------------------------------------- */
+
+/*
+ * Top-k routing: for each of T tokens, the topk experts with the largest
+ * logits (logits: DEVICE fp32 [T, E], finite), listed by decreasing logit,
+ * the lower expert index first among equal logits; topk_weights[t, j] is the
+ * softmax of the token's E logits at expert topk_ids[t, j] (fp32), divided by
+ * the sum over the topk picks when renormalize != 0.  topk_ids: DEVICE int32
+ * [T, topk]; topk_weights: DEVICE fp32 [T, topk].
+ * 1 <= E <= 1024, 1 <= topk <= min(E, 16).
+ */
+opscale_status opscale_moe_topk(const float* logits, int32_t* topk_ids, float* topk_weights, int64_t T,
+                                int32_t E, int32_t topk, int32_t renormalize, hipStream_t stream,
+                                opscale_timing* timing);
+
+/* Bytes of device workspace opscale_fused_moe needs for these sizes. */
+size_t opscale_fused_moe_workspace_size(int64_t T, int32_t H, int32_t F, int32_t E, int32_t topk);
+
+/*
+ * The routed expert MLPs:
+ *   out[t] = sum_j topk_weights[t, j] * W2[e] (silu(W1g[e] x[t]) * (W1u[e] x[t])),
+ *   e = topk_ids[t, j],
+ * with W1[e] = [W1g; W1u] ([2F, H]: the F gate rows first, as in the dense
+ * gate-up linear) and W2[e] [H, F].  x: [T, H]; w1: [E, 2F, H]; w2: [E, H, F];
+ * out: [T, H] (bf16, must not overlap x); topk_ids: DEVICE int32 [T, topk]
+ * (an id outside [0, E) contributes nothing); topk_weights: DEVICE fp32
+ * [T, topk].  bf16 only (OPSCALE_ERR_UNSUPPORTED otherwise); H and F
+ * multiples of 8; 1 <= E <= 1024; 1 <= topk <= 64; T * H and
+ * T * topk * 2F below 2^30 (else OPSCALE_ERR_UNSUPPORTED).
+ * The token-expert pairs are sorted by expert (stable) and each expert's rows
+ * run through two grouped GEMMs (gate-up with the SwiGLU, then down, rounded
+ * to bf16 as the dense layer's intermediates are); the topk results of a
+ * token are summed in fp32 in slot order.  Deterministic.
+ * workspace: DEVICE, at least opscale_fused_moe_workspace_size(...) bytes,
+ * 16-byte aligned, else OPSCALE_ERR_WORKSPACE; calls sharing one must be
+ * stream-ordered.
+ */
+opscale_status opscale_fused_moe(const void* x, const void* w1, const void* w2, const int32_t* topk_ids,
+                                 const float* topk_weights, void* out, int64_t T, int32_t H, int32_t F,
+                                 int32_t E, int32_t topk, opscale_dtype dt, void* workspace,
+                                 size_t workspace_bytes, hipStream_t stream, opscale_timing* timing);
 
 /* ---------------------------------------------------------------------------
  * Spatial sharing: operators on disjoint sets of compute units.

@@ -12,7 +12,8 @@ them in a full layer (rotary embedding, the paged KV-cache write, the residual
 add before each norm), evaluated in fp64 with no
 tiling, no online softmax and no split of the key range.  See `ops` for the
 per-function citations, `cost` for the algorithmic flop/byte closed forms and
-`spatial` for CU shares and the interference factor of Eq. 5.
+`spatial` for CU shares and the interference factor of Eq. 5, `moe` for
+top-k routing and the fused mixture-of-experts MLP.
 
 Parity status: every function here is pinned by brute force, closed forms or
 invariants in the CPU tests (tests/test_oracle_pins.py); none is "parity
@@ -25,3 +26,4 @@ from .ops import (  # noqa: F401
 )
 from . import cost  # noqa: F401
 from . import spatial  # noqa: F401
+from . import moe  # noqa: F401

@@ -17,7 +17,7 @@ LIB_PATH = os.path.join(_HERE, "libopscale.so")
 OPSCALE_OK, OPSCALE_ERR_INVALID_ARG, OPSCALE_ERR_UNSUPPORTED, OPSCALE_ERR_WORKSPACE, OPSCALE_ERR_HIP = range(5)
 OPSCALE_F32, OPSCALE_BF16 = 0, 1
 (OP_RMSNORM, OP_LINEAR, OP_SWIGLU, OP_ATTN_PREFILL, OP_ATTN_DECODE, OP_ROPE, OP_RESHAPE_AND_CACHE,
- OP_ADD_RMSNORM) = range(8)
+ OP_ADD_RMSNORM, OP_FUSED_MOE) = range(9)
 
 c_i32, c_i64, c_f32, c_f64, c_vp, c_sz = (ctypes.c_int32, ctypes.c_int64, ctypes.c_float,
                                           ctypes.c_double, ctypes.c_void_p, ctypes.c_size_t)
@@ -75,10 +75,17 @@ class _AddRmsnormArgs(ctypes.Structure):
                 ("eps", c_f32)]
 
 
+class _FusedMoeArgs(ctypes.Structure):
+    _fields_ = [("x", c_vp), ("w1", c_vp), ("w2", c_vp), ("topk_ids", c_vp), ("topk_weights", c_vp), ("out", c_vp),
+                ("T", c_i64), ("H", c_i32), ("F", c_i32), ("E", c_i32), ("topk", c_i32), ("workspace", c_vp),
+                ("workspace_bytes", c_sz)]
+
+
 class _OpUnion(ctypes.Union):
     _fields_ = [("rmsnorm", _RmsnormArgs), ("linear", _LinearArgs), ("swiglu", _SwigluArgs),
                 ("attn_prefill", _PrefillArgs), ("attn_decode", _DecodeArgs), ("rope", _RopeArgs),
-                ("reshape_and_cache", _CacheWriteArgs), ("add_rmsnorm", _AddRmsnormArgs)]
+                ("reshape_and_cache", _CacheWriteArgs), ("add_rmsnorm", _AddRmsnormArgs),
+                ("fused_moe", _FusedMoeArgs)]
 
 
 class OpDesc(ctypes.Structure):
@@ -134,6 +141,10 @@ EXPORTS = {
                                           c_i32, c_vp, ctypes.POINTER(Timing)]),
     "opscale_add_rmsnorm": (c_i32, [c_vp, c_vp, c_vp, c_vp, c_i64, c_i64, c_f32, c_i32, c_vp,
                                     ctypes.POINTER(Timing)]),
+    "opscale_moe_topk": (c_i32, [c_vp, c_vp, c_vp, c_i64, c_i32, c_i32, c_i32, c_vp, ctypes.POINTER(Timing)]),
+    "opscale_fused_moe_workspace_size": (c_sz, [c_i64, c_i32, c_i32, c_i32, c_i32]),
+    "opscale_fused_moe": (c_i32, [c_vp, c_vp, c_vp, c_vp, c_vp, c_vp, c_i64, c_i32, c_i32, c_i32, c_i32, c_i32,
+                                  c_vp, c_sz, c_vp, ctypes.POINTER(Timing)]),
     "opscale_cu_layout": (c_i32, [ctypes.POINTER(c_i32)] * 3),
     "opscale_cu_mask_build": (c_i32, [c_i32, c_i32, c_i32, c_i32, c_i32, ctypes.POINTER(ctypes.c_uint32), c_i32]),
     "opscale_cu_stream_create": (c_i32, [ctypes.POINTER(ctypes.c_uint32), c_i32, ctypes.POINTER(c_vp)]),
@@ -404,6 +415,59 @@ def opscale_op_profile(desc: OpDesc, warmup: int = 5, iters: int = 20, flush=Non
     _check(lib.opscale_op_profile(ctypes.byref(desc), warmup, iters, _ptr(flush), nbytes,
                                   _stream(stream), ctypes.byref(p)))
     return p
+
+
+# ------------------------------------------------------- mixture of experts --
+def opscale_moe_topk(logits, topk: int, renormalize: bool = False, ids=None, weights=None, stream=None,
+                     timed: bool = False):
+    """Top-k routing of fp32 logits [T, E]: (ids int32 [T, topk], weights fp32 [T, topk])."""
+    import torch
+    _dev(logits)
+    if logits.dtype != torch.float32 or logits.dim() != 2 or not logits.is_contiguous():
+        raise OpscaleError(OPSCALE_ERR_INVALID_ARG, "logits must be a contiguous float32 [T, E] tensor")
+    T, E = logits.shape
+    ids = torch.empty(T, topk, dtype=torch.int32, device=logits.device) if ids is None else ids
+    weights = torch.empty(T, topk, dtype=torch.float32, device=logits.device) if weights is None else weights
+    t = Timing() if timed else None
+    _check(load().opscale_moe_topk(_ptr(logits), _ptr(ids), _ptr(weights), T, E, topk, int(renormalize),
+                                   _stream(stream), ctypes.byref(t) if t else None))
+    return (ids, weights, t) if timed else (ids, weights)
+
+
+def opscale_fused_moe_workspace_size(T: int, H: int, F: int, E: int, topk: int) -> int:
+    return int(load().opscale_fused_moe_workspace_size(T, H, F, E, topk))
+
+
+def opscale_fused_moe(x, w1, w2, topk_ids, topk_weights, out=None, workspace=None, stream=None, timed: bool = False):
+    """out[t] = sum_j w[t, j] * MLP_e(x[t]) over the routed experts; x [T, H] bf16,
+    w1 [E, 2F, H], w2 [E, H, F]; topk_ids int32 / topk_weights fp32 [T, topk]."""
+    import torch
+    _dev(x, w1, w2, topk_ids, topk_weights)
+    for name, t_ in (("x", x), ("w1", w1), ("w2", w2), ("topk_ids", topk_ids), ("topk_weights", topk_weights)):
+        _contig(name, t_)
+    T, H = x.shape
+    E, F2, _ = w1.shape
+    topk = topk_ids.shape[1]
+    out = torch.empty_like(x) if out is None else out
+    need = opscale_fused_moe_workspace_size(T, H, F2 // 2, E, topk)
+    if workspace is None:
+        workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=x.device)
+    t = Timing() if timed else None
+    _check(load().opscale_fused_moe(_ptr(x), _ptr(w1), _ptr(w2), _ptr(topk_ids), _ptr(topk_weights), _ptr(out), T,
+                                    H, F2 // 2, E, topk, _dt(x), _ptr(workspace),
+                                    workspace.numel() * workspace.element_size(), _stream(stream),
+                                    ctypes.byref(t) if t else None))
+    return (out, t) if timed else out
+
+
+def desc_fused_moe(x, w1, w2, topk_ids, topk_weights, out, workspace) -> OpDesc:
+    d = OpDesc(op=OP_FUSED_MOE, dt=_dt(x))
+    T, H = x.shape
+    E, F2, _ = w1.shape
+    d.u.fused_moe = _FusedMoeArgs(_ptr(x), _ptr(w1), _ptr(w2), _ptr(topk_ids), _ptr(topk_weights), _ptr(out), T, H,
+                                  F2 // 2, E, topk_ids.shape[1], _ptr(workspace),
+                                  workspace.numel() * workspace.element_size())
+    return d
 
 
 # ---------------------------------------------------------- spatial sharing --

@@ -149,6 +149,25 @@ Work work_add_rmsnorm(int64_t M, int64_t H, int s) {
   return {5.0 * M * H, (double)s * (4.0 * M * H + H), s * H, s * 4 * M * H, s * 2 * M * H};
 }
 
+// MoE: each valid (token, slot) pair does the two expert GEMMs (2 H 2F + 2 F H
+// flops, 6 H F) and the SwiGLU (6 F); x and out are read / written once and
+// the weights of every expert that receives a token are read once.
+Work work_fused_moe(const std::vector<int32_t>& ids, int64_t T, int64_t H, int64_t F, int64_t E, int s) {
+  std::vector<char> used((size_t)E, 0);
+  double pairs = 0;
+  for (int32_t e : ids)
+    if (e >= 0 && e < E) {
+      used[(size_t)e] = 1;
+      pairs += 1;
+    }
+  int64_t experts = 0;
+  for (char u : used) experts += u;
+  const int64_t weight = (int64_t)s * experts * 3 * H * F;
+  const double by = (double)weight + 2.0 * s * T * H + 8.0 * (double)ids.size();
+  return {pairs * (6.0 * H * F + 6.0 * F), by, weight, (int64_t)s * T * H + 8 * (int64_t)ids.size(),
+          (int64_t)s * T * H};
+}
+
 opscale_status copy_ints(std::vector<int32_t>& dst, const int32_t* src, int64_t n, hipStream_t s) {
   dst.resize((size_t)n);
   if (n == 0) return OPSCALE_OK;
@@ -323,6 +342,46 @@ opscale_status check_add_rmsnorm(const void* x, void* res, const void* w, void* 
   const int64_t nb = M * H * esize(dt);
   if (overlap(res, nb, x, nb) || overlap(res, nb, y, nb) || overlap(res, nb, w, H * esize(dt)))
     return fail(OPSCALE_ERR_INVALID_ARG, "add_rmsnorm: residual must not overlap x, y or w");
+  return OPSCALE_OK;
+}
+
+opscale_status check_moe_topk(const float* logits, int32_t* ids, float* wts, int64_t T, int32_t E, int32_t k) {
+  if (T < 0 || T >= kMaxDim) return fail(OPSCALE_ERR_INVALID_ARG, "moe_topk: bad T=%lld", (long long)T);
+  if (E < 1 || E > opscale::moe_max_experts())
+    return fail(OPSCALE_ERR_INVALID_ARG, "moe_topk: E=%d outside [1, %d]", E, opscale::moe_max_experts());
+  if (k < 1 || k > std::min<int32_t>(E, 16))
+    return fail(OPSCALE_ERR_INVALID_ARG, "moe_topk: topk=%d outside [1, min(E, 16)]", k);
+  if (T == 0) return OPSCALE_OK;
+  if (!logits || !ids || !wts) return fail(OPSCALE_ERR_INVALID_ARG, "moe_topk: null pointer");
+  if ((reinterpret_cast<uintptr_t>(logits) | reinterpret_cast<uintptr_t>(ids) | reinterpret_cast<uintptr_t>(wts)) & 3)
+    return fail(OPSCALE_ERR_INVALID_ARG, "moe_topk: pointers must be 4-byte aligned");
+  return OPSCALE_OK;
+}
+
+opscale_status check_fused_moe(const void* x, const void* w1, const void* w2, const int32_t* ids, const float* wts,
+                               void* out, int64_t T, int32_t H, int32_t F, int32_t E, int32_t k, opscale_dtype dt,
+                               void* ws, size_t ws_bytes) {
+  if (!dtype_ok(dt)) return fail(OPSCALE_ERR_INVALID_ARG, "fused_moe: unknown dtype %d", (int)dt);
+  if (dt != OPSCALE_BF16) return fail(OPSCALE_ERR_UNSUPPORTED, "fused_moe: bf16 only");
+  if (T < 0 || H < 8 || F < 8 || H % 8 || F % 8)
+    return fail(OPSCALE_ERR_INVALID_ARG, "fused_moe: bad sizes T=%lld H=%d F=%d (H, F multiples of 8)",
+                (long long)T, H, F);
+  if (E < 1 || E > opscale::moe_max_experts())
+    return fail(OPSCALE_ERR_INVALID_ARG, "fused_moe: E=%d outside [1, %d]", E, opscale::moe_max_experts());
+  if (k < 1 || k > 64) return fail(OPSCALE_ERR_INVALID_ARG, "fused_moe: topk=%d outside [1, 64]", k);
+  if (T * H >= (1ll << 30) || T * k * 2ll * F >= (1ll << 30))
+    return fail(OPSCALE_ERR_UNSUPPORTED, "fused_moe: T*H and T*topk*2F must stay below 2^30");
+  if (T == 0) return OPSCALE_OK;
+  if (!x || !w1 || !w2 || !ids || !wts || !out || !ws) return fail(OPSCALE_ERR_INVALID_ARG, "fused_moe: null pointer");
+  if (!aligned16(x) || !aligned16(w1) || !aligned16(w2) || !aligned16(out) || !aligned16(ws))
+    return fail(OPSCALE_ERR_INVALID_ARG, "fused_moe: x, w1, w2, out and workspace must be 16-byte aligned");
+  if ((reinterpret_cast<uintptr_t>(ids) | reinterpret_cast<uintptr_t>(wts)) & 3)
+    return fail(OPSCALE_ERR_INVALID_ARG, "fused_moe: topk_ids and topk_weights must be 4-byte aligned");
+  if (overlap(out, T * H * 2, x, T * H * 2))
+    return fail(OPSCALE_ERR_INVALID_ARG, "fused_moe: out must not overlap x");
+  const size_t need = opscale::moe_workspace_bytes(T, H, F, E, k);
+  if (ws_bytes < need)
+    return fail(OPSCALE_ERR_WORKSPACE, "fused_moe: workspace of %zu bytes, %zu needed", ws_bytes, need);
   return OPSCALE_OK;
 }
 
@@ -562,6 +621,49 @@ opscale_status opscale_add_rmsnorm(const void* x, void* residual, const void* w,
   return st;
 }
 
+opscale_status opscale_moe_topk(const float* logits, int32_t* topk_ids, float* topk_weights, int64_t T, int32_t E,
+                                int32_t topk, int32_t renormalize, hipStream_t stream, opscale_timing* timing) {
+  opscale_status st = check_moe_topk(logits, topk_ids, topk_weights, T, E, topk);
+  if (st != OPSCALE_OK) return st;
+  zero_timing(timing);
+  if (T == 0) return OPSCALE_OK;
+  st = run_timed(stream, timing, "moe_topk launch", [&] {
+    return opscale::launch_moe_topk(logits, topk_ids, topk_weights, T, E, topk, renormalize != 0, stream);
+  });
+  if (st == OPSCALE_OK && timing) {
+    timing->alg_flops = 3.0 * T * E;
+    timing->alg_bytes = 4.0 * T * E + 8.0 * T * topk;
+  }
+  return st;
+}
+
+size_t opscale_fused_moe_workspace_size(int64_t T, int32_t H, int32_t F, int32_t E, int32_t topk) {
+  return opscale::moe_workspace_bytes(std::max<int64_t>(0, T), std::max(0, H), std::max(0, F), std::max(1, E),
+                                      std::max(1, topk));
+}
+
+opscale_status opscale_fused_moe(const void* x, const void* w1, const void* w2, const int32_t* topk_ids,
+                                 const float* topk_weights, void* out, int64_t T, int32_t H, int32_t F, int32_t E,
+                                 int32_t topk, opscale_dtype dt, void* workspace, size_t workspace_bytes,
+                                 hipStream_t stream, opscale_timing* timing) {
+  opscale_status st = check_fused_moe(x, w1, w2, topk_ids, topk_weights, out, T, H, F, E, topk, dt, workspace,
+                                      workspace_bytes);
+  if (st != OPSCALE_OK) return st;
+  zero_timing(timing);
+  if (T == 0) return OPSCALE_OK;
+  st = run_timed(stream, timing, "fused_moe launch", [&] {
+    return opscale::launch_fused_moe(x, w1, w2, topk_ids, topk_weights, out, T, H, F, E, topk, workspace, stream);
+  });
+  if (st == OPSCALE_OK && timing) {
+    std::vector<int32_t> ids;
+    if ((st = copy_ints(ids, topk_ids, T * topk, stream)) != OPSCALE_OK) return st;
+    const Work wk = work_fused_moe(ids, T, H, F, E, 2);
+    timing->alg_flops = wk.flops;
+    timing->alg_bytes = wk.bytes;
+  }
+  return st;
+}
+
 }  // extern "C"
 
 namespace {
@@ -671,6 +773,22 @@ opscale_status prepare_op(const opscale_op_desc* d, hipStream_t stream, const ch
       if (a.M == 0) return fail(OPSCALE_ERR_INVALID_ARG, "%s: empty problem", who);
       launch = [=] { return opscale::launch_add_rmsnorm(a.x, a.residual, a.w, a.y, a.M, a.H, a.eps, bf16, stream); };
       wk = work_add_rmsnorm(a.M, a.H, esize(dt));
+      break;
+    }
+    case OPSCALE_OP_FUSED_MOE: {
+      const auto& a = d->u.fused_moe;
+      st = check_fused_moe(a.x, a.w1, a.w2, a.topk_ids, a.topk_weights, a.out, a.T, a.H, a.F, a.E, a.topk, dt,
+                           a.workspace, a.workspace_bytes);
+      if (st != OPSCALE_OK) return st;
+      if (a.T == 0) return fail(OPSCALE_ERR_INVALID_ARG, "%s: empty problem", who);
+      launch = [=] {
+        return opscale::launch_fused_moe(a.x, a.w1, a.w2, a.topk_ids, a.topk_weights, a.out, a.T, a.H, a.F, a.E,
+                                         a.topk, a.workspace, stream);
+      };
+      std::vector<int32_t> ids;
+      st = copy_ints(ids, a.topk_ids, a.T * a.topk, stream);
+      if (st != OPSCALE_OK) return st;
+      wk = work_fused_moe(ids, a.T, a.H, a.F, a.E, 2);
       break;
     }
     default:

@@ -81,9 +81,14 @@ __device__ __forceinline__ void wait_vmcnt() {
 // based at the tile's first row) into an LDS stage region.  Wave w issues
 // loads w, w + waves, ...; lane p of a load writes LDS bytes [p*16, p*16+16)
 // of its 1 KB group: row p / CPR, physical chunk p % CPR.
+// A row that must read as zeros (past the end of a grouped operand).
+constexpr uint32_t kNoRow = 0xffffffffu;
+
+// row_off[g]: byte offset of the row this lane loads in its g-th load group
+// (kNoRow: a row that reads as zeros).
 template <class C, int ROWS>
-__device__ __forceinline__ void load_slice(__amdgpu_buffer_rsrc_t rsrc, OPS_LDS char* lds, int ld, int K,
-                                           int k0, int wave, int lane) {
+__device__ __forceinline__ void load_slice(__amdgpu_buffer_rsrc_t rsrc, OPS_LDS char* lds, const uint32_t* row_off,
+                                           int K, int k0, int wave, int lane) {
   const int rl = lane / C::kCPR, pc = lane % C::kCPR;
   constexpr int kPerWave = ROWS / C::kRowsPerLoad / C::kWaves;
 #pragma unroll
@@ -92,7 +97,7 @@ __device__ __forceinline__ void load_slice(__amdgpu_buffer_rsrc_t rsrc, OPS_LDS 
     const int r = grp * C::kRowsPerLoad + rl;
     const int c = pc ^ swz<C::kCPR>(r);
     const int k = k0 + c * 8;
-    const uint32_t voff = k < K ? (uint32_t)(((int64_t)r * ld + k) * 2) : kOobOffset;
+    const uint32_t voff = (k < K && row_off[g] != kNoRow) ? row_off[g] + (uint32_t)k * 2u : kOobOffset;
     buffer_load16_lds(rsrc, lds + grp * 1024, voff);
   }
 }
@@ -107,45 +112,98 @@ __device__ __forceinline__ bf16x8 lds_frag(const OPS_LDS char* p) {
 // Split-K (splits > 1): workgroup blockIdx.x / tiles takes the K range
 // [split * kchunk, (split + 1) * kchunk) and writes its fp32 partial tile to
 // part[split][M][N] (no bias); a second kernel sums the splits in order.
-template <class C>
+//
+// GROUPED (one GEMM per expert of a mixture-of-experts layer): the output
+// rows are grouped by expert, expert e owning rows [rows[e], rows[e + 1]) in
+// tiles tiles[e] .. tiles[e + 1] - 1 of BM rows; workgroup (tile t, column
+// block n) multiplies by W + e * w_stride, and output row m reads x row
+// gather[m] (m itself when gather is null).  x then has x_rows rows.
+struct GroupedGemm {
+  const int32_t* gather;  // output row -> x row (null: the identity)
+  const int32_t* rows;    // [E + 1]
+  const int32_t* tiles;   // [E + 1]
+  int E;
+  int x_rows;
+  int64_t w_stride;       // elements from one expert's W to the next
+};
+
+template <class C, bool GROUPED = false>
 __global__ __launch_bounds__(C::kThreads, 1) void gemm_bf16_kernel(const __bf16* __restrict__ x,
                                                                    const __bf16* __restrict__ W,
                                                                    const __bf16* __restrict__ bias,
                                                                    __bf16* __restrict__ y, int M, int N,
                                                                    int K_total, int group_m, int kchunk,
-                                                                   float* __restrict__ part) {
+                                                                   float* __restrict__ part, GroupedGemm gg) {
   extern __shared__ __attribute__((aligned(16))) char smem_raw[];
   OPS_LDS char* smem = (OPS_LDS char*)smem_raw;
   constexpr int BM = C::BM, BN = C::BN, BK = C::BK, WM = C::WM, WN = C::WN, S = C::STAGES;
   constexpr int TM = WM / 32, TN = WN / 32;  // 32x32 MFMA tiles per wave
 
-  const int tiles_m = (M + BM - 1) / BM, tiles_n = (N + BN - 1) / BN;
-  const int tiles = tiles_m * tiles_n;
-  const int split = blockIdx.x / tiles;
-  const uint32_t tid = xcd_remap(blockIdx.x - split * tiles, (uint32_t)tiles);
-  // this workgroup's K range: K elements starting at k_begin, rows ld apart
+  const int tiles_n = (N + BN - 1) / BN;
   const int ld = K_total;
+  int m0, n0, m_rows, split = 0;
+  if constexpr (GROUPED) {
+    // tile-row t of the expert list, column block n; experts by bisection
+    const int t = blockIdx.x / tiles_n;
+    n0 = (blockIdx.x - t * tiles_n) * BN;
+    if (t >= gg.tiles[gg.E]) return;
+    int lo = 0, hi = gg.E;  // gg.tiles[lo] <= t < gg.tiles[hi]
+    while (hi - lo > 1) {
+      const int mid = (lo + hi) >> 1;
+      if (gg.tiles[mid] <= t) lo = mid;
+      else hi = mid;
+    }
+    m0 = gg.rows[lo] + (t - gg.tiles[lo]) * BM;
+    m_rows = min(BM, gg.rows[lo + 1] - m0);
+    W += lo * gg.w_stride;
+  } else {
+    const int tiles_m = (M + BM - 1) / BM;
+    const int tiles = tiles_m * tiles_n;
+    split = blockIdx.x / tiles;
+    const uint32_t tid = xcd_remap(blockIdx.x - split * tiles, (uint32_t)tiles);
+    // grouped order: group_m tile-rows sweep the tile-columns together, so a
+    // W column-block is fetched once per group and reused from L2 / MALL by
+    // every tile-row of the group while the group's x rows stay cache resident
+    const int group = tid / (group_m * tiles_n);
+    const int first_m = group * group_m;
+    const int gsize = min(tiles_m - first_m, group_m);
+    const int in_group = tid % (group_m * tiles_n);
+    const int tm = first_m + in_group % gsize, tn = in_group / gsize;
+    m0 = tm * BM;
+    n0 = tn * BN;
+    m_rows = min(BM, M - m0);
+  }
+  // this workgroup's K range: K elements starting at k_begin, rows ld apart
   const int k_begin = split * kchunk;
   const int K = min(K_total - k_begin, kchunk);
-  // grouped order: group_m tile-rows sweep the tile-columns together, so a
-  // W column-block is fetched once per group and reused from L2 / MALL by
-  // every tile-row of the group while the group's x rows stay cache resident
-  const int group = tid / (group_m * tiles_n);
-  const int first_m = group * group_m;
-  const int gsize = min(tiles_m - first_m, group_m);
-  const int in_group = tid % (group_m * tiles_n);
-  const int tm = first_m + in_group % gsize, tn = in_group / gsize;
-  const int m0 = tm * BM, n0 = tn * BN;
 
   // wave index as a scalar: the LDS destinations of the loads are then
   // wave-uniform without a readfirstlane per load
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
   const int wm = wave % C::WGM, wn = wave / C::WGM;
 
-  const __amdgpu_buffer_rsrc_t xr = make_rsrc(x + (int64_t)m0 * ld + k_begin,
-                                              (uint32_t)(((int64_t)(min(BM, M - m0) - 1) * ld + K) * 2));
+  // x: the tile's rows (grouped: the gathered rows of the whole operand)
+  const __amdgpu_buffer_rsrc_t xr =
+      GROUPED ? make_rsrc(x + k_begin, (uint32_t)(((int64_t)gg.x_rows - 1) * ld * 2 + (int64_t)K * 2))
+              : make_rsrc(x + (int64_t)m0 * ld + k_begin, (uint32_t)(((int64_t)(m_rows - 1) * ld + K) * 2));
   const __amdgpu_buffer_rsrc_t wr = make_rsrc(W + (int64_t)n0 * ld + k_begin,
                                               (uint32_t)(((int64_t)(min(BN, N - n0) - 1) * ld + K) * 2));
+  // byte offsets of the rows this lane loads (per load group)
+  constexpr int LX = BM / C::kRowsPerLoad / C::kWaves, LW = BN / C::kRowsPerLoad / C::kWaves;
+  uint32_t xro[LX], wro[LW];
+#pragma unroll
+  for (int g = 0; g < LX; ++g) {
+    const int r = (g * C::kWaves + wave) * C::kRowsPerLoad + lane / C::kCPR;
+    if constexpr (GROUPED) {
+      const int src = r < m_rows ? (gg.gather ? gg.gather[m0 + r] : m0 + r) : -1;
+      xro[g] = src >= 0 ? (uint32_t)((int64_t)src * ld * 2) : kNoRow;
+    } else {
+      xro[g] = (uint32_t)((int64_t)r * ld * 2);
+    }
+  }
+#pragma unroll
+  for (int g = 0; g < LW; ++g)
+    wro[g] = (uint32_t)((int64_t)((g * C::kWaves + wave) * C::kRowsPerLoad + lane / C::kCPR) * ld * 2);
 
   f32x16 acc[TN][TM];
 #pragma unroll
@@ -157,8 +215,8 @@ __global__ __launch_bounds__(C::kThreads, 1) void gemm_bf16_kernel(const __bf16*
   auto stage_x = [&](int s) { return smem + s * C::kStageBytes; };
   auto stage_w = [&](int s) { return smem + s * C::kStageBytes + BM * C::kRowBytes; };
   auto load = [&](int kt) {
-    load_slice<C, BM>(xr, stage_x(kt % S), ld, K, kt * BK, wave, lane);
-    load_slice<C, BN>(wr, stage_w(kt % S), ld, K, kt * BK, wave, lane);
+    load_slice<C, BM>(xr, stage_x(kt % S), xro, K, kt * BK, wave, lane);
+    load_slice<C, BN>(wr, stage_w(kt % S), wro, K, kt * BK, wave, lane);
   };
 
 #pragma unroll
@@ -187,7 +245,7 @@ __global__ __launch_bounds__(C::kThreads, 1) void gemm_bf16_kernel(const __bf16*
   // Past the last slice the loads are out of range (they read zeros) and go
   // to the stage no wave reads any more.
   auto mfmas_loading = [&](int buf, int kt) {
-    constexpr int MF = TN * TM, L = C::kLoadsPerTile, LX = BM / C::kRowsPerLoad / C::kWaves;
+    constexpr int MF = TN * TM, L = C::kLoadsPerTile;
     OPS_LDS char* dst = smem + ((kt + 1 < nk ? kt : kt + 1) & 1) * C::kStageBytes;
     const int rl = lane / C::kCPR, pc = lane % C::kCPR;
     const int k0 = (kt + 2) * BK;
@@ -204,7 +262,8 @@ __global__ __launch_bounds__(C::kThreads, 1) void gemm_bf16_kernel(const __bf16*
         const int grp = (isx ? q : q - LX) * C::kWaves + wave;
         const int r = grp * C::kRowsPerLoad + rl;
         const int k = k0 + ((pc ^ swz<C::kCPR>(r)) << 3);
-        const uint32_t voff = (more && k < K) ? (uint32_t)(((int64_t)r * ld + k) * 2) : kOobOffset;
+        const uint32_t ro = isx ? xro[q < LX ? q : 0] : wro[q >= LX ? q - LX : 0];
+        const uint32_t voff = (more && k < K && ro != kNoRow) ? ro + (uint32_t)k * 2u : kOobOffset;
         buffer_load16_lds(isx ? xr : wr, dst + (isx ? 0 : BM * C::kRowBytes) + grp * 1024, voff);
         __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
       }
@@ -280,7 +339,7 @@ __global__ __launch_bounds__(C::kThreads, 1) void gemm_bf16_kernel(const __bf16*
 #pragma unroll
     for (int j = 0; j < TM; ++j) {
       const int m = m0 + wm * WM + j * 32 + fr;
-      if (m >= M) continue;
+      if (m - m0 >= m_rows) continue;
 #pragma unroll
       for (int i = 0; i < TN; ++i)
 #pragma unroll
@@ -296,7 +355,7 @@ __global__ __launch_bounds__(C::kThreads, 1) void gemm_bf16_kernel(const __bf16*
 #pragma unroll
   for (int j = 0; j < TM; ++j) {
     const int m = m0 + wm * WM + j * 32 + fr;
-    if (m >= M) continue;
+    if (m - m0 >= m_rows) continue;
     __bf16* yrow = y + (int64_t)m * N;
 #pragma unroll
     for (int i = 0; i < TN; ++i) {
@@ -413,7 +472,7 @@ static hipError_t launch_gemm_bf16(const void* x, const void* W, const void* bia
   hipLaunchKernelGGL((gemm_bf16_kernel<C>), dim3((unsigned)(tiles * nsplit)), dim3(C::kThreads), C::kLdsBytes, s,
                      static_cast<const __bf16*>(x), static_cast<const __bf16*>(W),
                      static_cast<const __bf16*>(bias), static_cast<__bf16*>(y), (int)M, (int)N, (int)K,
-                     group_m, (int)kchunk, part);
+                     group_m, (int)kchunk, part, GroupedGemm{});
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || !part) return e;
   const int64_t MN = M * N;
@@ -433,6 +492,26 @@ static int splitk_count(int64_t M, int64_t N, int64_t K) {
   const int64_t s = std::min<int64_t>(kNumCUs / tiles, K / 512);
   return s >= 2 ? (int)s : 0;
 }
+
+hipError_t launch_gemm_grouped(const void* x, int64_t x_rows, const void* W, int64_t w_stride, void* y,
+                               int64_t max_rows, int64_t N, int64_t K, int32_t E, const int32_t* gather,
+                               const int32_t* rows, const int32_t* tiles, hipStream_t s) {
+  using C = CfgBig8;
+  static const hipError_t attr = hipFuncSetAttribute(
+      reinterpret_cast<const void*>(gemm_bf16_kernel<C, true>), hipFuncAttributeMaxDynamicSharedMemorySize,
+      C::kLdsBytes);
+  if (attr != hipSuccess) return attr;
+  // at most ceil(rows / BM) + E tile-rows; workgroups past the list's end return
+  const int64_t tile_rows = (max_rows + C::BM - 1) / C::BM + E;
+  const int64_t tiles_n = (N + C::BN - 1) / C::BN;
+  GroupedGemm gg{gather, rows, tiles, E, (int)x_rows, w_stride};
+  hipLaunchKernelGGL((gemm_bf16_kernel<C, true>), dim3((unsigned)(tile_rows * tiles_n)), dim3(C::kThreads),
+                     C::kLdsBytes, s, static_cast<const __bf16*>(x), static_cast<const __bf16*>(W), nullptr,
+                     static_cast<__bf16*>(y), (int)max_rows, (int)N, (int)K, 1, (int)K, nullptr, gg);
+  return hipGetLastError();
+}
+
+int32_t grouped_gemm_tile_rows() { return CfgBig8::BM; }
 
 hipError_t launch_linear(const void* x, const void* W, const void* bias, void* y, int64_t M,
                          int64_t N, int64_t K, bool bf16, hipStream_t s) {

@@ -16,6 +16,16 @@ hipError_t launch_swiglu(const void* gu, void* out, int64_t M, int64_t F, bool b
 hipError_t launch_linear(const void* x, const void* W, const void* bias, void* y, int64_t M,
                          int64_t N, int64_t K, bool bf16, hipStream_t s);
 
+// Grouped bf16 GEMM of a mixture-of-experts layer: output rows grouped by
+// expert (expert e owns rows [rows[e], rows[e+1]) and tile-rows [tiles[e],
+// tiles[e+1]) of grouped_gemm_tile_rows() rows); row m multiplies x row
+// gather[m] (m if gather is null) by W + e * w_stride ([N, K] per expert).
+// max_rows bounds rows[E]; y has max_rows rows of N.
+hipError_t launch_gemm_grouped(const void* x, int64_t x_rows, const void* W, int64_t w_stride, void* y,
+                               int64_t max_rows, int64_t N, int64_t K, int32_t E, const int32_t* gather,
+                               const int32_t* rows, const int32_t* tiles, hipStream_t s);
+int32_t grouped_gemm_tile_rows();
+
 // The small-M (decode batch) bf16 linear: all M rows per workgroup, K split
 // over its waves.  Supported for 1 <= M <= kSkinnyMaxM with K % 32 == 0;
 // preferred over the tiled GEMM where it measured faster.
@@ -56,6 +66,15 @@ hipError_t launch_cache_write(const void* k, const void* v, int64_t kv_stride, v
 // residual <- x + residual; y <- rmsnorm(residual) * w.
 hipError_t launch_add_rmsnorm(const void* x, void* res, const void* w, void* y, int64_t M, int64_t H, float eps,
                               bool bf16, hipStream_t s);
+
+// Mixture-of-experts: top-k routing and the fused expert MLPs (k_moe.hip).
+int32_t moe_max_experts();
+size_t moe_workspace_bytes(int64_t T, int32_t H, int32_t F, int32_t E, int32_t topk);
+hipError_t launch_moe_topk(const float* logits, int32_t* ids, float* wts, int64_t T, int32_t E, int32_t k,
+                           bool renormalize, hipStream_t s);
+hipError_t launch_fused_moe(const void* x, const void* w1, const void* w2, const int32_t* ids, const float* wts,
+                            void* out, int64_t T, int32_t H, int32_t F, int32_t E, int32_t k, void* ws,
+                            hipStream_t s);
 
 // Stream-ordered scratch from a per-device pool the library keeps (freed
 // memory is reused by later calls; nothing is returned to the driver).

@@ -31,7 +31,8 @@ def test_header_declares_expected_entry_points():
                  "opscale_rope", "opscale_reshape_and_cache", "opscale_add_rmsnorm",
                  "opscale_cu_layout", "opscale_cu_mask_build", "opscale_cu_stream_create",
                  "opscale_cu_stream_destroy", "opscale_cu_stream_mask", "opscale_cu_probe",
-                 "opscale_corun_profile"):
+                 "opscale_corun_profile", "opscale_moe_topk", "opscale_fused_moe",
+                 "opscale_fused_moe_workspace_size"):
         assert name in d
 
 
@@ -193,7 +194,8 @@ def test_profile_descriptor_layout_matches_header(tmp_path):
     L = ops._lib
     members = {"rmsnorm": L._RmsnormArgs, "linear": L._LinearArgs, "swiglu": L._SwigluArgs,
                "attn_prefill": L._PrefillArgs, "attn_decode": L._DecodeArgs, "rope": L._RopeArgs,
-               "reshape_and_cache": L._CacheWriteArgs, "add_rmsnorm": L._AddRmsnormArgs}
+               "reshape_and_cache": L._CacheWriteArgs, "add_rmsnorm": L._AddRmsnormArgs,
+               "fused_moe": L._FusedMoeArgs}
     lines = ['#include <stdio.h>', '#include <stddef.h>', '#include "opscale.h"', "int main(void) {",
              'printf("desc_size %zu\\n", sizeof(opscale_op_desc));',
              'printf("desc_u %zu\\n", offsetof(opscale_op_desc, u));',
@@ -229,3 +231,32 @@ def test_profile_descriptor_layout_matches_header(tmp_path):
     for m, cls in members.items():
         for f, _ in cls._fields_:
             assert int(out[f"{m}.{f}"]) == getattr(cls, f).offset, f"{m}.{f}"
+
+
+def test_moe_validation(lib):
+    f = lib.opscale_fused_moe
+    need = lib.opscale_fused_moe_workspace_size(64, 128, 256, 8, 2)
+    assert need > 64 * 2 * (2 * 256 + 256 + 128) * 2
+    ok = dict(x=A16, w1=A16 * 2, w2=A16 * 4, ids=A16 * 6, wts=A16 * 7, out=A16 * 8, T=64, H=128, F=256, E=8, k=2,
+              dt=1, ws=A16 * 16, wsb=need)
+
+    def call(**kw):
+        a = dict(ok, **kw)
+        return f(a["x"], a["w1"], a["w2"], a["ids"], a["wts"], a["out"], a["T"], a["H"], a["F"], a["E"], a["k"],
+                 a["dt"], a["ws"], a["wsb"], None, None)
+
+    assert call(dt=0) == 2                      # fp32: bf16 only
+    assert call(H=100) == 1 and call(F=4) == 1  # multiples of 8
+    assert call(E=0) == 1 and call(E=1025) == 1
+    assert call(k=0) == 1 and call(k=65) == 1
+    assert call(wsb=need - 1) == 3
+    assert call(x=A16 + 4) == 1                 # misaligned
+    assert call(ids=A16 * 6 + 2) == 1
+    assert call(out=A16 + 64) == 1              # out overlaps x
+    assert call(T=1 << 24) == 2                 # T*H beyond the 32-bit offsets
+    assert call(T=0) == 0
+    t = lib.opscale_moe_topk
+    assert t(A16, A16 * 2, A16 * 3, 10, 8, 9, 1, None, None) == 1   # topk > E
+    assert t(A16, A16 * 2, A16 * 3, 10, 64, 17, 1, None, None) == 1  # topk > 16
+    assert t(A16, A16 * 2, A16 * 3, 10, 2000, 2, 1, None, None) == 1
+    assert t(None, None, None, 0, 8, 2, 1, None, None) == 0
