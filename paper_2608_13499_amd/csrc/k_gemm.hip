@@ -55,6 +55,7 @@ struct GemmCfg {
 using CfgBig8 = GemmCfg<256, 256, 64, 2, 4, 2>;    // 8 waves of 128x64, 2 x 64 KB stages
 using CfgT192 = GemmCfg<192, 256, 64, 2, 4, 2>;    // 8 waves of 96x64, 2 x 56 KB stages
 using CfgMid = GemmCfg<256, 128, 64, 2, 2, 3>;     // 4 waves of 128x64, 3 x 48 KB stages
+using CfgRow64 = GemmCfg<64, 256, 64, 1, 4, 2>;    // 4 waves of 64x64, 2 x 40 KB stages (few rows)
 
 
 // 16-byte chunk c of LDS row r is stored at physical chunk c ^ swz(r).  For
@@ -143,17 +144,24 @@ __global__ __launch_bounds__(C::kThreads, 1) void gemm_bf16_kernel(const __bf16*
   const int ld = K_total;
   int m0, n0, m_rows, split = 0;
   if constexpr (GROUPED) {
-    // tile-row t of the expert list, column block n; experts by bisection
-    const int t = blockIdx.x / tiles_n;
-    n0 = (blockIdx.x - t * tiles_n) * BN;
-    if (t >= gg.tiles[gg.E]) return;
-    int lo = 0, hi = gg.E;  // gg.tiles[lo] <= t < gg.tiles[hi]
+    // Work items in order expert, column block, tile-row of the expert, so
+    // an expert's tile-rows use one W column block back to back; spread over
+    // the XCDs in contiguous ranges of the items that exist (the grid is an
+    // upper bound; the workgroups past it return).
+    const int total = gg.tiles[gg.E] * tiles_n;
+    if ((int)blockIdx.x >= total) return;
+    const int id = (int)xcd_remap(blockIdx.x, (uint32_t)total);
+    int lo = 0, hi = gg.E;  // gg.tiles[lo] * tiles_n <= id < gg.tiles[hi] * tiles_n
     while (hi - lo > 1) {
       const int mid = (lo + hi) >> 1;
-      if (gg.tiles[mid] <= t) lo = mid;
+      if (gg.tiles[mid] * tiles_n <= id) lo = mid;
       else hi = mid;
     }
-    m0 = gg.rows[lo] + (t - gg.tiles[lo]) * BM;
+    const int tr_e = gg.tiles[lo + 1] - gg.tiles[lo];  // tile-rows of expert lo (>= 1)
+    const int local = id - gg.tiles[lo] * tiles_n;
+    const int tn = local / tr_e, tr = local - tn * tr_e;
+    n0 = tn * BN;
+    m0 = gg.rows[lo] + tr * BM;
     m_rows = min(BM, gg.rows[lo + 1] - m0);
     W += lo * gg.w_stride;
   } else {
@@ -493,10 +501,10 @@ static int splitk_count(int64_t M, int64_t N, int64_t K) {
   return s >= 2 ? (int)s : 0;
 }
 
-hipError_t launch_gemm_grouped(const void* x, int64_t x_rows, const void* W, int64_t w_stride, void* y,
-                               int64_t max_rows, int64_t N, int64_t K, int32_t E, const int32_t* gather,
-                               const int32_t* rows, const int32_t* tiles, hipStream_t s) {
-  using C = CfgBig8;
+template <class C>
+static hipError_t launch_grouped(const void* x, int64_t x_rows, const void* W, int64_t w_stride, void* y,
+                                 int64_t max_rows, int64_t N, int64_t K, int32_t E, const int32_t* gather,
+                                 const int32_t* rows, const int32_t* tiles, hipStream_t s) {
   static const hipError_t attr = hipFuncSetAttribute(
       reinterpret_cast<const void*>(gemm_bf16_kernel<C, true>), hipFuncAttributeMaxDynamicSharedMemorySize,
       C::kLdsBytes);
@@ -511,7 +519,19 @@ hipError_t launch_gemm_grouped(const void* x, int64_t x_rows, const void* W, int
   return hipGetLastError();
 }
 
-int32_t grouped_gemm_tile_rows() { return CfgBig8::BM; }
+int32_t grouped_gemm_tile_rows(int64_t rows, int32_t E) {
+  // about 96 rows or fewer per expert (decode batches): 64-row tiles, so the
+  // matrix cores do not spend most of a 256-row tile on padding
+  return rows <= (int64_t)96 * E ? CfgRow64::BM : CfgBig8::BM;
+}
+
+hipError_t launch_gemm_grouped(const void* x, int64_t x_rows, const void* W, int64_t w_stride, void* y,
+                               int64_t max_rows, int64_t N, int64_t K, int32_t E, int32_t tile_rows,
+                               const int32_t* gather, const int32_t* rows, const int32_t* tiles, hipStream_t s) {
+  if (tile_rows == CfgRow64::BM)
+    return launch_grouped<CfgRow64>(x, x_rows, W, w_stride, y, max_rows, N, K, E, gather, rows, tiles, s);
+  return launch_grouped<CfgBig8>(x, x_rows, W, w_stride, y, max_rows, N, K, E, gather, rows, tiles, s);
+}
 
 hipError_t launch_linear(const void* x, const void* W, const void* bias, void* y, int64_t M,
                          int64_t N, int64_t K, bool bf16, hipStream_t s) {

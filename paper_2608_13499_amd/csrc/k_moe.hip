@@ -298,22 +298,22 @@ hipError_t launch_fused_moe(const void* x, const void* w1, const void* w2, const
   const int64_t R = T * k;
   const int nb = (int)((R + kSortChunk - 1) / kSortChunk);
   const MoeWorkspace w = carve(ws, T, H, F, E, k);
+  const int32_t bm = grouped_gemm_tile_rows(R, E);
   hipLaunchKernelGGL(moe_count_kernel, dim3((unsigned)nb), dim3(64), 0, s, ids, R, E, w.counts);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(moe_scan_kernel, dim3(1), dim3(1024), 0, s, w.counts, nb, E, grouped_gemm_tile_rows(), w.rows,
-                     w.tiles);
+  hipLaunchKernelGGL(moe_scan_kernel, dim3(1), dim3(1024), 0, s, w.counts, nb, E, bm, w.rows, w.tiles);
   if ((e = hipGetLastError()) != hipSuccess) return e;
   hipLaunchKernelGGL(moe_scatter_kernel, dim3((unsigned)nb), dim3(64), 0, s, ids, R, E, k, w.counts, w.rows, w.gather,
                      w.pos);
   if ((e = hipGetLastError()) != hipSuccess) return e;
   // gate_up = W1[e] x[token]   (rows gathered), [R, 2F]
-  if ((e = launch_gemm_grouped(x, T, w1, (int64_t)2 * F * H, w.gate_up, R, 2 * (int64_t)F, H, E, w.gather, w.rows,
-                               w.tiles, s)) != hipSuccess)
+  if ((e = launch_gemm_grouped(x, T, w1, (int64_t)2 * F * H, w.gate_up, R, 2 * (int64_t)F, H, E, bm, w.gather,
+                               w.rows, w.tiles, s)) != hipSuccess)
     return e;
   if ((e = launch_swiglu(w.gate_up, w.act, R, F, true, s)) != hipSuccess) return e;
   // y = W2[e] act   (sorted rows), [R, H]
-  if ((e = launch_gemm_grouped(w.act, R, w2, (int64_t)H * F, w.y, R, H, F, E, nullptr, w.rows, w.tiles, s)) !=
+  if ((e = launch_gemm_grouped(w.act, R, w2, (int64_t)H * F, w.y, R, H, F, E, bm, nullptr, w.rows, w.tiles, s)) !=
       hipSuccess)
     return e;
   hipLaunchKernelGGL(moe_combine_kernel, dim3((unsigned)T), dim3(256), 0, s, w.y, w.pos, wts,

@@ -18,13 +18,14 @@ hipError_t launch_linear(const void* x, const void* W, const void* bias, void* y
 
 // Grouped bf16 GEMM of a mixture-of-experts layer: output rows grouped by
 // expert (expert e owns rows [rows[e], rows[e+1]) and tile-rows [tiles[e],
-// tiles[e+1]) of grouped_gemm_tile_rows() rows); row m multiplies x row
-// gather[m] (m if gather is null) by W + e * w_stride ([N, K] per expert).
-// max_rows bounds rows[E]; y has max_rows rows of N.
+// tiles[e+1]) of tile_rows rows); row m multiplies x row gather[m] (m if
+// gather is null) by W + e * w_stride ([N, K] per expert).  max_rows bounds
+// rows[E]; y has max_rows rows of N.  tile_rows is
+// grouped_gemm_tile_rows(max_rows, E), the value the tile table was built with.
+int32_t grouped_gemm_tile_rows(int64_t rows, int32_t E);
 hipError_t launch_gemm_grouped(const void* x, int64_t x_rows, const void* W, int64_t w_stride, void* y,
-                               int64_t max_rows, int64_t N, int64_t K, int32_t E, const int32_t* gather,
-                               const int32_t* rows, const int32_t* tiles, hipStream_t s);
-int32_t grouped_gemm_tile_rows();
+                               int64_t max_rows, int64_t N, int64_t K, int32_t E, int32_t tile_rows,
+                               const int32_t* gather, const int32_t* rows, const int32_t* tiles, hipStream_t s);
 
 // The small-M (decode batch) bf16 linear: all M rows per workgroup, K split
 // over its waves.  Supported for 1 <= M <= kSkinnyMaxM with K % 32 == 0;
