@@ -385,6 +385,22 @@ def main():
         extra_ops[nm] = {"us": round(pr.us_median, 2), "tokens/s": round(B / (pr.us_median * 1e-6), 1),
                          "tflops": round(pr.tflops, 1), "gbps": round(pr.gbps, 1),
                          "bound": "mfma+hbm", "roofline_frac": round(pr.roofline_frac, 4)}
+    # The mixture-of-experts FFN of the paper's MoE models, cold as above:
+    # Mixtral-8x7B over the prefill batch's 8871 tokens, Qwen2-57B-A14B at a
+    # 256-token decode batch (synthetic routing: N(0, 1) router logits).
+    for mc in (wl.MOE_MIXTRAL_PREFILL, wl.MOE_QWEN_DECODE):
+        H, F, E, k, T = mc.hidden, mc.ffn, mc.experts, mc.topk, mc.tokens
+        w1 = wl.device_normal((E, 2 * F, H), mc.seed, "moe_w1", "bf16", std=0.02)
+        w2 = wl.device_normal((E, H, F), mc.seed, "moe_w2", "bf16", std=0.02)
+        xm = wl.device_normal((T, H), mc.seed, "x", "bf16")
+        ids, wts = ops.opscale_moe_topk(wl.device_normal((T, E), mc.seed, "router", "f32"), k, True)
+        om = torch.empty_like(xm)
+        wsm = torch.empty(ops.opscale_fused_moe_workspace_size(T, H, F, E, k), dtype=torch.uint8, device="cuda")
+        pr = ops.opscale_op_profile(ops.desc_fused_moe(xm, w1, w2, ids, wts, om, wsm), a.warmup, a.steps, flush)
+        extra_ops[mc.name] = {"us": round(pr.us_median, 2), "tokens/s": round(T / (pr.us_median * 1e-6), 1),
+                              "tflops": round(pr.tflops, 1), "gbps": round(pr.gbps, 1),
+                              "bound": "mfma" if pr.bound == 0 else "hbm", "roofline_frac": round(pr.roofline_frac, 4)}
+        del w1, w2, xm, ids, wts, om, wsm
     del flush
     M = layer.p["M"]
     out = {

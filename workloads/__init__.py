@@ -36,6 +36,7 @@ TAG = {
     "x": 1, "w_norm": 2, "w_qkv": 3, "w_o": 4, "w_gate_up": 5, "w_down": 6,
     "q": 7, "k": 8, "v": 9, "gate_up": 10, "k_cache": 11, "v_cache": 12,
     "block_table": 13, "attn_out": 14, "ffn_act": 15, "dq": 16, "bias": 17,
+    "moe_w1": 18, "moe_w2": 19, "router": 20,
 }
 
 
@@ -91,6 +92,27 @@ C3 = LayerConfig("llama8b_decode_b256", "bf16", 4096, 32, 8, 128, 14336, mode="d
 C4 = LayerConfig("llama70b_prefill_16k", "bf16", 8192, 64, 8, 128, 28672)
 C5 = LayerConfig("llama8b_bursty_longctx", "bf16", 4096, 32, 8, 128, 14336)
 CONFIGS = {c.name: c for c in (C1, C2, C3, C4, C5)}
+
+
+@dataclasses.dataclass(frozen=True)
+class MoEConfig:
+    """The FFN of a mixture-of-experts layer (the paper's MoE models, Table 3):
+    E experts of hidden H and expert width F, topk routed experts per token."""
+    name: str
+    hidden: int
+    ffn: int
+    experts: int
+    topk: int
+    tokens: int
+    seed: int = 0
+
+
+# Mixtral-8x7B: 8 experts of 14336, top-2; Qwen2-57B-A14B: 64 experts of 2560,
+# top-8 (its shared expert is a dense MLP and not part of the routed operator).
+# Routing is synthetic: router logits ~ N(0, 1), iid per token and expert,
+# through top-k softmax with the k weights renormalized.
+MOE_MIXTRAL_PREFILL = MoEConfig("mixtral8x7b_moe_prefill8871", 4096, 14336, 8, 2, 8871)
+MOE_QWEN_DECODE = MoEConfig("qwen2_57b_a14b_moe_decode256", 3584, 2560, 64, 8, 256)
 ORDER = [C1.name, C2.name, C3.name, C4.name, C5.name]
 
 
