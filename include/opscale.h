@@ -156,8 +156,11 @@ size_t opscale_attn_decode_workspace_size(int32_t B, int32_t Hq, int32_t D,
  * max_blocks_per_seq * block_size are clamped to it.  Keys whose block id is
  * outside [0, num_blocks) are skipped (never read); a row whose keys are all
  * skipped is zero.
- * max_context_len: an upper bound on context_lens used to size the split-KV
- *   launch and the workspace; results do not depend on it.
+ * max_context_len: the expected largest context length; it sizes the
+ *   split-KV launch (one workgroup per 32 keys of B x max_context_len, at most
+ *   2048, each taking an equal share of the keys actually present) and the
+ *   workspace.  Longer contexts are still served whole; the value changes
+ *   only how the keys are split, so results agree to rounding across values.
  * workspace: DEVICE scratch of at least opscale_attn_decode_workspace_size(B,
  *   Hq, D, max_context_len) bytes, else OPSCALE_ERR_WORKSPACE.  Contents on
  *   entry are ignored.  Calls sharing a workspace must be stream-ordered.

@@ -41,11 +41,10 @@ hipError_t launch_attn_prefill(const void* q, const void* k, const void* v, int6
                                int64_t total_tokens, int32_t max_seqlen, int32_t Hq, int32_t Hkv,
                                int32_t D, float scale, bool causal, bool bf16, hipStream_t s);
 
-// Split-KV decode: keys per split and the number of key-range splits per
-// sequence the launch uses (both depend on the batch: small batches get short
-// splits so that the launch still fills the GPU).
-int32_t decode_chunk_keys(int32_t B, int32_t max_context_len);
-int32_t decode_max_splits(int32_t B, int32_t max_context_len);
+// Balanced split-KV decode: workgroups of a launch (each takes an equal range
+// of the batch's 32-key tiles) and the workspace it needs (the tile prefix
+// sums, then (workgroups + B) x Hq partial results of D + 2 floats).
+int32_t decode_workgroups(int32_t B, int32_t max_context_len, int32_t groups);
 size_t decode_workspace_bytes(int32_t B, int32_t Hq, int32_t D, int32_t max_context_len);
 
 hipError_t launch_attn_decode(const void* q, int64_t q_stride, const void* kc, const void* vc, const int32_t* table,

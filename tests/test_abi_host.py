@@ -109,14 +109,20 @@ def test_prefill_validation(lib):
 def test_decode_validation_and_workspace(lib):
     f = lib.opscale_attn_decode
     need = lib.opscale_attn_decode_workspace_size(256, 32, 128, 8192)
-    assert need == 4 * 256 * 32 * 16 * 130            # 512-key splits
-    # small batches get shorter splits (about 1024 workgroups, at most 64
-    # splits a sequence): one sequence of 2048 keys takes 64 splits of 32
-    # keys, of 8192 keys 64 splits of 128, 16 sequences 64 splits of 32
-    assert lib.opscale_attn_decode_workspace_size(1, 32, 128, 2048) == 4 * 1 * 32 * 64 * 130
-    assert lib.opscale_attn_decode_workspace_size(1, 32, 128, 8192) == 4 * 1 * 32 * 64 * 130
-    assert lib.opscale_attn_decode_workspace_size(16, 32, 128, 2048) == 4 * 16 * 32 * 64 * 130
-    assert lib.opscale_attn_decode_workspace_size(64, 32, 128, 2048) == 4 * 64 * 32 * 16 * 130
+    # balanced split-KV: one workgroup per 32-key tile of B x max_context_len
+    # keys, at most 512 and 64 per sequence; the tile prefix sums (B + 1 int64), above 512
+    # sequences each workgroup's first sequence (int32), each 256-byte aligned,
+    # then (workgroups + B) x Hq partials of D + 2 floats
+    def ws(B, Hq, D, mc):
+        nwg = min(512, B * -(-mc // 32), 64 * B)
+        up = lambda x: (x + 255) // 256 * 256
+        return up(8 * (B + 1)) + (up(4 * nwg) if B > 512 else 0) + 4 * (nwg + B) * Hq * (D + 2)
+    assert need == ws(256, 32, 128, 8192) == 2304 + 4 * (512 + 256) * 32 * 130
+    assert lib.opscale_attn_decode_workspace_size(1, 32, 128, 2048) == 256 + 4 * (64 + 1) * 32 * 130
+    assert lib.opscale_attn_decode_workspace_size(1, 32, 128, 8192) == 256 + 4 * (64 + 1) * 32 * 130
+    for B, Hq, D, mc in [(1, 32, 128, 8192), (16, 32, 128, 2048), (64, 32, 128, 2048), (3, 8, 64, 33),
+                         (1000, 64, 128, 1), (512, 8, 64, 100), (513, 8, 64, 100)]:
+        assert lib.opscale_attn_decode_workspace_size(B, Hq, D, mc) == ws(B, Hq, D, mc)
     ok = dict(q=A16, qs=32 * 128, kc=A16, vc=A16, tab=A16, ctx=A16, o=A16 * 8, B=256, Hq=32, Hkv=8, D=128, bs=16,
               mb=512, nb=69424, mc=8192, scale=0.08, dt=1, ws=A16 * 32, wsb=need)
 

@@ -306,6 +306,29 @@ def test_attn_decode_invalid_block_is_skipped(ops, dtype):
     assert_close(got, ref, dtype, "attn_decode bad block")
 
 
+@pytest.mark.parametrize("name,ctx,maxc", [
+    # far fewer 32-key tiles than workgroups: most workgroups have no keys
+    ("sparse", [0, 5, 0, 33, 1, 0, 64, 2], 4096),
+    ("one long, many short", [9000] + [3] * 39, None),
+    # about 1.5 tiles a workgroup: ranges straddle sequence boundaries
+    ("straddling", list(np.random.default_rng(8).integers(1, 2000, 100)), None),
+    # one workgroup a sequence, each over several 512-key page windows
+    ("few workgroups", [3000, 1, 1500, 0, 2047], 1),
+    ("all empty", [0, 0, 0], 64),
+    # above 512 sequences the plan comes from its own kernel
+    ("large batch", list(np.random.default_rng(9).integers(0, 300, 700)), None),
+    ("large batch, sparse", [0] * 600 + [40] + [0] * 100 + [1], 2048),
+])
+def test_attn_decode_balanced_ranges(ops, name, ctx, maxc):
+    """Every workgroup takes an equal range of the batch's 32-key tiles; the
+    ranges and the merge must cover each sequence's keys exactly once."""
+    say(f"attn_decode balanced ranges: {name} (B={len(ctx)})")
+    got, ref = _decode_case(ops, "bf16", ctx, 8, 2, 128, 16, seed=len(ctx), max_context_len=maxc)
+    assert_close(got, ref, "bf16", f"attn_decode {name}")
+    if max(ctx) == 0:
+        assert np.all(got == 0)
+
+
 @pytest.mark.parametrize("bs", [16, 1])
 def test_attn_decode_context_beyond_launch_bound(ops, bs):
     """max_context_len only sizes the launch: a longer context is processed in
