@@ -277,12 +277,20 @@ __global__ __launch_bounds__(C::kThreads, 1) void gemm_bf16_kernel(const __bf16*
       }
     }
   };
+  // The next k-step's fragment reads (issued just before, in the same block)
+  // go one after each MFMA: left to itself the scheduler puts them after the
+  // MFMAs, and the next k-step then waits for a whole LDS round trip.
   auto mfmas = [&](int buf) {
 #pragma unroll
     for (int i = 0; i < TN; ++i)
 #pragma unroll
       for (int j = 0; j < TM; ++j)
         acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[buf][i], b[buf][j], acc[i][j], 0, 0, 0);
+#pragma unroll
+    for (int q = 0; q < TN * TM; ++q) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // one MFMA
+      if (q < TN + TM) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // one LDS read
+    }
   };
 
   if constexpr (S == 2) {
