@@ -28,10 +28,14 @@ __device__ __forceinline__ u32x4 buffer_load16(__amdgpu_buffer_rsrc_t r, uint32_
   return __builtin_amdgcn_raw_buffer_load_b128(r, voff, 0, 0);
 }
 
-// 16 bytes per lane straight into LDS at lds_wave_base + lane * 16.
+// 16 bytes per lane straight into LDS at lds_wave_base + lane * 16.  POLICY
+// is the instruction's cache-policy field; kNoL1 (sc0) keeps the line out of
+// the CU's L1, for data each CU reads once (it still allocates in L2).
+constexpr int kNoL1 = 1;
+template <int POLICY = 0>
 __device__ __forceinline__ void buffer_load16_lds(__amdgpu_buffer_rsrc_t r, OPS_LDS void* lds_wave_base,
                                                   uint32_t voff) {
-  __builtin_amdgcn_raw_ptr_buffer_load_lds(r, lds_wave_base, 16, voff, 0, 0, 0);
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(r, lds_wave_base, 16, voff, 0, 0, POLICY);
 }
 
 // 16 bytes per lane from a 64-bit global address into LDS at lds_wave_base +

@@ -99,7 +99,7 @@ __device__ __forceinline__ void load_slice(__amdgpu_buffer_rsrc_t rsrc, OPS_LDS 
     const int c = pc ^ swz<C::kCPR>(r);
     const int k = k0 + c * 8;
     const uint32_t voff = (k < K && row_off[g] != kNoRow) ? row_off[g] + (uint32_t)k * 2u : kOobOffset;
-    buffer_load16_lds(rsrc, lds + grp * 1024, voff);
+    buffer_load16_lds<kNoL1>(rsrc, lds + grp * 1024, voff);
   }
 }
 
@@ -110,9 +110,30 @@ __device__ __forceinline__ bf16x8 lds_frag(const OPS_LDS char* p) {
 
 }  // namespace
 
+// Tile (tm, tn) of plain-GEMM tile id tid in grouped order: group_m
+// tile-rows sweep the tile-columns together, so a W column-block is fetched
+// once per group and reused from L2 / MALL by every tile-row of the group
+// while the group's x rows stay cache resident.
+__device__ __forceinline__ void tile_coords(uint32_t tid, int tiles_m, int tiles_n, int group_m, int& tm, int& tn) {
+  const int group = tid / (group_m * tiles_n);
+  const int first_m = group * group_m;
+  const int gsize = min(tiles_m - first_m, group_m);
+  const int in_group = tid % (group_m * tiles_n);
+  tm = first_m + in_group % gsize;
+  tn = in_group / gsize;
+}
+
 // Split-K (splits > 1): workgroup blockIdx.x / tiles takes the K range
 // [split * kchunk, (split + 1) * kchunk) and writes its fp32 partial tile to
 // part[split][M][N] (no bias); a second kernel sums the splits in order.
+//
+// Split tail (tail_cnt > 0): workgroups [0, dp_cnt) take whole tiles 0 ..
+// dp_cnt - 1 (full K, results to y); the rest take the K ranges of the last
+// tail_cnt tiles: item b (from dp_cnt) covers tile dp_cnt + b % tail_cnt, K
+// range b / tail_cnt, and writes its fp32 tile compactly to
+// part[(split * tail_cnt + tile - dp_cnt) * BM * BN] (row-major BM x BN); a
+// second kernel sums those in split order.  Runs a launch whose last round
+// would be mostly idle at a fraction of a tile's time.
 //
 // GROUPED (one GEMM per expert of a mixture-of-experts layer): the output
 // rows are grouped by expert, expert e owning rows [rows[e], rows[e + 1]) in
@@ -134,7 +155,8 @@ __global__ __launch_bounds__(C::kThreads, 1) void gemm_bf16_kernel(const __bf16*
                                                                    const __bf16* __restrict__ bias,
                                                                    __bf16* __restrict__ y, int M, int N,
                                                                    int K_total, int group_m, int kchunk,
-                                                                   float* __restrict__ part, GroupedGemm gg) {
+                                                                   float* __restrict__ part, GroupedGemm gg,
+                                                                   int dp_cnt, int tail_cnt) {
   extern __shared__ __attribute__((aligned(16))) char smem_raw[];
   OPS_LDS char* smem = (OPS_LDS char*)smem_raw;
   constexpr int BM = C::BM, BN = C::BN, BK = C::BK, WM = C::WM, WN = C::WN, S = C::STAGES;
@@ -143,6 +165,8 @@ __global__ __launch_bounds__(C::kThreads, 1) void gemm_bf16_kernel(const __bf16*
   const int tiles_n = (N + BN - 1) / BN;
   const int ld = K_total;
   int m0, n0, m_rows, split = 0;
+  int kc = kchunk;                  // K elements per split
+  float* tile_part = nullptr;       // split tail: this item's compact partial tile
   if constexpr (GROUPED) {
     // Work items in order expert, column block, tile-row of the expert, so
     // an expert's tile-rows use one W column block back to back; spread over
@@ -167,23 +191,29 @@ __global__ __launch_bounds__(C::kThreads, 1) void gemm_bf16_kernel(const __bf16*
   } else {
     const int tiles_m = (M + BM - 1) / BM;
     const int tiles = tiles_m * tiles_n;
-    split = blockIdx.x / tiles;
-    const uint32_t tid = xcd_remap(blockIdx.x - split * tiles, (uint32_t)tiles);
-    // grouped order: group_m tile-rows sweep the tile-columns together, so a
-    // W column-block is fetched once per group and reused from L2 / MALL by
-    // every tile-row of the group while the group's x rows stay cache resident
-    const int group = tid / (group_m * tiles_n);
-    const int first_m = group * group_m;
-    const int gsize = min(tiles_m - first_m, group_m);
-    const int in_group = tid % (group_m * tiles_n);
-    const int tm = first_m + in_group % gsize, tn = in_group / gsize;
+    uint32_t tid;
+    if (tail_cnt == 0) {
+      split = blockIdx.x / tiles;
+      tid = xcd_remap(blockIdx.x - split * tiles, (uint32_t)tiles);
+    } else if ((int)blockIdx.x < dp_cnt) {
+      tid = xcd_remap(blockIdx.x, (uint32_t)dp_cnt);
+      kc = K_total;
+    } else {
+      const int b = blockIdx.x - dp_cnt;
+      split = b / tail_cnt;
+      const int t = (int)xcd_remap(b - split * tail_cnt, (uint32_t)tail_cnt);
+      tid = dp_cnt + t;
+      tile_part = part + ((int64_t)split * tail_cnt + t) * BM * BN;
+    }
+    int tm, tn;
+    tile_coords(tid, tiles_m, tiles_n, group_m, tm, tn);
     m0 = tm * BM;
     n0 = tn * BN;
     m_rows = min(BM, M - m0);
   }
   // this workgroup's K range: K elements starting at k_begin, rows ld apart
-  const int k_begin = split * kchunk;
-  const int K = min(K_total - k_begin, kchunk);
+  const int k_begin = split * kc;
+  const int K = min(K_total - k_begin, kc);
 
   // wave index as a scalar: the LDS destinations of the loads are then
   // wave-uniform without a readfirstlane per load
@@ -272,7 +302,7 @@ __global__ __launch_bounds__(C::kThreads, 1) void gemm_bf16_kernel(const __bf16*
         const int k = k0 + ((pc ^ swz<C::kCPR>(r)) << 3);
         const uint32_t ro = isx ? xro[q < LX ? q : 0] : wro[q >= LX ? q - LX : 0];
         const uint32_t voff = (more && k < K && ro != kNoRow) ? ro + (uint32_t)k * 2u : kOobOffset;
-        buffer_load16_lds(isx ? xr : wr, dst + (isx ? 0 : BM * C::kRowBytes) + grp * 1024, voff);
+        buffer_load16_lds<kNoL1>(isx ? xr : wr, dst + (isx ? 0 : BM * C::kRowBytes) + grp * 1024, voff);
         __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
       }
     }
@@ -350,7 +380,22 @@ __global__ __launch_bounds__(C::kThreads, 1) void gemm_bf16_kernel(const __bf16*
   // Epilogue.  acc[i][j] element e: n = n0 + wn*WN + i*32 + (e/4)*8 + fh*4 + e%4,
   // m = m0 + wm*WM + j*32 + fr.  Four consecutive n per lane -> one 8-byte store
   // (one 16-byte store of fp32 partials under split-K).
-  if (part) {
+  if (tile_part) {
+#pragma unroll
+    for (int j = 0; j < TM; ++j) {
+      const int r = wm * WM + j * 32 + fr;
+#pragma unroll
+      for (int i = 0; i < TN; ++i)
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+          const int c = wn * WN + i * 32 + g * 8 + fh * 4;
+          *reinterpret_cast<f32x4*>(tile_part + r * BN + c) =
+              f32x4{acc[i][j][g * 4 + 0], acc[i][j][g * 4 + 1], acc[i][j][g * 4 + 2], acc[i][j][g * 4 + 3]};
+        }
+    }
+    return;
+  }
+  if (part && tail_cnt == 0) {
     float* pbase = part + (int64_t)split * M * N;
 #pragma unroll
     for (int j = 0; j < TM; ++j) {
@@ -465,9 +510,45 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(const float* __restr
   }
 }
 
+// y of the split tail: tile dp_cnt + t is the sum over splits (in order) of
+// its compact partials, plus bias.  Grid (tail_cnt, BM / 16): 16 rows of one
+// tile per workgroup, four consecutive columns per thread (N % 8 == 0).
+template <int BM, int BN>
+__global__ __launch_bounds__(256) void splitk_tile_reduce_kernel(const float* __restrict__ part, int splits,
+                                                                 int dp_cnt, int tail_cnt, int M, int N,
+                                                                 int tiles_m, int tiles_n, int group_m,
+                                                                 const __bf16* __restrict__ bias,
+                                                                 __bf16* __restrict__ y) {
+  const int t = blockIdx.x;
+  int tm, tn;
+  tile_coords(dp_cnt + t, tiles_m, tiles_n, group_m, tm, tn);
+  const int m0 = tm * BM, n0 = tn * BN;
+  constexpr int C4 = BN / 4;
+  for (int idx = threadIdx.x; idx < 16 * C4; idx += 256) {
+    const int r = blockIdx.y * 16 + idx / C4, c = (idx % C4) * 4;
+    const int m = m0 + r, n = n0 + c;
+    if (m >= M || n >= N) continue;
+    const float* p = part + (int64_t)t * BM * BN + r * BN + c;
+    f32x4 a = *reinterpret_cast<const f32x4*>(p);
+    for (int sp = 1; sp < splits; ++sp) a += *reinterpret_cast<const f32x4*>(p + (int64_t)sp * tail_cnt * BM * BN);
+    if (bias) {
+      const u32x2 bb = *reinterpret_cast<const u32x2*>(bias + n);
+      a[0] += bf_lo(bb[0]);
+      a[1] += bf_hi(bb[0]);
+      a[2] += bf_lo(bb[1]);
+      a[3] += bf_hi(bb[1]);
+    }
+    *reinterpret_cast<u32x2*>(y + (int64_t)m * N + n) = u32x2{pack_bf2(a[0], a[1]), pack_bf2(a[2], a[3])};
+  }
+}
+
+// tail_splits > 1: the tiles of the last, partly filled round run as that many
+// K ranges each (compact fp32 partials in stream-ordered scratch, then an
+// ordered reduce); the other tiles as usual, in the same launch.
 template <class C>
 static hipError_t launch_gemm_bf16(const void* x, const void* W, const void* bias, void* y, int64_t M,
-                                   int64_t N, int64_t K, hipStream_t s, int splits = 1, float* part = nullptr) {
+                                   int64_t N, int64_t K, hipStream_t s, int splits = 1, float* part = nullptr,
+                                   int tail_splits = 0) {
   // More than 64 KB of dynamic LDS per workgroup needs the limit raised once
   // per process (a host-side function attribute, no allocation).
   static const hipError_t attr = hipFuncSetAttribute(
@@ -482,13 +563,35 @@ static hipError_t launch_gemm_bf16(const void* x, const void* W, const void* bia
   constexpr int64_t kGroupBytes = 16ll << 20;
   const int64_t row_block_bytes = (int64_t)C::BM * K * 2;
   const int group_m = (int)std::max<int64_t>(1, std::min<int64_t>(tiles_m, kGroupBytes / row_block_bytes));
+  if (tail_splits > 1) {
+    const int64_t tail = tiles % kNumCUs, dp = tiles - tail;
+    const int64_t kchunk = ((K + tail_splits - 1) / tail_splits + C::BK - 1) / C::BK * C::BK;
+    const int64_t nsplit = (K + kchunk - 1) / kchunk;
+    void* ws = nullptr;
+    hipError_t e = scratch_alloc((size_t)nsplit * tail * C::BM * C::BN * sizeof(float), s, &ws);
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL((gemm_bf16_kernel<C>), dim3((unsigned)(dp + tail * nsplit)), dim3(C::kThreads), C::kLdsBytes,
+                       s, static_cast<const __bf16*>(x), static_cast<const __bf16*>(W),
+                       static_cast<const __bf16*>(bias), static_cast<__bf16*>(y), (int)M, (int)N, (int)K, group_m,
+                       (int)kchunk, static_cast<float*>(ws), GroupedGemm{}, (int)dp, (int)tail);
+    e = hipGetLastError();
+    if (e == hipSuccess) {
+      hipLaunchKernelGGL((splitk_tile_reduce_kernel<C::BM, C::BN>), dim3((unsigned)tail, C::BM / 16), dim3(256), 0, s,
+                         static_cast<const float*>(ws), (int)nsplit, (int)dp, (int)tail, (int)M, (int)N,
+                         (int)tiles_m, (int)((N + C::BN - 1) / C::BN), group_m, static_cast<const __bf16*>(bias),
+                         static_cast<__bf16*>(y));
+      e = hipGetLastError();
+    }
+    const hipError_t f = scratch_free(ws, s);
+    return e != hipSuccess ? e : f;
+  }
   // K range per split: a whole number of BK slices
   const int64_t kchunk = part ? ((K + splits - 1) / splits + C::BK - 1) / C::BK * C::BK : K;
   const int64_t nsplit = part ? (K + kchunk - 1) / kchunk : 1;
   hipLaunchKernelGGL((gemm_bf16_kernel<C>), dim3((unsigned)(tiles * nsplit)), dim3(C::kThreads), C::kLdsBytes, s,
                      static_cast<const __bf16*>(x), static_cast<const __bf16*>(W),
                      static_cast<const __bf16*>(bias), static_cast<__bf16*>(y), (int)M, (int)N, (int)K,
-                     group_m, (int)kchunk, part, GroupedGemm{});
+                     group_m, (int)kchunk, part, GroupedGemm{}, 0, 0);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || !part) return e;
   const int64_t MN = M * N;
@@ -523,7 +626,7 @@ static hipError_t launch_grouped(const void* x, int64_t x_rows, const void* W, i
   GroupedGemm gg{gather, rows, tiles, E, (int)x_rows, w_stride};
   hipLaunchKernelGGL((gemm_bf16_kernel<C, true>), dim3((unsigned)(tile_rows * tiles_n)), dim3(C::kThreads),
                      C::kLdsBytes, s, static_cast<const __bf16*>(x), static_cast<const __bf16*>(W), nullptr,
-                     static_cast<__bf16*>(y), (int)max_rows, (int)N, (int)K, 1, (int)K, nullptr, gg);
+                     static_cast<__bf16*>(y), (int)max_rows, (int)N, (int)K, 1, (int)K, nullptr, gg, 0, 0);
   return hipGetLastError();
 }
 
@@ -590,9 +693,19 @@ hipError_t launch_linear(const void* x, const void* W, const void* bias, void* y
       const double t = (double)((tiles + kNumCUs - 1) / kNumCUs) * choices[c].bm * choices[c].bn * choices[c].cost;
       if (c == 0 || t < best_t) { best = c; best_t = t; }
     }
-    if (best == 0) return launch_gemm_bf16<CfgBig8>(x, W, bias, y, M, N, K, s);
-    if (best == 1) return launch_gemm_bf16<CfgT192>(x, W, bias, y, M, N, K, s);
-    return launch_gemm_bf16<CfgMid>(x, W, bias, y, M, N, K, s);
+    // A last round at most half full runs split over K: 2-4 ranges per tile
+    // (at most one workgroup per CU in all), each at least 8 slices long.
+    // OPSCALE_GEMM_TAIL=0 turns this off (tuning and tests).
+    const int64_t tiles = ((M + choices[best].bm - 1) / choices[best].bm) * ((N + choices[best].bn - 1) / choices[best].bn);
+    const int64_t tail = tiles % kNumCUs;
+    const char* te = getenv("OPSCALE_GEMM_TAIL");
+    int ts = 0;
+    if (!(te && strcmp(te, "0") == 0) && tiles > kNumCUs && tail > 0 && tail * 2 <= kNumCUs)
+      ts = (int)std::min<int64_t>(std::min<int64_t>(4, kNumCUs / tail), K / (8 * 64));
+    if (ts < 2) ts = 0;
+    if (best == 0) return launch_gemm_bf16<CfgBig8>(x, W, bias, y, M, N, K, s, 1, nullptr, ts);
+    if (best == 1) return launch_gemm_bf16<CfgT192>(x, W, bias, y, M, N, K, s, 1, nullptr, ts);
+    return launch_gemm_bf16<CfgMid>(x, W, bias, y, M, N, K, s, 1, nullptr, ts);
   }
 #endif
   const dim3 grid((unsigned)((N + 63) / 64), (unsigned)((M + 63) / 64));

@@ -136,6 +136,32 @@ def test_linear_split_k(ops, monkeypatch, M, N, K, bias):
     assert_close(f64(y.cpu()), oracle.linear(f64(x), f64(W), None if b is None else f64(b)), "bf16", "linear")
 
 
+@pytest.mark.parametrize("tile,M,N,K,bias", [("256x256", 4352, 4096, 1024, True), ("256x256", 4300, 4104, 2056, False),
+                                             ("192x256", 4352, 4096, 1024, False)])
+def test_linear_split_tail(ops, monkeypatch, tile, M, N, K, bias):
+    """More tiles than CUs with the last round at most half full: those tiles
+    run as 2-4 K ranges (fp32 partials summed in split order) in the same
+    launch as the others.  Ragged M, N and K, bias; bitwise equal across
+    calls; the same result with the split tail turned off."""
+    import torch
+    say(f"linear bf16 split tail tile={tile} M={M} N={N} K={K} bias={bias}")
+    monkeypatch.setenv("OPSCALE_GEMM_TILE", tile)
+    monkeypatch.delenv("OPSCALE_GEMM_TAIL", raising=False)
+    x = gen(26, "x", (M, K), "bf16")
+    W = gen(26, "w_qkv", (N, K), "bf16", std=0.02)
+    b = gen(26, "bias", (N,), "bf16") if bias else None
+    args = (cuda(x), cuda(W), None if b is None else cuda(b))
+    y = ops.opscale_linear(*args)
+    y2 = ops.opscale_linear(*args)
+    monkeypatch.setenv("OPSCALE_GEMM_TAIL", "0")
+    y0 = ops.opscale_linear(*args)
+    torch.cuda.synchronize()
+    assert torch.equal(y, y2)
+    ref = oracle.linear(f64(x), f64(W), None if b is None else f64(b))
+    assert_close(f64(y.cpu()), ref, "bf16", "linear split tail")
+    assert_close(f64(y0.cpu()), ref, "bf16", "linear without split tail")
+
+
 def test_linear_identity_weight(ops):
     """W = I (bf16-exact) returns x exactly: no accumulation rounding occurs."""
     import torch
