@@ -30,6 +30,9 @@ namespace opscale {
 namespace {
 
 constexpr int kNumCUs = 256;  // MI355X compute units
+#ifndef OPSCALE_GEMM_GROUP_MB
+#define OPSCALE_GEMM_GROUP_MB 16  // x rows per tile group, in MB (see launch_gemm_bf16)
+#endif
 constexpr int64_t kSplitKMaxM = 2048;  // split-K is for small M (decode batches)
 
 // Tile configuration: BM x BN block tile, K in slices of BK, WGM x WGN waves
@@ -560,7 +563,7 @@ static hipError_t launch_gemm_bf16(const void* x, const void* W, const void* bia
   // Tile-rows per group: as many as keep the group's x rows (BM x K bf16 each)
   // within 16 MB, so they stay in the last-level cache while the group sweeps
   // the tile-columns; at least one, at most all.
-  constexpr int64_t kGroupBytes = 16ll << 20;
+  constexpr int64_t kGroupBytes = (int64_t)OPSCALE_GEMM_GROUP_MB << 20;
   const int64_t row_block_bytes = (int64_t)C::BM * K * 2;
   const int group_m = (int)std::max<int64_t>(1, std::min<int64_t>(tiles_m, kGroupBytes / row_block_bytes));
   if (tail_splits > 1) {
