@@ -89,24 +89,45 @@ hipError_t launch_rope(void* q, void* k, int64_t q_stride, int64_t k_stride, con
 }
 
 // ------------------------------------------------------- KV cache write ----
-// One workgroup per token: the first half of the threads' 16-byte chunks copy
-// the token's K row (Hkv x D elements), the second half its V row, to cache
-// row `slot` (the cache [num_blocks, block_size, Hkv, D] is an array of such
-// rows).  Tokens whose slot is outside [0, num_slots) are skipped.
+// The rows to copy are a list of 16-byte chunks: token t owns chunks
+// [t * 2 * row_chunks, (t + 1) * 2 * row_chunks), its K row first, then its V
+// row, each copied to cache row `slot` (the cache [num_blocks, block_size,
+// Hkv, D] is an array of such rows).  A workgroup takes kChunksPerWg
+// consecutive chunks, a thread kCwPerThread of them 256 apart: every load (the
+// row chunks and their tokens' slots) is issued before the first store.
+// Tokens whose slot is outside [0, num_slots) are skipped.
+constexpr int kCwPerThread = 4;
+constexpr int kChunksPerWg = 256 * kCwPerThread;
 __global__ __launch_bounds__(256) void cache_write_kernel(const char* __restrict__ k, const char* __restrict__ v,
                                                          int64_t kv_stride_bytes, char* kc, char* vc,
                                                          const int32_t* __restrict__ slots, int row_chunks,
-                                                         int64_t num_slots) {
-  const int64_t t = blockIdx.x;
-  const int64_t slot = slots[t];
-  if (slot < 0 || slot >= num_slots) return;
-  for (int c = threadIdx.x; c < 2 * row_chunks; c += 256) {
+                                                         int64_t T, int64_t num_slots) {
+  const int64_t total = T * 2 * row_chunks;
+  for (int64_t blk = blockIdx.x; blk * kChunksPerWg < total; blk += gridDim.x) {
+  const int64_t q0 = blk * kChunksPerWg + threadIdx.x;
+  u32x4 val[kCwPerThread];
+  int64_t slot[kCwPerThread];
+#pragma unroll
+  for (int i = 0; i < kCwPerThread; ++i) {
+    const int64_t q = min(q0 + i * 256, total - 1);  // clamped: the stores below check q
+    const int64_t t = q / (2 * row_chunks);
+    const int c = (int)(q - t * 2 * row_chunks);
     const bool isv = c >= row_chunks;
-    const int cc = isv ? c - row_chunks : c;
-    const u32x4 val = __builtin_nontemporal_load(
-        reinterpret_cast<const u32x4*>((isv ? v : k) + t * kv_stride_bytes) + cc);
-    *(reinterpret_cast<u32x4*>((isv ? vc : kc) + slot * (int64_t)row_chunks * 16) + cc) = val;
+    val[i] = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>((isv ? v : k) + t * kv_stride_bytes) +
+                                        (isv ? c - row_chunks : c));
+    slot[i] = slots[t];
   }
+#pragma unroll
+  for (int i = 0; i < kCwPerThread; ++i) {
+    const int64_t q = q0 + i * 256;
+    if (q >= total || slot[i] < 0 || slot[i] >= num_slots) continue;
+    const int64_t t = q / (2 * row_chunks);
+    const int c = (int)(q - t * 2 * row_chunks);
+    const bool isv = c >= row_chunks;
+    *(reinterpret_cast<u32x4*>((isv ? vc : kc) + slot[i] * (int64_t)row_chunks * 16) + (isv ? c - row_chunks : c)) =
+        val[i];
+  }
+  }  // block stride
 }
 
 hipError_t launch_cache_write(const void* k, const void* v, int64_t kv_stride, void* kc, void* vc,
@@ -114,9 +135,11 @@ hipError_t launch_cache_write(const void* k, const void* v, int64_t kv_stride, v
                               bool bf16, hipStream_t s) {
   const int es = bf16 ? 2 : 4;
   const int row_chunks = (int)((int64_t)Hkv * D * es / 16);
-  hipLaunchKernelGGL(cache_write_kernel, dim3((unsigned)T), dim3(256), 0, s, static_cast<const char*>(k),
-                     static_cast<const char*>(v), kv_stride * es, static_cast<char*>(kc), static_cast<char*>(vc),
-                     slots, row_chunks, num_slots);
+  const int64_t total = T * 2 * row_chunks;
+  const int64_t blocks = std::min<int64_t>((total + kChunksPerWg - 1) / kChunksPerWg, 1 << 20);
+  hipLaunchKernelGGL(cache_write_kernel, dim3((unsigned)blocks), dim3(256), 0, s,
+                     static_cast<const char*>(k), static_cast<const char*>(v), kv_stride * es,
+                     static_cast<char*>(kc), static_cast<char*>(vc), slots, row_chunks, T, num_slots);
   return hipGetLastError();
 }
 
@@ -176,7 +199,7 @@ __global__ __launch_bounds__(256) void add_rmsnorm_kernel(const void* x, void* r
       for (int e = 0; e < EPV; ++e) sum[i][e] = 0.f;
     }
   }
-  ss = wave_sum(ss);
+  ss = wave_sum_f(ss);
   const float r = rsqrtf(ss / (float)H + eps);
 #pragma unroll
   for (int i = 0; i < VPL; ++i) {

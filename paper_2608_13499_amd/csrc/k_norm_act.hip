@@ -58,20 +58,27 @@ __global__ __launch_bounds__(256) void rmsnorm_kernel(const void* x, const void*
 
   float ss = 0.f;
   if constexpr (VPL > 0) {
-    u32x4 v[VPL];
+    // the row and the weight are requested together, so the weight (an L2
+    // hit) costs no round trip after the reduction
+    u32x4 v[VPL], g[VPL];
 #pragma unroll
     for (int i = 0; i < VPL; ++i) {
       const int idx = lane + i * 64;
       v[i] = idx < nvec ? __builtin_nontemporal_load(xr + idx) : u32x4{0u, 0u, 0u, 0u};
     }
 #pragma unroll
+    for (int i = 0; i < VPL; ++i) {
+      const int idx = lane + i * 64;
+      g[i] = idx < nvec ? wr[idx] : u32x4{0u, 0u, 0u, 0u};
+    }
+#pragma unroll
     for (int i = 0; i < VPL; ++i) ss += sq(v[i]);
-    ss = wave_sum(ss);
+    ss = wave_sum_f(ss);
     const float r = rsqrtf(ss / (float)H + eps);
 #pragma unroll
     for (int i = 0; i < VPL; ++i) {
       const int idx = lane + i * 64;
-      if (idx < nvec) __builtin_nontemporal_store(scale(v[i], wr[idx], r), yr + idx);
+      if (idx < nvec) __builtin_nontemporal_store(scale(v[i], g[i], r), yr + idx);
     }
   } else {
     for (int idx = lane; idx < nvec; idx += 64) ss += sq(xr[idx]);
