@@ -59,6 +59,9 @@ using CfgBig8 = GemmCfg<256, 256, 64, 2, 4, 2>;    // 8 waves of 128x64, 2 x 64 
 using CfgT192 = GemmCfg<192, 256, 64, 2, 4, 2>;    // 8 waves of 96x64, 2 x 56 KB stages
 using CfgMid = GemmCfg<256, 128, 64, 2, 2, 3>;     // 4 waves of 128x64, 3 x 48 KB stages
 using CfgRow64 = GemmCfg<64, 256, 64, 1, 4, 2>;    // 4 waves of 64x64, 2 x 40 KB stages (few rows)
+// split-K tiles for decode-sized M: a K range is short, so the ring is deep
+using CfgSk64 = GemmCfg<64, 256, 64, 1, 4, 4>;     // M <= 64: 4 waves of 64x64, 4 x 40 KB stages
+using CfgSk128 = GemmCfg<128, 256, 64, 2, 4, 3>;   // M <= 128: 8 waves of 64x64, 3 x 48 KB stages
 
 
 // 16-byte chunk c of LDS row r is stored at physical chunk c ^ swz(r).  For
@@ -606,9 +609,10 @@ static hipError_t launch_gemm_bf16(const void* x, const void* W, const void* bia
 // K is cut into floor(kNumCUs / tiles) ranges (each at least 512 wide), so
 // about kNumCUs workgroups run.  (A split that only lifts 129-255 tiles a
 // little past the CU count measured slower than no split.)  0: no split.
+template <class C>
 static int splitk_count(int64_t M, int64_t N, int64_t K) {
   if (M > kSplitKMaxM || K < 1024) return 0;
-  const int64_t tiles = ((M + 255) / 256) * ((N + 127) / 128);
+  const int64_t tiles = ((M + C::BM - 1) / C::BM) * ((N + C::BN - 1) / C::BN);
   const int64_t s = std::min<int64_t>(kNumCUs / tiles, K / 512);
   return s >= 2 ? (int)s : 0;
 }
@@ -663,12 +667,32 @@ hipError_t launch_linear(const void* x, const void* W, const void* bias, void* y
     // stream-ordered scratch, summed in split order by a second kernel).
     // OPSCALE_GEMM_SPLITK=0 turns this off (tuning and tests).
     const char* spk = getenv("OPSCALE_GEMM_SPLITK");
-    const int splits = (spk && strcmp(spk, "0") == 0) || getenv("OPSCALE_GEMM_TILE") ? 0 : splitk_count(M, N, K);
+    const bool spk_off = (spk && strcmp(spk, "0") == 0) || getenv("OPSCALE_GEMM_TILE");
+    // up to 64 rows: 64-row tiles, so the matrix cores do not work on padding
+    // Tile rows by M (64, 128 or 256: the matrix cores work on little
+    // padding); with 256 rows, 256 or 128 columns, whichever gives more
+    // workgroups (ties: 256, which re-reads x half as often).
+    int rows = M <= 64 ? 64 : M <= 128 ? 128 : 256;
+    int splits = 0;
+    if (!spk_off) {
+      if (rows == 64) splits = splitk_count<CfgSk64>(M, N, K);
+      else if (rows == 128) splits = splitk_count<CfgSk128>(M, N, K);
+      else {
+        const int s_wide = splitk_count<CfgBig8>(M, N, K), s_mid = splitk_count<CfgMid>(M, N, K);
+        const int64_t w_wide = (int64_t)s_wide * ((N + 255) / 256), w_mid = (int64_t)s_mid * ((N + 127) / 128);
+        if (w_wide >= w_mid && s_wide > 1) splits = s_wide;
+        else { splits = s_mid; rows = 257; }  // 257: the 256x128 tile
+      }
+    }
     if (splits > 1) {
       void* part = nullptr;
       hipError_t e = scratch_alloc((size_t)splits * M * N * sizeof(float), s, &part);
       if (e != hipSuccess) return e;
-      e = launch_gemm_bf16<CfgMid>(x, W, bias, y, M, N, K, s, splits, static_cast<float*>(part));
+      float* pp = static_cast<float*>(part);
+      e = rows == 64    ? launch_gemm_bf16<CfgSk64>(x, W, bias, y, M, N, K, s, splits, pp)
+          : rows == 128 ? launch_gemm_bf16<CfgSk128>(x, W, bias, y, M, N, K, s, splits, pp)
+          : rows == 256 ? launch_gemm_bf16<CfgBig8>(x, W, bias, y, M, N, K, s, splits, pp)
+                        : launch_gemm_bf16<CfgMid>(x, W, bias, y, M, N, K, s, splits, pp);
       const hipError_t f = scratch_free(part, s);
       return e != hipSuccess ? e : f;
     }
