@@ -696,11 +696,23 @@ hipError_t launch_linear(const void* x, const void* W, const void* bias, void* y
       const hipError_t f = scratch_free(part, s);
       return e != hipSuccess ? e : f;
     }
-    // One workgroup per CU at a time, so a launch runs in ceil(tiles / 256)
-    // rounds.  Pick the tile whose rounds x tile area x relative per-element
-    // cost is smallest: 256x256 moves the fewest operand bytes per flop,
-    // 192x256 (about 15 % more per element) and 256x128 (about 30 % more)
-    // fill the last round better when 256x256 would leave it mostly idle.
+    // A last round at most half full runs split over K: 2-4 ranges per tile
+    // (at most one workgroup per CU in all), each at least 8 slices long.
+    // OPSCALE_GEMM_TAIL=0 turns this off (tuning and tests).
+    const char* te = getenv("OPSCALE_GEMM_TAIL");
+    const bool tail_off = te && strcmp(te, "0") == 0;
+    auto tail_splits = [&](int64_t tiles) {
+      const int64_t tail = tiles % kNumCUs;
+      if (tail_off || tiles <= kNumCUs || tail == 0 || tail * 2 > kNumCUs) return 0;
+      const int ts = (int)std::min<int64_t>(std::min<int64_t>(4, kNumCUs / tail), K / (8 * 64));
+      return ts < 2 ? 0 : ts;
+    };
+    // One workgroup per CU at a time, so a launch runs in full rounds plus a
+    // last one (a split last round counts as 1 / splits of a round).  Pick
+    // the tile whose rounds x tile area x relative per-element cost is
+    // smallest: 256x256 moves the fewest operand bytes per flop, 192x256
+    // (about 15 % more per element) and 256x128 (about 30 % more) fill the
+    // last round better when 256x256 would leave it mostly idle.
     struct Choice { int bm, bn; double cost; };
     const Choice choices[] = {{256, 256, 1.0}, {192, 256, 1.15}, {256, 128, 1.3}};
     int best = 0;
@@ -715,19 +727,12 @@ hipError_t launch_linear(const void* x, const void* W, const void* bias, void* y
         if (strcmp(force, name) == 0) { best = c; break; }
       }
       const int64_t tiles = ((M + choices[c].bm - 1) / choices[c].bm) * ((N + choices[c].bn - 1) / choices[c].bn);
-      const double t = (double)((tiles + kNumCUs - 1) / kNumCUs) * choices[c].bm * choices[c].bn * choices[c].cost;
+      const int ts = tail_splits(tiles);
+      const double rounds = (double)(tiles / kNumCUs) + (tiles % kNumCUs == 0 ? 0.0 : ts ? 1.0 / ts : 1.0);
+      const double t = rounds * choices[c].bm * choices[c].bn * choices[c].cost;
       if (c == 0 || t < best_t) { best = c; best_t = t; }
     }
-    // A last round at most half full runs split over K: 2-4 ranges per tile
-    // (at most one workgroup per CU in all), each at least 8 slices long.
-    // OPSCALE_GEMM_TAIL=0 turns this off (tuning and tests).
-    const int64_t tiles = ((M + choices[best].bm - 1) / choices[best].bm) * ((N + choices[best].bn - 1) / choices[best].bn);
-    const int64_t tail = tiles % kNumCUs;
-    const char* te = getenv("OPSCALE_GEMM_TAIL");
-    int ts = 0;
-    if (!(te && strcmp(te, "0") == 0) && tiles > kNumCUs && tail > 0 && tail * 2 <= kNumCUs)
-      ts = (int)std::min<int64_t>(std::min<int64_t>(4, kNumCUs / tail), K / (8 * 64));
-    if (ts < 2) ts = 0;
+    const int ts = tail_splits(((M + choices[best].bm - 1) / choices[best].bm) * ((N + choices[best].bn - 1) / choices[best].bn));
     if (best == 0) return launch_gemm_bf16<CfgBig8>(x, W, bias, y, M, N, K, s, 1, nullptr, ts);
     if (best == 1) return launch_gemm_bf16<CfgT192>(x, W, bias, y, M, N, K, s, 1, nullptr, ts);
     return launch_gemm_bf16<CfgMid>(x, W, bias, y, M, N, K, s, 1, nullptr, ts);
