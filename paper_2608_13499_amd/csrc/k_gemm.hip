@@ -153,6 +153,11 @@ struct GroupedGemm {
   int E;
   int x_rows;
   int64_t w_stride;       // elements from one expert's W to the next
+  // > 0: W is a gate-up projection [2F, K] (gate rows first) and y the SwiGLU
+  // activation [rows, F]: output column c of the GEMM is gate row c / 2 (even
+  // c) or up row F + c / 2 (odd c), so each lane's runs of 4 columns hold two
+  // (gate, up) pairs and the epilogue stores silu(gate) * up.  N = 2F.
+  int swiglu_f;
 };
 
 template <class C, bool GROUPED = false>
@@ -234,8 +239,11 @@ __global__ __launch_bounds__(C::kThreads, 1) void gemm_bf16_kernel(const __bf16*
   const __amdgpu_buffer_rsrc_t xr =
       GROUPED ? make_rsrc(x + k_begin, (uint32_t)(((int64_t)gg.x_rows - 1) * ld * 2 + (int64_t)K * 2))
               : make_rsrc(x + (int64_t)m0 * ld + k_begin, (uint32_t)(((int64_t)(m_rows - 1) * ld + K) * 2));
-  const __amdgpu_buffer_rsrc_t wr = make_rsrc(W + (int64_t)n0 * ld + k_begin,
-                                              (uint32_t)(((int64_t)(min(BN, N - n0) - 1) * ld + K) * 2));
+  // W: the tile's rows (fused SwiGLU: the expert's whole gate-up weight)
+  const bool fused = GROUPED && gg.swiglu_f > 0;
+  const __amdgpu_buffer_rsrc_t wr =
+      fused ? make_rsrc(W + k_begin, (uint32_t)(((int64_t)N - 1) * ld * 2 + (int64_t)K * 2))
+            : make_rsrc(W + (int64_t)n0 * ld + k_begin, (uint32_t)(((int64_t)(min(BN, N - n0) - 1) * ld + K) * 2));
   // byte offsets of the rows this lane loads (per load group)
   constexpr int LX = BM / C::kRowsPerLoad / C::kWaves, LW = BN / C::kRowsPerLoad / C::kWaves;
   uint32_t xro[LX], wro[LW];
@@ -250,8 +258,15 @@ __global__ __launch_bounds__(C::kThreads, 1) void gemm_bf16_kernel(const __bf16*
     }
   }
 #pragma unroll
-  for (int g = 0; g < LW; ++g)
-    wro[g] = (uint32_t)((int64_t)((g * C::kWaves + wave) * C::kRowsPerLoad + lane / C::kCPR) * ld * 2);
+  for (int g = 0; g < LW; ++g) {
+    const int r = (g * C::kWaves + wave) * C::kRowsPerLoad + lane / C::kCPR;
+    if (fused) {
+      const int c = n0 + r;  // interleaved column: gate row c / 2, up row F + c / 2
+      wro[g] = c < N ? (uint32_t)((int64_t)((c & 1) ? gg.swiglu_f + (c >> 1) : (c >> 1)) * ld * 2) : kNoRow;
+    } else {
+      wro[g] = (uint32_t)((int64_t)r * ld * 2);
+    }
+  }
 
   f32x4 acc[TN][TM];
 #pragma unroll
@@ -422,6 +437,19 @@ __global__ __launch_bounds__(C::kThreads, 1) void gemm_bf16_kernel(const __bf16*
   for (int j = 0; j < TM; ++j) {
     const int m = m0 + wm * WM + j * MI + fr;
     if (m - m0 >= m_rows) continue;
+    if (fused) {
+      // two (gate, up) pairs per lane: act[m][n / 2], act[m][n / 2 + 1]
+      __bf16* arow = y + (int64_t)m * gg.swiglu_f;
+#pragma unroll
+      for (int i = 0; i < TN; ++i) {
+        const int n = n0 + wn * WN + i * MI + fh * 4;
+        if (n >= N) continue;
+        const float g0 = acc[i][j][0], u0 = acc[i][j][1], g1 = acc[i][j][2], u1 = acc[i][j][3];
+        const float a0 = g0 / (1.f + __expf(-g0)) * u0, a1 = g1 / (1.f + __expf(-g1)) * u1;
+        *reinterpret_cast<uint32_t*>(arow + (n >> 1)) = pack_bf2(a0, a1);
+      }
+      continue;
+    }
     __bf16* yrow = y + (int64_t)m * N;
 #pragma unroll
     for (int i = 0; i < TN; ++i) {
@@ -620,7 +648,7 @@ static int splitk_count(int64_t M, int64_t N, int64_t K) {
 template <class C>
 static hipError_t launch_grouped(const void* x, int64_t x_rows, const void* W, int64_t w_stride, void* y,
                                  int64_t max_rows, int64_t N, int64_t K, int32_t E, const int32_t* gather,
-                                 const int32_t* rows, const int32_t* tiles, hipStream_t s) {
+                                 const int32_t* rows, const int32_t* tiles, int32_t swiglu_f, hipStream_t s) {
   static const hipError_t attr = hipFuncSetAttribute(
       reinterpret_cast<const void*>(gemm_bf16_kernel<C, true>), hipFuncAttributeMaxDynamicSharedMemorySize,
       C::kLdsBytes);
@@ -628,7 +656,7 @@ static hipError_t launch_grouped(const void* x, int64_t x_rows, const void* W, i
   // at most ceil(rows / BM) + E tile-rows; workgroups past the list's end return
   const int64_t tile_rows = (max_rows + C::BM - 1) / C::BM + E;
   const int64_t tiles_n = (N + C::BN - 1) / C::BN;
-  GroupedGemm gg{gather, rows, tiles, E, (int)x_rows, w_stride};
+  GroupedGemm gg{gather, rows, tiles, E, (int)x_rows, w_stride, swiglu_f};
   hipLaunchKernelGGL((gemm_bf16_kernel<C, true>), dim3((unsigned)(tile_rows * tiles_n)), dim3(C::kThreads),
                      C::kLdsBytes, s, static_cast<const __bf16*>(x), static_cast<const __bf16*>(W), nullptr,
                      static_cast<__bf16*>(y), (int)max_rows, (int)N, (int)K, 1, (int)K, nullptr, gg, 0, 0);
@@ -643,10 +671,11 @@ int32_t grouped_gemm_tile_rows(int64_t rows, int32_t E) {
 
 hipError_t launch_gemm_grouped(const void* x, int64_t x_rows, const void* W, int64_t w_stride, void* y,
                                int64_t max_rows, int64_t N, int64_t K, int32_t E, int32_t tile_rows,
-                               const int32_t* gather, const int32_t* rows, const int32_t* tiles, hipStream_t s) {
+                               const int32_t* gather, const int32_t* rows, const int32_t* tiles, int32_t swiglu_f,
+                               hipStream_t s) {
   if (tile_rows == CfgRow64::BM)
-    return launch_grouped<CfgRow64>(x, x_rows, W, w_stride, y, max_rows, N, K, E, gather, rows, tiles, s);
-  return launch_grouped<CfgBig8>(x, x_rows, W, w_stride, y, max_rows, N, K, E, gather, rows, tiles, s);
+    return launch_grouped<CfgRow64>(x, x_rows, W, w_stride, y, max_rows, N, K, E, gather, rows, tiles, swiglu_f, s);
+  return launch_grouped<CfgBig8>(x, x_rows, W, w_stride, y, max_rows, N, K, E, gather, rows, tiles, swiglu_f, s);
 }
 
 hipError_t launch_linear(const void* x, const void* W, const void* bias, void* y, int64_t M,

@@ -16,6 +16,9 @@
 #include <algorithm>
 #include <cmath>
 
+#include <cstdlib>
+#include <cstring>
+
 #include "common.h"
 #include "launch.h"
 
@@ -307,13 +310,23 @@ hipError_t launch_fused_moe(const void* x, const void* w1, const void* w2, const
   hipLaunchKernelGGL(moe_scatter_kernel, dim3((unsigned)nb), dim3(64), 0, s, ids, R, E, k, w.counts, w.rows, w.gather,
                      w.pos);
   if ((e = hipGetLastError()) != hipSuccess) return e;
-  // gate_up = W1[e] x[token]   (rows gathered), [R, 2F]
-  if ((e = launch_gemm_grouped(x, T, w1, (int64_t)2 * F * H, w.gate_up, R, 2 * (int64_t)F, H, E, bm, w.gather,
-                               w.rows, w.tiles, s)) != hipSuccess)
-    return e;
-  if ((e = launch_swiglu(w.gate_up, w.act, R, F, true, s)) != hipSuccess) return e;
+  // act = silu(W1g[e] x[token]) * (W1u[e] x[token])   (rows gathered), [R, F]:
+  // the SwiGLU sits in the GEMM's epilogue when an expert's gate-up weight
+  // spans less than 4 GB (32-bit row offsets); else gate_up [R, 2F] first
+  // (OPSCALE_MOE_FUSE=0 forces the unfused path, for tests)
+  const char* fz = getenv("OPSCALE_MOE_FUSE");
+  if ((int64_t)2 * F * H * 2 < ((int64_t)1 << 32) && !(fz && strcmp(fz, "0") == 0)) {
+    if ((e = launch_gemm_grouped(x, T, w1, (int64_t)2 * F * H, w.act, R, 2 * (int64_t)F, H, E, bm, w.gather, w.rows,
+                                 w.tiles, F, s)) != hipSuccess)
+      return e;
+  } else {
+    if ((e = launch_gemm_grouped(x, T, w1, (int64_t)2 * F * H, w.gate_up, R, 2 * (int64_t)F, H, E, bm, w.gather,
+                                 w.rows, w.tiles, 0, s)) != hipSuccess)
+      return e;
+    if ((e = launch_swiglu(w.gate_up, w.act, R, F, true, s)) != hipSuccess) return e;
+  }
   // y = W2[e] act   (sorted rows), [R, H]
-  if ((e = launch_gemm_grouped(w.act, R, w2, (int64_t)H * F, w.y, R, H, F, E, bm, nullptr, w.rows, w.tiles, s)) !=
+  if ((e = launch_gemm_grouped(w.act, R, w2, (int64_t)H * F, w.y, R, H, F, E, bm, nullptr, w.rows, w.tiles, 0, s)) !=
       hipSuccess)
     return e;
   hipLaunchKernelGGL(moe_combine_kernel, dim3((unsigned)T), dim3(256), 0, s, w.y, w.pos, wts,

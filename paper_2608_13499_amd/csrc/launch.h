@@ -23,9 +23,13 @@ hipError_t launch_linear(const void* x, const void* W, const void* bias, void* y
 // rows[E]; y has max_rows rows of N.  tile_rows is
 // grouped_gemm_tile_rows(max_rows, E), the value the tile table was built with.
 int32_t grouped_gemm_tile_rows(int64_t rows, int32_t E);
+// swiglu_f > 0: W is a gate-up weight [2F, K] (N = 2F) and y receives
+// silu(gate) * up, [rows, F] (fused epilogue); every expert's W must then span
+// less than 4 GB.
 hipError_t launch_gemm_grouped(const void* x, int64_t x_rows, const void* W, int64_t w_stride, void* y,
                                int64_t max_rows, int64_t N, int64_t K, int32_t E, int32_t tile_rows,
-                               const int32_t* gather, const int32_t* rows, const int32_t* tiles, hipStream_t s);
+                               const int32_t* gather, const int32_t* rows, const int32_t* tiles, int32_t swiglu_f,
+                               hipStream_t s);
 
 // The small-M (decode batch) bf16 linear: all M rows per workgroup, K split
 // over its waves.  Supported for 1 <= M <= kSkinnyMaxM with K % 32 == 0;
