@@ -55,6 +55,30 @@ def source_sha(kernel: str) -> str:
     return hashlib.sha256(src.encode()).hexdigest()[:16]
 
 
+def gpu_state():
+    """Shader clock, memory clock and package power of GPU 0 as rocm-smi
+    reports them (read from a child process; None where it reports nothing)."""
+    import re
+    import subprocess
+    try:
+        r = subprocess.run(["rocm-smi", "-d", "0", "--showclocks", "--showpower", "--json"],
+                           capture_output=True, text=True, timeout=30)
+        card = next(iter(json.loads(r.stdout).values()))
+    except Exception as ex:  # noqa: BLE001 - the record is informative only
+        return {"error": f"rocm-smi: {type(ex).__name__}"}
+
+    def num(pred):
+        for k, v in card.items():
+            if pred(k.lower()):
+                m = re.search(r"[-+]?\d+(\.\d+)?", str(v))
+                if m:
+                    return float(m.group(0))
+        return None
+    return {"sclk_mhz": num(lambda k: k.startswith("sclk clock speed")),
+            "mclk_mhz": num(lambda k: k.startswith("mclk clock speed")),
+            "power_w": num(lambda k: "power" in k and "(w)" in k)}
+
+
 def measured_traffic(op: str, kernel: str):
     """HBM bytes per launch of `op` (FETCH_SIZE + WRITE_SIZE, calibrated) from
     the committed counter summary, or None when the kernel's source changed
@@ -324,6 +348,7 @@ def main():
     torch.cuda.synchronize()
     n = len(layer.names)
     evs = [[torch.cuda.Event(enable_timing=True) for _ in range(n + 1)] for _ in range(a.steps)]
+    state_before = gpu_state()
     log(f"timing {a.steps} steps ...")
     torch.cuda.synchronize()
     t0 = time.perf_counter()
@@ -331,6 +356,7 @@ def main():
         layer.step(evs[s])
     torch.cuda.synchronize()
     t1 = time.perf_counter()
+    state_after = gpu_state()
     ms_step = (t1 - t0) * 1e3 / a.steps
     per_op_us = {nm: sum(evs[s][i].elapsed_time(evs[s][i + 1]) for s in range(a.steps)) * 1e3 / a.steps
                  for i, nm in enumerate(layer.names)}
@@ -402,6 +428,21 @@ def main():
                               "bound": "mfma" if pr.bound == 0 else "hbm", "roofline_frac": round(pr.roofline_frac, 4)}
         del w1, w2, xm, ids, wts, om, wsm
     del flush
+    # Peaks re-measured on this GPU (sustained clock, real data): the spec
+    # peaks above stay the primary denominators.
+    log("peak probes ...")
+    big = torch.empty(2 << 30, dtype=torch.uint8, device="cuda")
+    big2 = torch.empty_like(big)
+    meas = {"mfma_bf16_tflops": round(ops.opscale_probe_mfma(32768, 10), 1),
+            "hbm_read_gbps": round(ops.opscale_probe_hbm(big, None, 5), 1),
+            "hbm_copy_gbps": round(ops.opscale_probe_hbm(big, big2, 5), 1)}
+    del big, big2
+    meas["spec_bf16_tflops"], meas["spec_hbm_gbps"] = PEAK_BF16 * 1e-12, PEAK_HBM * 1e-9
+    roof["frac_of_measured"] = round(roof["achieved"] / (meas["mfma_bf16_tflops"] if roof["bound"] == "mfma"
+                                                         else meas["hbm_read_gbps"]), 4)
+    for nm, rec in per_op.items():
+        rec["frac_of_measured"] = round(rec["tflops"] / meas["mfma_bf16_tflops"] if rec["bound"] == "mfma"
+                                        else rec["gbps"] / meas["hbm_read_gbps"], 4)
     M = layer.p["M"]
     out = {
         "metric": "per-operator prefill tokens/s + % of MFMA/HBM roofline, Llama-8B-shaped layer",
@@ -417,6 +458,8 @@ def main():
         "roofline": roof,
         "per_op": per_op,
         "extra_ops": extra_ops,
+        "measured_peaks": meas,
+        "gpu_state": {"before": state_before, "after": state_after},
     }
     if not a.no_cpu_baseline:
         log("cpu baseline (oracle) ...")

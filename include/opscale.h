@@ -304,6 +304,31 @@ opscale_status opscale_op_profile(const opscale_op_desc* desc, int32_t warmup, i
                                   opscale_profile* out);
 
 /* ---------------------------------------------------------------------------
+ * Peak probes: what this GPU's matrix cores and HBM deliver, measured, to
+ * report the operators against beside the published peaks (the paper
+ * characterizes each operator by how much of the GPU it uses, Section 2.1).
+ * Blocking; results are means over reps launches after one untimed launch.
+ * ------------------------------------------------------------------------- */
+
+/*
+ * bf16 MFMA throughput: 4 waves per SIMD on every CU, each running 8
+ * independent chains of iters 16x16x32 bf16 MFMAs on register operands
+ * (non-zero values); iters is rounded up to a multiple of 4.  *tflops =
+ * flops / time.  1 <= iters <= 2^24, 1 <= reps <= 1000.
+ */
+opscale_status opscale_probe_mfma(int64_t iters, int32_t reps, hipStream_t stream, double* tflops);
+
+/*
+ * HBM streaming: with dst NULL, read `bytes` of src (DEVICE, 16-byte aligned)
+ * once per launch with 16-byte nontemporal loads (*gbps = bytes / time); with
+ * dst (DEVICE, `bytes`, not overlapping src) copy src to dst (*gbps =
+ * 2 * bytes / time).  Use a buffer well above the 256 MB last-level cache.
+ * bytes a multiple of 16; 1 <= reps <= 1000.
+ */
+opscale_status opscale_probe_hbm(const void* src, void* dst, size_t bytes, int32_t reps, hipStream_t stream,
+                                 double* gbps);
+
+/* ---------------------------------------------------------------------------
  * Mixture-of-experts FFN (the FusedMoE operator of the paper's MoE models,
  * Qwen2-57B-A14B and Mixtral-8x7B: Table 3; Section 2.1 counts it among the
  * compute-heavy linear operators, Appendix D shows it dominating at short

@@ -15,7 +15,7 @@ from ._lib import (  # noqa: F401
     desc_rope, desc_reshape_and_cache, desc_add_rmsnorm,
     opscale_moe_topk, opscale_fused_moe_workspace_size, opscale_fused_moe, desc_fused_moe,
     Corun, opscale_cu_layout, opscale_cu_mask_build, opscale_cu_stream_create, opscale_cu_stream_destroy,
-    opscale_cu_stream_mask, opscale_cu_probe, opscale_corun_profile,
+    opscale_cu_stream_mask, opscale_cu_probe, opscale_probe_mfma, opscale_probe_hbm, opscale_corun_profile,
     OPSCALE_OK, OPSCALE_ERR_INVALID_ARG, OPSCALE_ERR_UNSUPPORTED, OPSCALE_ERR_WORKSPACE,
     OPSCALE_ERR_HIP, OPSCALE_F32, OPSCALE_BF16,
 )

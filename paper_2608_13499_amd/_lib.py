@@ -151,6 +151,8 @@ EXPORTS = {
     "opscale_cu_stream_destroy": (c_i32, [c_vp]),
     "opscale_cu_stream_mask": (c_i32, [c_vp, ctypes.POINTER(ctypes.c_uint32), c_i32]),
     "opscale_cu_probe": (c_i32, [c_vp, c_vp, c_i32, c_i32]),
+    "opscale_probe_mfma": (c_i32, [c_i64, c_i32, c_vp, ctypes.POINTER(c_f64)]),
+    "opscale_probe_hbm": (c_i32, [c_vp, c_vp, c_sz, c_i32, c_vp, ctypes.POINTER(c_f64)]),
     "opscale_corun_profile": (c_i32, [ctypes.POINTER(OpDesc), c_vp, ctypes.POINTER(OpDesc), c_vp, c_i32, c_i32,
                                       c_f32, c_i32, ctypes.POINTER(_CorunTrace), ctypes.POINTER(Corun)]),
 }
@@ -514,6 +516,28 @@ def opscale_cu_probe(out, spins: int = 4, stream=None):
         raise OpscaleError(OPSCALE_ERR_INVALID_ARG, "out must be a contiguous 4-byte [n, 2] tensor")
     _check(load().opscale_cu_probe(_stream(stream), _ptr(out), out.shape[0], spins))
     return out
+
+
+def opscale_probe_mfma(iters: int = 4096, reps: int = 5, stream=None) -> float:
+    """Measured bf16 MFMA throughput of this GPU (TFLOP/s), blocking."""
+    out = c_f64(0.0)
+    _check(load().opscale_probe_mfma(int(iters), int(reps), _stream(stream), ctypes.byref(out)))
+    return out.value
+
+
+def opscale_probe_hbm(src, dst=None, reps: int = 5, stream=None) -> float:
+    """Measured HBM streaming rate (GB/s), blocking: reads of src (a GPU
+    tensor), or with dst (same byte size) a copy, counted as read + write."""
+    _dev(src)
+    nbytes = src.numel() * src.element_size()
+    if dst is not None:
+        _dev(dst)
+        if dst.numel() * dst.element_size() != nbytes:
+            raise OpscaleError(OPSCALE_ERR_INVALID_ARG, "dst must have the byte size of src")
+    out = c_f64(0.0)
+    _check(load().opscale_probe_hbm(_ptr(src), None if dst is None else _ptr(dst), nbytes, int(reps),
+                                    _stream(stream), ctypes.byref(out)))
+    return out.value
 
 
 def opscale_corun_profile(desc_a: OpDesc, stream_a, desc_b: OpDesc, stream_b, warmup: int = 3,

@@ -30,7 +30,7 @@ def test_header_declares_expected_entry_points():
                  "opscale_version", "opscale_status_string", "opscale_last_error",
                  "opscale_rope", "opscale_reshape_and_cache", "opscale_add_rmsnorm",
                  "opscale_cu_layout", "opscale_cu_mask_build", "opscale_cu_stream_create",
-                 "opscale_cu_stream_destroy", "opscale_cu_stream_mask", "opscale_cu_probe",
+                 "opscale_cu_stream_destroy", "opscale_cu_stream_mask", "opscale_cu_probe", "opscale_probe_mfma", "opscale_probe_hbm",
                  "opscale_corun_profile", "opscale_moe_topk", "opscale_fused_moe",
                  "opscale_fused_moe_workspace_size"):
         assert name in d
@@ -237,6 +237,19 @@ def test_profile_descriptor_layout_matches_header(tmp_path):
     for m, cls in members.items():
         for f, _ in cls._fields_:
             assert int(out[f"{m}.{f}"]) == getattr(cls, f).offset, f"{m}.{f}"
+
+
+def test_probe_validation(lib):
+    """The peak probes reject bad arguments before touching a device."""
+    import ctypes
+    out = ctypes.c_double(0.0)
+    assert lib.opscale_probe_mfma(0, 5, None, ctypes.byref(out)) == 1          # iters < 1
+    assert lib.opscale_probe_mfma(16, 0, None, ctypes.byref(out)) == 1         # reps < 1
+    assert lib.opscale_probe_mfma(16, 5, None, None) == 1                      # no result pointer
+    assert lib.opscale_probe_hbm(None, None, 1 << 20, 5, None, ctypes.byref(out)) == 1
+    assert lib.opscale_probe_hbm(A16, None, 100, 5, None, ctypes.byref(out)) == 1      # not a multiple of 16
+    assert lib.opscale_probe_hbm(A16 + 8, None, 1 << 20, 5, None, ctypes.byref(out)) == 1  # misaligned
+    assert lib.opscale_probe_hbm(A16, None, 1 << 20, 0, None, ctypes.byref(out)) == 1  # reps < 1
 
 
 def test_moe_validation(lib):
