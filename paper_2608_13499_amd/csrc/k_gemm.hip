@@ -51,7 +51,10 @@ struct GemmCfg {
   static constexpr int kLoadsPerTile = (BM + BN) / kRowsPerLoad / kWaves;  // per wave
   static_assert(BM % (kRowsPerLoad * kWaves) == 0 && BN % (kRowsPerLoad * kWaves) == 0,
                 "each operand's rows must split evenly over the waves");
-  static_assert(BK % 32 == 0, "an even number of 16-wide k-steps per slice");
+  // The fragment double buffer alternates by k-step within a slice and
+  // restarts at buffer 0 in the next, so a slice must hold an even number of
+  // 32-wide k-steps; the LDS swizzle assumes 128-byte rows.
+  static_assert(BK == 64, "64-wide K slices: two 32-wide k-steps of 128-byte rows");
   static_assert(kLoadsPerTile * (STAGES - 2 > 0 ? STAGES - 2 : 0) <= 63, "vmcnt range");
 };
 
@@ -70,14 +73,14 @@ using CfgSk128 = GemmCfg<128, 256, 64, 2, 4, 3>;   // M <= 128: 8 waves of 64x64
 // lane (lanes in 4-lane blocks, blocks of odd and even bit parity alternating;
 // measured).  A 16x16x32 operand read puts row lane % 16 and logical chunk
 // 4 ks + lane / 16 in each lane, so a pass holds 8 rows of one parity class at
-// each of two chunks; the swizzle below gives those 16 lanes 16 distinct
-// 16-byte bank groups for both k-steps of a 64-wide slice.  swz depends only
+// each of two chunks; XOR with the row mod 8 gives those 16 lanes 16
+// distinct 16-byte bank groups for both k-steps of a 64-wide slice.  swz depends only
 // on the row mod 16, i.e. on the lane, so one per-lane offset per K step
 // serves every 16-row fragment of a wave (the rest is an immediate offset).
 template <int CPR>
 __device__ __forceinline__ int swz(int r) {
-  if constexpr (CPR == 8) return r & 7;  // 128-byte rows
-  else return (r >> 1) & 3;              // 64-byte rows
+  static_assert(CPR == 8, "128-byte rows");
+  return r & 7;
 }
 
 // s_waitcnt with only the vector-memory counter constrained (gfx9 encoding:
