@@ -158,7 +158,7 @@ size_t opscale_attn_decode_workspace_size(int32_t B, int32_t Hq, int32_t D,
  * skipped is zero.
  * max_context_len: the expected largest context length; it sizes the
  *   split-KV launch (one workgroup per 32 keys of B x max_context_len, at most
- *   2048, each taking an equal share of the keys actually present) and the
+ *   256, each taking an equal share of the keys actually present) and the
  *   workspace.  Longer contexts are still served whole; the value changes
  *   only how the keys are split, so results agree to rounding across values.
  * workspace: DEVICE scratch of at least opscale_attn_decode_workspace_size(B,

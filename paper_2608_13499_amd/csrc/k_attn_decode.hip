@@ -6,10 +6,10 @@
 // builds it in LDS from the context lengths (one lane a sequence), beyond that
 // a one-workgroup plan kernel writes it, with each workgroup's first sequence,
 // to the workspace.  A fixed grid of nwg workgroups (one per tile of B x
-// max_context_len keys, at most 512 in all, two per CU so that the grid runs
-// in one round, and 64 per sequence) takes equal consecutive ranges of the
-// tile list, so every workgroup streams the same number of keys
-// however ragged the contexts are, and a range may span sequence boundaries.
+// max_context_len keys, at most 256 in all, one per CU, and 64 per sequence)
+// takes equal consecutive ranges of the tile list, so every workgroup streams
+// the same number of keys however ragged the contexts are, and a range may
+// span sequence boundaries.
 // Each (workgroup g, sequence b) segment of the range is processed on its own
 // and leaves (max, sum, unnormalized output) in slot g + b of the caller's
 // workspace: unique, as the ranges are ordered like the sequences.
@@ -27,9 +27,9 @@
 //     A operand P (a lane holds one head and 8 keys), and V, DMA'd into LDS
 //     row-major, is read as the B operand with ds_read_b64_tr_b16.
 // A wave loads a tile and waits for it; the latency is covered by the other
-// waves of the CU: with one V buffer per wave (64 KB of LDS) and at most 128
-// VGPRs, two workgroups (16 waves) share a CU.  V is read with the
-// nontemporal hint, the cache is streamed once.
+// waves of the CU (one V buffer per wave: 64 KB of LDS, at most 128 VGPRs;
+// the grid gives each CU one workgroup).  V is read with the nontemporal
+// hint, the cache is streamed once.
 // A second kernel merges the segments of a (sequence, head) in workgroup
 // order, so the result is deterministic; for small batches it recomputes the
 // sequence's tile range from the context lengths instead of reading the plan
@@ -52,14 +52,15 @@ constexpr int kTile = 32;    // keys per wave step
 constexpr int kWaves = 8;    // waves per workgroup
 constexpr int kChunk = 512;  // keys per page window
 #ifndef OPSCALE_DECODE_MAX_WG
-#define OPSCALE_DECODE_MAX_WG 512
+#define OPSCALE_DECODE_MAX_WG 256
 #endif
 #ifndef OPSCALE_DECODE_SEQ_WG
 #define OPSCALE_DECODE_SEQ_WG 64
 #endif
-// Workgroups of a launch, at most (two per CU: one round of the grid); and per
-// sequence of the batch, at most (so a sequence's merge takes about one
-// 64-wide pass).
+// Workgroups of a launch, at most (one per CU: the grid runs in one round,
+// and 8 waves per CU keep fewer loads in flight, which streams HBM faster
+// than 16 did); and per sequence of the batch, at most (so a sequence's merge
+// takes about one 64-wide pass).
 constexpr int kMaxWorkgroups = OPSCALE_DECODE_MAX_WG;
 constexpr int kSeqWorkgroups = OPSCALE_DECODE_SEQ_WG;
 constexpr int kInlineB = kWaves * 64;  // up to this batch every workgroup builds the plan itself
@@ -336,8 +337,7 @@ __global__ __launch_bounds__(512, 4) void attn_decode_split_kernel(
   };
 
   // Each wave loads a tile, waits for it and uses it; latency is hidden by
-  // the other waves of the CU (two workgroups of 8 waves fit: 64 KB of LDS
-  // and at most 128 VGPRs each), not by register double buffering.  V is
+  // the other 7 waves of the CU, not by register double buffering.  V is
   // refilled only after the previous tile's transposed reads fed its MFMAs.
   KRegs cur;
   for (int w0 = k_begin; w0 < k_end; w0 += kChunk) {

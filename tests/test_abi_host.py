@@ -110,14 +110,14 @@ def test_decode_validation_and_workspace(lib):
     f = lib.opscale_attn_decode
     need = lib.opscale_attn_decode_workspace_size(256, 32, 128, 8192)
     # balanced split-KV: one workgroup per 32-key tile of B x max_context_len
-    # keys, at most 512 and 64 per sequence; the tile prefix sums (B + 1 int64), above 512
+    # keys, at most 256 and 64 per sequence; the tile prefix sums (B + 1 int64), above 512
     # sequences each workgroup's first sequence (int32), each 256-byte aligned,
     # then (workgroups + B) x Hq partials of D + 2 floats
     def ws(B, Hq, D, mc):
-        nwg = min(512, B * -(-mc // 32), 64 * B)
+        nwg = min(256, B * -(-mc // 32), 64 * B)
         up = lambda x: (x + 255) // 256 * 256
         return up(8 * (B + 1)) + (up(4 * nwg) if B > 512 else 0) + 4 * (nwg + B) * Hq * (D + 2)
-    assert need == ws(256, 32, 128, 8192) == 2304 + 4 * (512 + 256) * 32 * 130
+    assert need == ws(256, 32, 128, 8192) == 2304 + 4 * (256 + 256) * 32 * 130
     assert lib.opscale_attn_decode_workspace_size(1, 32, 128, 2048) == 256 + 4 * (64 + 1) * 32 * 130
     assert lib.opscale_attn_decode_workspace_size(1, 32, 128, 8192) == 256 + 4 * (64 + 1) * 32 * 130
     for B, Hq, D, mc in [(1, 32, 128, 8192), (16, 32, 128, 2048), (64, 32, 128, 2048), (3, 8, 64, 33),
