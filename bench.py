@@ -59,9 +59,14 @@ def gpu_state():
     """Shader clock, memory clock and package power of GPU 0 as rocm-smi
     reports them (read from a child process; None where it reports nothing)."""
     import re
+    import shutil
     import subprocess
     try:
-        r = subprocess.run(["rocm-smi", "-d", "0", "--showclocks", "--showpower", "--json"],
+        # rocm-smi is a Python script: run it with this interpreter, so that
+        # the child starts it directly (no #!/usr/bin/env hop that would exec
+        # a second program).
+        script = os.path.realpath(shutil.which("rocm-smi") or "/opt/rocm/bin/rocm-smi")
+        r = subprocess.run([sys.executable, script, "-d", "0", "--showclocks", "--showpower", "--json"],
                            capture_output=True, text=True, timeout=30)
         card = next(iter(json.loads(r.stdout).values()))
     except Exception as ex:  # noqa: BLE001 - the record is informative only
