@@ -149,6 +149,25 @@ class Layer:
         ops.opscale_attn_decode(d["q"], d["k_cache"], d["v_cache"], d["block_table"], d["context_lens"],
                                 d["max_context_len"], self.scale, workspace=self.ws, out=self.dout); mark(9)
 
+    def step_descs(self):
+        """(name, descriptor) of each operator of the step, on the step's own buffers."""
+        ops, p, d = self.ops, self.p, self.d
+        eps = self.pc.eps
+        return [
+            ("rmsnorm_1", ops.desc_rmsnorm(p["x"], p["w_norm1"], self.h1, eps)),
+            ("qkv_linear", ops.desc_linear(self.h1, p["w_qkv"], self.qkv)),
+            ("attn_prefill", ops.desc_attn_prefill(self.q, self.k, self.v, self.attn, p["cu_seqlens"],
+                                                   self.max_seqlen, self.scale, True)),
+            ("o_linear", ops.desc_linear(self.attn.view(self.p["M"], -1), p["w_o"], self.o)),
+            ("rmsnorm_2", ops.desc_rmsnorm(self.o, p["w_norm2"], self.h2, eps)),
+            ("gate_up_linear", ops.desc_linear(self.h2, p["w_gate_up"], self.gu)),
+            ("swiglu", ops.desc_swiglu(self.gu, self.act)),
+            ("down_linear", ops.desc_linear(self.act, p["w_down"], self.y)),
+            ("attn_decode", ops.desc_attn_decode(d["q"], d["k_cache"], d["v_cache"], d["block_table"],
+                                                 d["context_lens"], self.dout, d["max_context_len"], self.scale,
+                                                 self.ws)),
+        ]
+
     def setup_extras(self):
         """Operands of the operators around attention at the same shape: RoPE on
         the packed QKV output, the write of every token's k / v into a shuffled
@@ -389,6 +408,28 @@ def main():
     roof["traffic"] = measured_traffic(dom, kernel)
     roof["kernel"] = f"{kernel} ({dom})"
     roof["work_per_launch"] = {"flops": fl, "bytes": by}
+    # Each operator of the step alone on its stream: with a 512 MiB write
+    # between iterations (primary: weights and activations come from HBM, not
+    # the 256 MB last-level cache) and warm, median / p10 / p90 of HIP events,
+    # with the clocks before and after.
+    flush = torch.empty(512 << 20, dtype=torch.uint8, device="cuda")
+    iso_iters = max(20, a.steps)
+    isolated = {}
+    for nm, desc in layer.step_descs():
+        before = gpu_state()
+        pf = ops.opscale_op_profile(desc, 5, iso_iters, flush)
+        pw = ops.opscale_op_profile(desc, 5, iso_iters, None)
+        after = gpu_state()
+        isolated[nm] = {
+            "flushed": {"us_median": round(pf.us_median, 2), "us_p10": round(pf.us_p10, 2),
+                        "us_p90": round(pf.us_p90, 2), "roofline_frac": round(pf.roofline_frac, 4)},
+            "warm": {"us_median": round(pw.us_median, 2), "us_p10": round(pw.us_p10, 2),
+                     "us_p90": round(pw.us_p90, 2), "roofline_frac": round(pw.roofline_frac, 4)},
+            "sclk_mhz": [before.get("sclk_mhz"), after.get("sclk_mhz")],
+            "mclk_mhz": [before.get("mclk_mhz"), after.get("mclk_mhz")],
+            "power_w": [before.get("power_w"), after.get("power_w")],
+        }
+    del flush
     # The operators around attention of a full layer (RoPE, cache write,
     # residual + norm), timed separately: they are not part of the step.
     layer.setup_extras()
@@ -463,6 +504,7 @@ def main():
         "roofline": roof,
         "per_op": per_op,
         "extra_ops": extra_ops,
+        "isolated": isolated,
         "measured_peaks": meas,
         "gpu_state": {"before": state_before, "after": state_after},
     }
