@@ -250,6 +250,8 @@ def test_probe_validation(lib):
     assert lib.opscale_probe_hbm(A16, None, 100, 5, None, ctypes.byref(out)) == 1      # not a multiple of 16
     assert lib.opscale_probe_hbm(A16 + 8, None, 1 << 20, 5, None, ctypes.byref(out)) == 1  # misaligned
     assert lib.opscale_probe_hbm(A16, None, 1 << 20, 0, None, ctypes.byref(out)) == 1  # reps < 1
+    assert lib.opscale_probe_hbm(A16, A16 + 4096, 1 << 20, 5, None, ctypes.byref(out)) == 1  # dst overlaps src
+    assert lib.opscale_probe_hbm(A16 + 4096, A16, 1 << 20, 5, None, ctypes.byref(out)) == 1  # src overlaps dst
 
 
 def test_moe_validation(lib):

@@ -59,3 +59,6 @@ def test_probe_rejects(ops):
     src = torch.ones(1024, dtype=torch.int16, device="cuda")
     with pytest.raises(ops.OpscaleError):
         ops.opscale_probe_hbm(src, torch.empty(8, dtype=torch.int16, device="cuda"))
+    buf = torch.zeros(2048, dtype=torch.int16, device="cuda")
+    with pytest.raises(ops.OpscaleError):  # the copy's source and destination overlap
+        ops.opscale_probe_hbm(buf[:1024], buf[512:1536])
