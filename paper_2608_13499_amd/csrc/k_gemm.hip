@@ -704,16 +704,22 @@ hipError_t launch_linear(const void* x, const void* W, const void* bias, void* y
     // OPSCALE_GEMM_SPLITK=0 turns this off (tuning and tests).
     const char* spk = getenv("OPSCALE_GEMM_SPLITK");
     const bool spk_off = (spk && strcmp(spk, "0") == 0) || getenv("OPSCALE_GEMM_TILE");
-    // up to 64 rows: 64-row tiles, so the matrix cores do not work on padding
-    // Tile rows by M (64, 128 or 256: the matrix cores work on little
-    // padding); with 256 rows, 256 or 128 columns, whichever gives more
+    // Tile rows by M: 64 up to 64 rows (the matrix cores work on little
+    // padding), 128 up to 256.  The 128-row tile keeps three K slices in its
+    // LDS ring, so each CU has two weight slices in flight where the 256-row
+    // tile has one: the weights stream from HBM, latency-bound, so 129-256
+    // rows run as two 128-row tiles (gate-up at M = 256, flushed: 142 -> 124
+    // us), without splitting K when those tiles fill the GPU.  Larger M
+    // takes 256 rows with 256 or 128 columns, whichever gives more
     // workgroups (ties: 256, which re-reads x half as often).
-    int rows = M <= 64 ? 64 : M <= 128 ? 128 : 256;
+    int rows = M <= 64 ? 64 : M <= 256 ? 128 : 256;
     int splits = 0;
     if (!spk_off) {
       if (rows == 64) splits = splitk_count<CfgSk64>(M, N, K);
-      else if (rows == 128) splits = splitk_count<CfgSk128>(M, N, K);
-      else {
+      else if (rows == 128) {
+        splits = splitk_count<CfgSk128>(M, N, K);
+        if (splits <= 1 && M > 128) return launch_gemm_bf16<CfgSk128>(x, W, bias, y, M, N, K, s, 1, nullptr);
+      } else {
         const int s_wide = splitk_count<CfgBig8>(M, N, K), s_mid = splitk_count<CfgMid>(M, N, K);
         const int64_t w_wide = (int64_t)s_wide * ((N + 255) / 256), w_mid = (int64_t)s_mid * ((N + 127) / 128);
         if (w_wide >= w_mid && s_wide > 1) splits = s_wide;

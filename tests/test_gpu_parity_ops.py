@@ -117,12 +117,14 @@ def test_linear_small_m(ops, monkeypatch, ng, M, N, K, bias):
     (256, 6144, 4096, False), (100, 520, 1032, True), (17, 4096, 14336, False), (200, 1000, 2048, True),
     (64, 8, 1024, False), (700, 4096, 4096, True), (64, 6144, 4096, True), (65, 1000, 2048, False),
     (96, 4096, 4096, False), (128, 28672, 1024, True), (256, 4096, 14336, False),
+    (200, 16648, 1024, True), (256, 28672, 4096, False),
 ])
 def test_linear_split_k(ops, monkeypatch, M, N, K, bias):
     """Decode-sized M with K split over workgroups (fp32 partials summed in
-    split order), on each tile the path picks (64, 128 or 256 rows; 256 or
-    128 columns): ragged M, N and K, a K range that does not divide evenly,
-    bias; bitwise equal across calls."""
+    split order), on each tile the path picks (64 or 128 rows up to 256, 256
+    rows with 256 or 128 columns above): ragged M, N and K, a K range that
+    does not divide evenly, bias; 129-256 rows whose 128-row tiles fill the
+    GPU without a split (the last two cases); bitwise equal across calls."""
     import torch
     monkeypatch.delenv("OPSCALE_GEMM_TILE", raising=False)
     monkeypatch.delenv("OPSCALE_GEMM_SPLITK", raising=False)
