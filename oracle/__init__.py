@@ -15,14 +15,16 @@ per-function citations, `cost` for the algorithmic flop/byte closed forms and
 `spatial` for CU shares and the interference factor of Eq. 5, `moe` for
 top-k routing and the fused mixture-of-experts MLP.
 
-Parity status: every function here is pinned by brute force, closed forms or
-invariants in the CPU tests (tests/test_oracle_pins.py); none is "parity
-unpinned".
+Parity status: every exported function has a named pin in the CPU tests
+(brute force, a hand-worked golden, a closed form or an invariant, plus planted
+mistakes each pin must catch): tests/test_oracle_pins.py for `ops` and `cost`,
+tests/test_oracle_moe.py for `moe`, tests/test_oracle_spatial.py for
+`spatial`.  The whole-layer dataflow is pinned by a two-token layer worked by
+hand (tests/golden/layer_two_tokens_hand.txt).
 """
 from .ops import (  # noqa: F401
     rmsnorm, linear, silu, swiglu, softmax, attn_prefill, attn_prefill_rows,
-    attn_decode, attn_decode_rows, gather_paged, decoder_layer_prefill,
-    rope, reshape_and_cache, add_rmsnorm, decoder_layer_forward, decoder_layer_decode,
+    attn_decode, gather_paged, rope, reshape_and_cache, add_rmsnorm, decoder_layer_forward, decoder_layer_decode,
 )
 from . import cost  # noqa: F401
 from . import spatial  # noqa: F401

@@ -188,13 +188,6 @@ def attn_decode(q, k_cache, v_cache, block_table, context_lens, scale: float) ->
     return out
 
 
-def attn_decode_rows(q, k_cache, v_cache, block_table, context_lens, seqs, scale: float):
-    """attn_decode for a subset of sequences; returns [len(seqs), Hq, D]."""
-    seqs = list(seqs)
-    return attn_decode(np.asarray(q)[seqs], k_cache, v_cache,
-                       np.asarray(block_table)[seqs], np.asarray(context_lens)[seqs], scale)
-
-
 # -------------------------------------------------------- rotary embedding ---
 def rope(x, positions, theta: float) -> np.ndarray:
     """Rotary position embedding of query or key heads (the RoPE attention
@@ -245,31 +238,6 @@ def add_rmsnorm(x, residual, w, eps: float):
 
 
 # ----------------------------------------------------- whole decoder layer ---
-def decoder_layer_prefill(x, p, cu_seqlens, n_q_heads, n_kv_heads, head_dim, eps):
-    """The layer dataflow the operators form (Section 2.2: a model is a data
-    flow graph of operators): norm -> QKV -> attention -> O, norm -> gate-up ->
-    SiLU-mul -> down.  Residual adds and rotary embeddings are not among the
-    profiled operators here and are omitted, so this is the operator chain only.
-
-    p: dict with w_norm1, w_qkv, w_o, w_norm2, w_gate_up, w_down.
-    Returns dict of every intermediate (fp64).
-    """
-    T = x.shape[0]
-    D = head_dim
-    h1 = rmsnorm(x, p["w_norm1"], eps)
-    qkv = linear(h1, p["w_qkv"])
-    q = qkv[:, : n_q_heads * D].reshape(T, n_q_heads, D)
-    k = qkv[:, n_q_heads * D:(n_q_heads + n_kv_heads) * D].reshape(T, n_kv_heads, D)
-    v = qkv[:, (n_q_heads + n_kv_heads) * D:].reshape(T, n_kv_heads, D)
-    a = attn_prefill(q, k, v, cu_seqlens, 1.0 / np.sqrt(D), causal=True)
-    o = linear(a.reshape(T, n_q_heads * D), p["w_o"])
-    h2 = rmsnorm(o, p["w_norm2"], eps)
-    gu = linear(h2, p["w_gate_up"])
-    act = swiglu(gu)
-    y = linear(act, p["w_down"])
-    return {"h1": h1, "qkv": qkv, "attn": a, "o": o, "h2": h2, "gate_up": gu, "act": act, "y": y}
-
-
 def decoder_layer_forward(x, residual, p, positions, cu_seqlens, n_q_heads, n_kv_heads, head_dim, eps,
                           theta, k_cache, v_cache, slot_mapping):
     """One decoder layer over a ragged prefill batch with every operator of its

@@ -44,11 +44,6 @@ def mask_bit(num_cus: int, num_xcds: int, interleaved: bool, xcd: int, slot: int
     return slot * num_xcds + xcd if interleaved else xcd * per + slot
 
 
-def xcd_of_bit(num_cus: int, num_xcds: int, interleaved: bool, bit: int) -> int:
-    """Inverse direction: which XCD a mask bit names."""
-    return bit % num_xcds if interleaved else bit // (num_cus // num_xcds)
-
-
 def cu_mask(num_cus: int, num_xcds: int, interleaved: bool, first: int, count: int):
     """The mask of a share as a list of uint32 words (bit n of word n // 32)."""
     words = [0] * ((num_cus + 31) // 32)

@@ -394,6 +394,39 @@ def check_layer(impl):
     np.testing.assert_allclose(a["y"], b_["y"], rtol=1e-13)
 
 
+def _kv(name):
+    """A golden of `key value value ...` lines, as a dict of float arrays."""
+    out = {}
+    with open(os.path.join(GOLDEN, name)) as f:
+        for line in f:
+            line = line.strip()
+            if line and not line.startswith("#"):
+                key, *vals = line.split()
+                out[key] = np.array([float(t) for t in vals])
+    return out
+
+
+def check_layer_golden(impl):
+    """The two-token layer worked by hand: every intermediate, the written
+    cache, the output and the carried residual (tests/golden/layer_two_tokens_hand.txt)."""
+    g = _kv("layer_two_tokens_hand.txt")
+    H, D, F = int(g["H"][0]), int(g["D"][0]), int(g["F"][0])
+    Hq, Hkv = (int(t) for t in g["heads"])
+    T = len(g["positions"])
+    nb, bs = int(g["num_blocks"][0]), int(g["block_size"][0])
+    p = {"w_norm1": g["w_norm1"], "w_norm2": g["w_norm2"],
+         "w_qkv": g["w_qkv"].reshape((Hq + 2 * Hkv) * D, H), "w_o": g["w_o"].reshape(H, Hq * D),
+         "w_gate_up": g["w_gate_up"].reshape(2 * F, H), "w_down": g["w_down"].reshape(H, F)}
+    fill = np.full((nb, bs, Hkv, D), g["cache_fill"][0])
+    out = impl.decoder_layer_forward(g["x"].reshape(T, H), g["residual"].reshape(T, H), p,
+                                     g["positions"].astype(int), g["cu_seqlens"].astype(int), Hq, Hkv, D,
+                                     float(g["eps"][0]), float(g["theta"][0]), fill, fill,
+                                     g["slots"].astype(int))
+    for key in ("h1", "q", "k", "v", "k_cache", "v_cache", "attn", "o", "r2", "h2", "act", "y"):
+        np.testing.assert_allclose(np.asarray(out[key]).ravel(), g[key], rtol=1e-12, atol=1e-13,
+                                   err_msg=key)
+
+
 def check_cost(c):
     # causal visible pairs counted by a loop
     lens = [1, 2, 5, 0, 9]
@@ -421,7 +454,7 @@ def check_cost(c):
 
 
 CHECKS = [check_linear, check_rmsnorm, check_swiglu, check_softmax, check_attn_prefill, check_attn_decode,
-          check_rope, check_cache_write, check_add_rmsnorm, check_layer]
+          check_rope, check_cache_write, check_add_rmsnorm, check_layer, check_layer_golden]
 
 
 @pytest.mark.parametrize("check", CHECKS, ids=lambda f: f.__name__)
@@ -504,6 +537,48 @@ def _mut_layer_decode_pos(x, res, p, ctx, bt, Hq, Hkv, D, eps, theta, kc, vc):
                                        Hq, Hkv, D, eps, theta, kc, vc)
 
 
+def _mut_layer(norm2_without_residual=False, gate_up_fed_h1=False, carry_r1=False, first_norm_of_x=False,
+               rope_q_only=False, cache_before_rope=False, attend_unrotated=False, rope_v=False):
+    """A copy of the prefill layer dataflow with one planted wiring mistake."""
+    def f(x, residual, p, positions, cu, Hq, Hkv, D, eps, theta, kc, vc, slots):
+        T = x.shape[0]
+        x = np.asarray(x, float)
+        r1 = x if residual is None else x + residual
+        h1 = oracle.rmsnorm(x if first_norm_of_x else r1, p["w_norm1"], eps)
+        qkv = oracle.linear(h1, p["w_qkv"])
+        q0 = qkv[:, : Hq * D].reshape(T, Hq, D)
+        k0 = qkv[:, Hq * D:(Hq + Hkv) * D].reshape(T, Hkv, D)
+        v = qkv[:, (Hq + Hkv) * D:].reshape(T, Hkv, D)
+        q = oracle.rope(q0, positions, theta)
+        k = k0 if rope_q_only else oracle.rope(k0, positions, theta)
+        if rope_v:
+            v = oracle.rope(v, positions, theta)
+        kc2, vc2 = oracle.reshape_and_cache(k0 if cache_before_rope else k, v, kc, vc, slots)
+        a = oracle.attn_prefill(q0 if attend_unrotated else q, k0 if attend_unrotated else k, v, cu,
+                                1.0 / np.sqrt(D), causal=True)
+        o = oracle.linear(a.reshape(T, Hq * D), p["w_o"])
+        r2 = r1 if carry_r1 else o + r1
+        h2 = oracle.rmsnorm(o if norm2_without_residual else o + r1, p["w_norm2"], eps)
+        gu = oracle.linear(h1 if gate_up_fed_h1 else h2, p["w_gate_up"])
+        act = oracle.swiglu(gu)
+        y = oracle.linear(act, p["w_down"])
+        return {"h1": h1, "r1": r1, "qkv": qkv, "q": q, "k": k, "v": v, "attn": a, "o": o, "h2": h2, "r2": r2,
+                "gate_up": gu, "act": act, "y": y, "k_cache": kc2, "v_cache": vc2}
+    return f
+
+
+def _mut_layer_decode_attends_first(x, res, p, ctx, bt, Hq, Hkv, D, eps, theta, kc, vc):
+    """decode step whose attention reads the cache before its own k and v are
+    written to it."""
+    out = oracle.decoder_layer_decode(x, res, p, ctx, bt, Hq, Hkv, D, eps, theta, kc, vc)
+    a = oracle.attn_decode(out["q"], kc, vc, bt, ctx, 1.0 / np.sqrt(D))
+    B = x.shape[0]
+    o = oracle.linear(a.reshape(B, Hq * D), p["w_o"])
+    h2, r2 = oracle.add_rmsnorm(o, out["r1"], p["w_norm2"], eps)
+    y = oracle.linear(oracle.swiglu(oracle.linear(h2, p["w_gate_up"])), p["w_down"])
+    return dict(out, attn=a, o=o, h2=h2, r2=r2, y=y)
+
+
 MUTANTS = {
     "linear_k_reversed": (check_linear, dict(linear=lambda x, W, b=None: np.asarray(x, float) @ np.asarray(W, float)[:, ::-1].T + (0 if b is None else b))),
     "linear_bias_dropped": (check_linear, dict(linear=lambda x, W, b=None: np.asarray(x, float) @ np.asarray(W, float).T)),
@@ -527,7 +602,22 @@ MUTANTS = {
     "cache_block_offset_swapped": (check_cache_write, dict(reshape_and_cache=_mut_cache(swap=True))),
     "add_rmsnorm_norms_x": (check_add_rmsnorm, dict(add_rmsnorm=lambda x, r, w, eps: (oracle.rmsnorm(x, w, eps), np.asarray(x) + r))),
     "layer_decode_position_is_len": (check_layer, dict(decoder_layer_decode=_mut_layer_decode_pos)),
+    "layer_decode_attends_before_cache_write": (check_layer, dict(decoder_layer_decode=_mut_layer_decode_attends_first)),
+    "layer_norm2_without_residual": (check_layer_golden, dict(decoder_layer_forward=_mut_layer(norm2_without_residual=True))),
+    "layer_gate_up_fed_h1": (check_layer_golden, dict(decoder_layer_forward=_mut_layer(gate_up_fed_h1=True))),
+    "layer_carries_r1": (check_layer_golden, dict(decoder_layer_forward=_mut_layer(carry_r1=True))),
+    "layer_first_norm_of_x": (check_layer_golden, dict(decoder_layer_forward=_mut_layer(first_norm_of_x=True))),
+    "layer_rope_q_only": (check_layer_golden, dict(decoder_layer_forward=_mut_layer(rope_q_only=True))),
+    "layer_cache_before_rope": (check_layer_golden, dict(decoder_layer_forward=_mut_layer(cache_before_rope=True))),
+    "layer_attends_unrotated": (check_layer_golden, dict(decoder_layer_forward=_mut_layer(attend_unrotated=True))),
+    "layer_rope_on_v": (check_layer_golden, dict(decoder_layer_forward=_mut_layer(rope_v=True))),
 }
+
+
+def test_layer_copy_without_a_mistake_passes():
+    """The mutant layer with no mistake planted matches the golden, so each
+    wiring mutant fails for its planted mistake alone."""
+    check_layer_golden(_mutant(decoder_layer_forward=_mut_layer()))
 
 
 @pytest.mark.parametrize("name", sorted(MUTANTS))
