@@ -100,15 +100,16 @@ def measured_traffic(op: str, kernel: str):
 
 
 class Layer:
-    """Preallocated operands of one step (inputs resident in HBM)."""
+    """Preallocated operands of one step (inputs resident in HBM): the prefill
+    layer of `pc` and, when `dc` is given, decode attention of `dc`."""
 
-    def __init__(self, ops, wl, torch):
+    def __init__(self, ops, wl, torch, pc=None, dc=None):
         self.ops, self.torch = ops, torch
-        self.pc = wl.C2
-        self.dc = wl.C3
-        pc, dc = self.pc, self.dc
+        self.pc = pc or wl.C2
+        self.dc = dc
+        pc = self.pc
         self.p = wl.prefill_layer_inputs(pc)
-        self.d = wl.decode_inputs(dc)
+        self.d = wl.decode_inputs(dc) if dc is not None else None
         M, H, F = self.p["M"], pc.hidden, pc.ffn
         Hq, Hkv, D = pc.n_q_heads, pc.n_kv_heads, pc.head_dim
         bf = torch.bfloat16
@@ -120,14 +121,20 @@ class Layer:
         self.v = self.qkv[:, (Hq + Hkv) * D:].view(M, Hkv, D)
         self.scale = 1.0 / math.sqrt(D)
         self.max_seqlen = int(self.p["lengths"].max())
-        dd = self.d
-        B = len(dd["context_lens_host"])
-        self.ws = torch.empty(ops.opscale_attn_decode_workspace_size(B, dc.n_q_heads, dc.head_dim,
-                                                                    dd["max_context_len"]),
-                              dtype=torch.uint8, device="cuda")
-        self.dout = torch.empty_like(dd["q"])
+        # one workspace for the linears' split partials, sized for the largest
+        self.lws = torch.empty(max(16, max(ops.opscale_linear_workspace_size(M, N, K)
+                                           for N, K in ((pc.qkv_out, H), (H, Hq * D), (2 * F, H), (H, F)))),
+                               dtype=torch.uint8, device="cuda")
         self.names = ["rmsnorm_1", "qkv_linear", "attn_prefill", "o_linear", "rmsnorm_2",
-                      "gate_up_linear", "swiglu", "down_linear", "attn_decode"]
+                      "gate_up_linear", "swiglu", "down_linear"]
+        dd = self.d
+        if dd is not None:
+            B = len(dd["context_lens_host"])
+            self.ws = torch.empty(ops.opscale_attn_decode_workspace_size(B, dc.n_q_heads, dc.head_dim,
+                                                                        dd["max_context_len"]),
+                                  dtype=torch.uint8, device="cuda")
+            self.dout = torch.empty_like(dd["q"])
+            self.names.append("attn_decode")
 
     def step(self, events=None):
         ops, p, d = self.ops, self.p, self.d
@@ -136,37 +143,42 @@ class Layer:
         def mark(i):
             if events is not None:
                 events[i].record()
+        ws = self.lws
         mark(0)
         ops.opscale_rmsnorm(p["x"], p["w_norm1"], y=self.h1, eps=eps); mark(1)
-        ops.opscale_linear(self.h1, p["w_qkv"], y=self.qkv); mark(2)
+        ops.opscale_linear(self.h1, p["w_qkv"], y=self.qkv, workspace=ws); mark(2)
         ops.opscale_attn_prefill(self.q, self.k, self.v, p["cu_seqlens"], self.max_seqlen, self.scale,
                                  True, out=self.attn); mark(3)
-        ops.opscale_linear(self.attn.view(self.p["M"], -1), p["w_o"], y=self.o); mark(4)
+        ops.opscale_linear(self.attn.view(self.p["M"], -1), p["w_o"], y=self.o, workspace=ws); mark(4)
         ops.opscale_rmsnorm(self.o, p["w_norm2"], y=self.h2, eps=eps); mark(5)
-        ops.opscale_linear(self.h2, p["w_gate_up"], y=self.gu); mark(6)
+        ops.opscale_linear(self.h2, p["w_gate_up"], y=self.gu, workspace=ws); mark(6)
         ops.opscale_swiglu(self.gu, out=self.act); mark(7)
-        ops.opscale_linear(self.act, p["w_down"], y=self.y); mark(8)
-        ops.opscale_attn_decode(d["q"], d["k_cache"], d["v_cache"], d["block_table"], d["context_lens"],
-                                d["max_context_len"], self.scale, workspace=self.ws, out=self.dout); mark(9)
+        ops.opscale_linear(self.act, p["w_down"], y=self.y, workspace=ws); mark(8)
+        if d is not None:
+            ops.opscale_attn_decode(d["q"], d["k_cache"], d["v_cache"], d["block_table"], d["context_lens"],
+                                    d["max_context_len"], self.scale, workspace=self.ws, out=self.dout); mark(9)
 
     def step_descs(self):
         """(name, descriptor) of each operator of the step, on the step's own buffers."""
         ops, p, d = self.ops, self.p, self.d
         eps = self.pc.eps
-        return [
+        ws = self.lws
+        out = [
             ("rmsnorm_1", ops.desc_rmsnorm(p["x"], p["w_norm1"], self.h1, eps)),
-            ("qkv_linear", ops.desc_linear(self.h1, p["w_qkv"], self.qkv)),
+            ("qkv_linear", ops.desc_linear(self.h1, p["w_qkv"], self.qkv, workspace=ws)),
             ("attn_prefill", ops.desc_attn_prefill(self.q, self.k, self.v, self.attn, p["cu_seqlens"],
                                                    self.max_seqlen, self.scale, True)),
-            ("o_linear", ops.desc_linear(self.attn.view(self.p["M"], -1), p["w_o"], self.o)),
+            ("o_linear", ops.desc_linear(self.attn.view(self.p["M"], -1), p["w_o"], self.o, workspace=ws)),
             ("rmsnorm_2", ops.desc_rmsnorm(self.o, p["w_norm2"], self.h2, eps)),
-            ("gate_up_linear", ops.desc_linear(self.h2, p["w_gate_up"], self.gu)),
+            ("gate_up_linear", ops.desc_linear(self.h2, p["w_gate_up"], self.gu, workspace=ws)),
             ("swiglu", ops.desc_swiglu(self.gu, self.act)),
-            ("down_linear", ops.desc_linear(self.act, p["w_down"], self.y)),
-            ("attn_decode", ops.desc_attn_decode(d["q"], d["k_cache"], d["v_cache"], d["block_table"],
-                                                 d["context_lens"], self.dout, d["max_context_len"], self.scale,
-                                                 self.ws)),
+            ("down_linear", ops.desc_linear(self.act, p["w_down"], self.y, workspace=ws)),
         ]
+        if d is not None:
+            out.append(("attn_decode", ops.desc_attn_decode(d["q"], d["k_cache"], d["v_cache"], d["block_table"],
+                                                            d["context_lens"], self.dout, d["max_context_len"],
+                                                            self.scale, self.ws)))
+        return out
 
     def setup_extras(self):
         """Operands of the operators around attention at the same shape: RoPE on
@@ -205,8 +217,10 @@ class Layer:
         out = []
         for name, xin, W in plan:
             y = e(B, W.shape[0])
-            self._dec_keep.append(y)
-            out.append((name, ops.desc_linear(xs[xin], W, y), B))
+            ws = self.torch.empty(max(16, ops.opscale_linear_workspace_size(B, W.shape[0], W.shape[1])),
+                                  dtype=self.torch.uint8, device="cuda")
+            self._dec_keep += [y, ws]
+            out.append((name, ops.desc_linear(xs[xin], W, y, workspace=ws), B))
         return out
 
     def extra(self, i):
@@ -233,9 +247,8 @@ class Layer:
         M, H, F = self.p["M"], pc.hidden, pc.ffn
         Hq, Hkv, D = pc.n_q_heads, pc.n_kv_heads, pc.head_dim
         lens = self.p["lengths"]
-        ctx = self.d["context_lens_host"]
         s = 2
-        return {
+        out = {
             "rmsnorm_1": (*from_cost["rmsnorm"](M, H, s), "hbm", M, "tokens/s"),
             "qkv_linear": (*from_cost["linear"](M, pc.qkv_out, H, s), "mfma", M, "tokens/s"),
             "attn_prefill": (*from_cost["attn_prefill"](lens, Hq, Hkv, D, s), "mfma", M, "tokens/s"),
@@ -244,9 +257,54 @@ class Layer:
             "gate_up_linear": (*from_cost["linear"](M, 2 * F, H, s), "mfma", M, "tokens/s"),
             "swiglu": (*from_cost["swiglu"](M, F, s), "hbm", M, "tokens/s"),
             "down_linear": (*from_cost["linear"](M, H, F, s), "mfma", M, "tokens/s"),
-            "attn_decode": (*from_cost["attn_decode"](ctx, dc.n_q_heads, dc.n_kv_heads, dc.head_dim, s,
-                                                      dc.block_size), "hbm", len(ctx), "seq/s"),
         }
+        if self.d is not None:
+            ctx = self.d["context_lens_host"]
+            out["attn_decode"] = (*from_cost["attn_decode"](ctx, dc.n_q_heads, dc.n_kv_heads, dc.head_dim, s,
+                                                            dc.block_size), "hbm", len(ctx), "seq/s")
+        return out
+
+
+def per_op_records(names, per_op_us, work):
+    """tokens/s (seq/s), TFLOP/s, GB/s and roofline fraction of each operator
+    from its average event-timed duration and its algorithmic work."""
+    per_op = {}
+    for nm in names:
+        fl, by, bound, units, unit = work[nm]
+        t_s = per_op_us[nm] * 1e-6
+        att = min(PEAK_BF16, fl / by * PEAK_HBM)
+        per_op[nm] = {"us": round(per_op_us[nm], 2), unit: round(units / t_s, 1),
+                      "tflops": round(fl / t_s * 1e-12, 2), "gbps": round(by / t_s * 1e-9, 1),
+                      "bound": bound, "roofline_frac": round((fl / t_s) / att, 4)}
+    return per_op
+
+
+def time_prefill_config(ops, wl, torch, cfg, steps: int, warmup: int):
+    """The prefill layer of another configuration, operator by operator: each
+    timed with device events on the stream it runs on, averaged over `steps`
+    passes of the whole layer (inputs resident in HBM, as in the step)."""
+    layer = Layer(ops, wl, torch, cfg, None)
+    for _ in range(warmup):
+        layer.step()
+    torch.cuda.synchronize()
+    n = len(layer.names)
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(n + 1)] for _ in range(steps)]
+    t0 = time.perf_counter()
+    for s_ in range(steps):
+        layer.step(evs[s_])
+    torch.cuda.synchronize()
+    ms = (time.perf_counter() - t0) * 1e3 / steps
+    us = {nm: sum(evs[s_][i].elapsed_time(evs[s_][i + 1]) for s_ in range(steps)) * 1e3 / steps
+          for i, nm in enumerate(layer.names)}
+    lens = layer.p["lengths"]
+    M = layer.p["M"]
+    rec = {"workload": f"{cfg.name} ({len(lens)} prompts, {M} tokens, lengths {int(lens.min())}-{int(lens.max())}, "
+                       f"hidden {cfg.hidden}, {cfg.n_q_heads}/{cfg.n_kv_heads} heads x {cfg.head_dim}, FFN {cfg.ffn})",
+           "tokens": M, "steps": steps, "ms_per_layer": round(ms, 4), "tokens/s": round(M / (ms * 1e-3), 1),
+           "per_op": per_op_records(layer.names, us, layer.work())}
+    del layer
+    torch.cuda.empty_cache()
+    return rec
 
 
 def _closed_forms():
@@ -275,41 +333,58 @@ def _closed_forms():
                 attn_decode=attn_decode)
 
 
+def _blas_info():
+    """BLAS library and thread count NumPy uses (threadpoolctl)."""
+    try:
+        from threadpoolctl import threadpool_info
+        info = [i for i in threadpool_info() if i.get("user_api") == "blas"]
+        if info:
+            return {"blas": f"{info[0].get('internal_api')} {info[0].get('version')}",
+                    "threads": int(max(i.get("num_threads", 1) for i in info))}
+    except Exception:  # noqa: BLE001 - informative only
+        pass
+    return {"blas": "unknown", "threads": len(os.sched_getaffinity(0))}
+
+
 def cpu_baseline(budget_s: float = 20.0):
-    """Time the fp64 CPU oracle on a bounded sample of the same prefill layer
-    and extrapolate to the full batch: the per-row operators on `rows` token
-    rows (linears on `cols` output columns, scaled by N / cols), attention on
-    whole prompts, shortest first, scaled by the causal key-query pair count.
-    Reported as a baseline only."""
+    """Time the CPU oracle as it stands (fp64 NumPy) on a bounded sample of the
+    step's workload and scale it to the whole step: the per-row operators
+    (both norms, the four full-width linears, SwiGLU) on `rows` token rows,
+    scaled by M / rows; prefill attention on whole prompts, shortest first,
+    scaled by the causal key-query pairs; decode attention on whole sequences
+    of the decode batch, scaled by the cached keys.  value = prefill tokens of
+    the step / the step's extrapolated time (the step includes decode
+    attention, as on the GPU).  Reported as a baseline only."""
     import numpy as np
 
     import oracle
     import workloads as wl
-    cfg = wl.C2
+    cfg, dcfg = wl.C2, wl.C3
     lens = wl.seq_lengths(cfg)
     M, H, F = int(lens.sum()), cfg.hidden, cfg.ffn
     Hq, Hkv, D = cfg.n_q_heads, cfg.n_kv_heads, cfg.head_dim
-    rows, cols = 256, 1024
+    rows = 256
     g = lambda tag, shape, std=1.0, mean=0.0: wl.normal(wl.rng_for(cfg, tag), shape, std, mean).astype(np.float64)
     x = g("x", (rows, H))
     wn = g("w_norm", (H,), 0.02, 1.0)
-    # (N, K) of each linear and a `cols`-row slice of its weight
     shapes = {"qkv": (cfg.qkv_out, H), "o": (H, Hq * D), "gate_up": (2 * F, H), "down": (H, F)}
-    Ws = {k: g("w_" + k, (cols, K), 0.02) for k, (N, K) in shapes.items()}
-    xs = {"qkv": x, "o": x[:, : Hq * D], "gate_up": x, "down": g("ffn_act", (rows, F))}
-    t0 = time.perf_counter()
-    oracle.rmsnorm(x, wn, cfg.eps)
-    t_rows = 2 * (time.perf_counter() - t0)
-    t_lin = 0.0
-    for k, (N, K) in shapes.items():
-        t0 = time.perf_counter()
-        oracle.linear(xs[k], Ws[k])
-        t_lin += (time.perf_counter() - t0) * N / cols
+    # Every output column of each linear is computed, 2048 columns per oracle
+    # call, with one drawn 2048-row weight block per K (drawing and holding
+    # the full fp64 weights costs more than the timed work; the values do not
+    # change it).
+    nblk = 2048
+    Wb = {K: g("w_qkv" if K == H else "w_down", (nblk, K), 0.02) for K in {K for _, K in shapes.values()}}
+    xs = {"qkv": x, "o": g("attn_out", (rows, Hq * D)), "gate_up": x, "down": g("ffn_act", (rows, F))}
     u = g("gate_up", (rows, 2 * F))
     t0 = time.perf_counter()
+    oracle.rmsnorm(x, wn, cfg.eps)
+    oracle.rmsnorm(x, wn, cfg.eps)
+    for k, (N, K) in shapes.items():
+        for _ in range(N // nblk):
+            oracle.linear(xs[k], Wb[K])
     oracle.swiglu(u)
-    t_rows += time.perf_counter() - t0
-    per_row = (t_rows + t_lin) / rows
+    per_row = (time.perf_counter() - t0) / rows
+    del Wb
     order = np.argsort(lens)
     done_pairs, att_s, used = 0, 0.0, []
     for b in order:
@@ -323,17 +398,33 @@ def cpu_baseline(budget_s: float = 20.0):
         if att_s > budget_s * 0.5:
             break
     all_pairs = int(sum(int(L) * (int(L) + 1) // 2 for L in lens))
-    total_s = per_row * M + att_s * all_pairs / done_pairs
-    try:
-        from threadpoolctl import threadpool_info
-        cores = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
-    except Exception:  # pragma: no cover
-        cores = len(os.sched_getaffinity(0))
-    return {"value": M / total_s, "unit": "tokens/s", "cores": int(cores), "kind": "oracle",
-            "sample": f"fp64 NumPy oracle: RMSNorm and SwiGLU on {rows} token rows, the 4 linears on {rows} rows x "
-                      f"{cols} output columns, attention on {len(used)} whole prompts (lengths {used}); "
-                      f"extrapolated to the {M}-token batch by rows, columns and causal key-query pairs; "
-                      f"decode attention not included"}
+    # decode attention: sequences of the decode batch in their drawn order,
+    # each in a cache of its own pages (block table 0, 1, 2, ...)
+    ctx = wl.seq_lengths(dcfg)
+    bs = dcfg.block_size
+    dec_s, dec_keys, dec_used = 0.0, 0, 0
+    for n in ctx:
+        n = int(n)
+        nb = (n + bs - 1) // bs
+        kc = g("k_cache", (nb, bs, dcfg.n_kv_heads, dcfg.head_dim))
+        vc = g("v_cache", (nb, bs, dcfg.n_kv_heads, dcfg.head_dim))
+        qd = g("q", (1, dcfg.n_q_heads, dcfg.head_dim))
+        t0 = time.perf_counter()
+        oracle.attn_decode(qd, kc, vc, np.arange(nb)[None, :], np.array([n]), 1 / math.sqrt(dcfg.head_dim))
+        dec_s += time.perf_counter() - t0
+        dec_keys += n
+        dec_used += 1
+        if dec_s > budget_s * 0.15:
+            break
+    total_s = per_row * M + att_s * all_pairs / done_pairs + dec_s * int(ctx.sum()) / dec_keys
+    info = _blas_info()
+    return {"value": M / total_s, "unit": "tokens/s", "cores": info["threads"], "kind": "oracle",
+            "blas": info["blas"],
+            "sample": f"fp64 NumPy oracle ({info['blas']}, {info['threads']} threads): both RMS Norms, the 4 "
+                      f"full-width linears (in 2048-column calls) and SwiGLU on {rows} token rows; prefill attention on {len(used)} whole "
+                      f"prompts (lengths {used}); decode attention on {dec_used} whole sequences of the decode "
+                      f"batch ({dec_keys} keys); scaled to the step ({M} prefill tokens, {int(ctx.sum())} cached "
+                      f"keys) by rows, causal key-query pairs and keys"}
 
 
 def main():
@@ -358,7 +449,7 @@ def main():
     ops.load()
     torch.cuda.set_device(0)
     log("building inputs ...")
-    layer = Layer(ops, wl, torch)
+    layer = Layer(ops, wl, torch, wl.C2, wl.C3)
     torch.cuda.synchronize()
     if a.calibrate_copy_mib:
         src = torch.empty(a.calibrate_copy_mib << 20, dtype=torch.uint8, device="cuda")
@@ -385,14 +476,7 @@ def main():
     per_op_us = {nm: sum(evs[s][i].elapsed_time(evs[s][i + 1]) for s in range(a.steps)) * 1e3 / a.steps
                  for i, nm in enumerate(layer.names)}
     work = layer.work()
-    per_op = {}
-    for nm in layer.names:
-        fl, by, bound, units, unit = work[nm]
-        t_s = per_op_us[nm] * 1e-6
-        att = min(PEAK_BF16, fl / by * PEAK_HBM)
-        per_op[nm] = {"us": round(per_op_us[nm], 2), unit: round(units / t_s, 1),
-                      "tflops": round(fl / t_s * 1e-12, 2), "gbps": round(by / t_s * 1e-9, 1),
-                      "bound": bound, "roofline_frac": round((fl / t_s) / att, 4)}
+    per_op = per_op_records(layer.names, per_op_us, work)
     dom = max(layer.names, key=lambda nm: per_op_us[nm])
     fl, by, bound, _, _ = work[dom]
     kernel = {"mfma": "gemm_bf16_kernel", "hbm": "rmsnorm_kernel"}[bound] if "linear" in dom or "norm" in dom else \
@@ -474,6 +558,12 @@ def main():
                               "bound": "mfma" if pr.bound == 0 else "hbm", "roofline_frac": round(pr.roofline_frac, 4)}
         del w1, w2, xm, ids, wts, om, wsm
     del flush
+    # The 70B-shaped layer (16384 tokens) and the bursty long-context mix
+    # (4 x 32768 + 64 short prompts), operator by operator.
+    configs = {}
+    for cfg, n in ((wl.C4, max(3, a.steps // 2)), (wl.C5, 3)):
+        log(f"config {cfg.name} ...")
+        configs[cfg.name] = time_prefill_config(ops, wl, torch, cfg, n, 1)
     # Peaks re-measured on this GPU (sustained clock, real data): the spec
     # peaks above stay the primary denominators.
     log("peak probes ...")
@@ -504,6 +594,7 @@ def main():
         "roofline": roof,
         "per_op": per_op,
         "extra_ops": extra_ops,
+        "configs": configs,
         "isolated": isolated,
         "measured_peaks": meas,
         "gpu_state": {"before": state_before, "after": state_after},

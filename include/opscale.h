@@ -17,7 +17,9 @@
  * Conventions shared by every entry point
  *  - Pointers: all tensor pointers are DEVICE pointers to caller-owned memory,
  *    16-byte aligned.  The library never allocates or frees device memory in an
- *    operator call; the decode split-KV scratch is a caller workspace.
+ *    operator call: every scratch buffer (the linear's split-K partials, the
+ *    decode split-KV partials, the mixture-of-experts intermediates) is a
+ *    caller workspace whose size a *_workspace_size query returns.
  *  - Layout: row-major, innermost dimension contiguous.  Element type is given
  *    by `dt` and shared by every tensor of the call (indices are int32).
  *  - Sizes: int64 element counts.  A zero-sized problem (M == 0, B == 0 or
@@ -32,7 +34,9 @@
  *    message of the last failure is available from opscale_last_error().
  *    Nothing aborts, exits or throws across this interface.
  *  - Concurrency: entry points are re-entrant; the only library state is a
- *    pair of timing events per host thread, created on first use.
+ *    pair of timing events per host thread, created on first use, and the
+ *    process-wide tuning overrides of opscale_set_tuning (all automatic
+ *    unless a caller sets one).
  */
 #ifndef OPSCALE_H
 #define OPSCALE_H
@@ -68,6 +72,30 @@ typedef struct {
   double alg_bytes;
 } opscale_timing;
 
+/*
+ * Tuning and test overrides.  Not needed in normal use: every knob starts at
+ * -1, "automatic", and each entry point then picks its kernel path from the
+ * problem shape.  Tests and tuning sweeps force one path with another value.
+ * A setting is process-wide and applies to calls made after it; calls in
+ * flight keep the path they were planned with.  A workspace size queried
+ * under one setting is valid for calls made under the same setting.
+ * Returns OPSCALE_ERR_INVALID_ARG for an unknown knob or a value out of range.
+ */
+typedef enum {
+  OPSCALE_TUNE_GEMM_TILE = 0,        /* bf16 linear block tile: 0 = 256x256, 1 = 192x256, 2 = 256x128
+                                        (forcing one also turns off the small-M and split-K paths) */
+  OPSCALE_TUNE_GEMM_SKINNY = 1,      /* 0: never the small-M kernel; 1: wherever it is supported */
+  OPSCALE_TUNE_GEMM_SPLITK = 2,      /* 0: no K split for decode-sized M */
+  OPSCALE_TUNE_GEMM_TAIL = 3,        /* 0: no K split of the last partly filled round */
+  OPSCALE_TUNE_SKINNY_NG = 4,        /* 1 or 2: 16 or 32 output columns per small-M workgroup */
+  OPSCALE_TUNE_PREFILL_SCHEDULE = 5, /* 0: one workgroup per grid cell; 1: the work list */
+  OPSCALE_TUNE_MOE_FUSE = 6,         /* 0: gate-up output, then the SwiGLU kernel */
+  OPSCALE_TUNE_COUNT = 7
+} opscale_tune;
+opscale_status opscale_set_tuning(opscale_tune knob, int32_t value);
+/* The current value of a knob (-1: automatic, also for an unknown knob). */
+int32_t opscale_get_tuning(opscale_tune knob);
+
 /* Library version string, e.g. "opscale 0.1.0 gfx950". */
 const char* opscale_version(void);
 const char* opscale_status_string(opscale_status s);
@@ -85,16 +113,31 @@ opscale_status opscale_rmsnorm(const void* x, const void* w, void* y, int64_t M,
                                opscale_timing* timing);
 
 /*
+ * Bytes of device workspace opscale_linear can use for these sizes: the fp32
+ * partial results of a K split (small M, or the last partly filled round of
+ * tiles of a large problem).  0 when the planned path splits nothing.
+ */
+size_t opscale_linear_workspace_size(int64_t M, int64_t N, int64_t K, opscale_dtype dt);
+
+/*
  * Linear projection (Section 2.1: QKV Linear, wide projections, MLP linears).
  *   y[m, n] = sum_k x[m, k] * W[n, k] (+ bias[n])
  * x: [M, K]; W: [N, K] (the nn.Linear weight layout); bias: [N] or NULL;
  * y: [M, N], must not alias x or W.  bf16: MFMA with fp32 accumulation.
  * K * sizeof(dt) and N * sizeof(dt) must be multiples of 16.
- * The bf16 block tile (256x256, 192x256 or 256x128) is chosen per shape; the
- * environment variable OPSCALE_GEMM_TILE set to one of those names forces it.
+ * The bf16 path (small-M kernel, or a 256x256, 192x256 or 256x128 block tile,
+ * with K split over workgroups where that fills the GPU) is chosen per shape.
+ * workspace: NULL, or DEVICE scratch of workspace_bytes, 16-byte aligned, not
+ *   overlapping x, W or y.  NULL takes a path that needs none (no K split;
+ *   slower for decode-sized M and for a last round of tiles that is mostly
+ *   idle).  Non-NULL must hold opscale_linear_workspace_size(M, N, K, dt)
+ *   bytes, else OPSCALE_ERR_WORKSPACE with nothing enqueued.  Its contents on
+ *   entry are ignored; calls sharing a workspace must be stream-ordered.
+ *   Split partials are summed in a fixed order, so results are deterministic.
  */
 opscale_status opscale_linear(const void* x, const void* W, const void* bias, void* y,
                               int64_t M, int64_t N, int64_t K, opscale_dtype dt,
+                              void* workspace, size_t workspace_bytes,
                               hipStream_t stream, opscale_timing* timing);
 
 /*
@@ -245,7 +288,10 @@ typedef struct {
   opscale_dtype dt;
   union {
     struct { const void* x; const void* w; void* y; int64_t M, H; float eps; } rmsnorm;
-    struct { const void* x; const void* W; const void* bias; void* y; int64_t M, N, K; } linear;
+    struct {
+      const void* x; const void* W; const void* bias; void* y; int64_t M, N, K;
+      void* workspace; size_t workspace_bytes;
+    } linear;
     struct { const void* gate_up; void* out; int64_t M, F; } swiglu;
     struct {
       const void *q, *k, *v; int64_t q_row_stride, kv_row_stride; void* o;

@@ -8,7 +8,8 @@ entry points (layer), the operator profiler (profiler) and spatial sharing
 over CU-masked streams (spatial)."""
 from ._lib import (  # noqa: F401
     OpscaleError, Timing, Profile, OpDesc, load, LIB_PATH, EXPORTS,
-    opscale_version, opscale_rmsnorm, opscale_linear, opscale_swiglu, opscale_attn_prefill,
+    opscale_version, opscale_rmsnorm, opscale_linear, opscale_linear_workspace_size, opscale_swiglu,
+    opscale_attn_prefill, opscale_set_tuning, opscale_get_tuning,
     opscale_rope, opscale_reshape_and_cache, opscale_add_rmsnorm,
     opscale_attn_decode_workspace_size, opscale_attn_decode, opscale_op_profile,
     desc_rmsnorm, desc_linear, desc_swiglu, desc_attn_prefill, desc_attn_decode,
@@ -18,4 +19,6 @@ from ._lib import (  # noqa: F401
     opscale_cu_stream_mask, opscale_cu_probe, opscale_probe_mfma, opscale_probe_hbm, opscale_corun_profile,
     OPSCALE_OK, OPSCALE_ERR_INVALID_ARG, OPSCALE_ERR_UNSUPPORTED, OPSCALE_ERR_WORKSPACE,
     OPSCALE_ERR_HIP, OPSCALE_F32, OPSCALE_BF16,
+    TUNE_AUTO, TUNE_GEMM_TILE, TUNE_GEMM_SKINNY, TUNE_GEMM_SPLITK, TUNE_GEMM_TAIL, TUNE_SKINNY_NG,
+    TUNE_PREFILL_SCHEDULE, TUNE_MOE_FUSE,
 )

@@ -18,6 +18,9 @@ OPSCALE_OK, OPSCALE_ERR_INVALID_ARG, OPSCALE_ERR_UNSUPPORTED, OPSCALE_ERR_WORKSP
 OPSCALE_F32, OPSCALE_BF16 = 0, 1
 (OP_RMSNORM, OP_LINEAR, OP_SWIGLU, OP_ATTN_PREFILL, OP_ATTN_DECODE, OP_ROPE, OP_RESHAPE_AND_CACHE,
  OP_ADD_RMSNORM, OP_FUSED_MOE) = range(9)
+(TUNE_GEMM_TILE, TUNE_GEMM_SKINNY, TUNE_GEMM_SPLITK, TUNE_GEMM_TAIL, TUNE_SKINNY_NG, TUNE_PREFILL_SCHEDULE,
+ TUNE_MOE_FUSE) = range(7)
+TUNE_AUTO = -1
 
 c_i32, c_i64, c_f32, c_f64, c_vp, c_sz = (ctypes.c_int32, ctypes.c_int64, ctypes.c_float,
                                           ctypes.c_double, ctypes.c_void_p, ctypes.c_size_t)
@@ -38,7 +41,8 @@ class _RmsnormArgs(ctypes.Structure):
 
 
 class _LinearArgs(ctypes.Structure):
-    _fields_ = [("x", c_vp), ("W", c_vp), ("bias", c_vp), ("y", c_vp), ("M", c_i64), ("N", c_i64), ("K", c_i64)]
+    _fields_ = [("x", c_vp), ("W", c_vp), ("bias", c_vp), ("y", c_vp), ("M", c_i64), ("N", c_i64), ("K", c_i64),
+                ("workspace", c_vp), ("workspace_bytes", c_sz)]
 
 
 class _SwigluArgs(ctypes.Structure):
@@ -125,7 +129,11 @@ EXPORTS = {
     "opscale_status_string": (ctypes.c_char_p, [c_i32]),
     "opscale_last_error": (ctypes.c_char_p, []),
     "opscale_rmsnorm": (c_i32, [c_vp, c_vp, c_vp, c_i64, c_i64, c_f32, c_i32, c_vp, ctypes.POINTER(Timing)]),
-    "opscale_linear": (c_i32, [c_vp, c_vp, c_vp, c_vp, c_i64, c_i64, c_i64, c_i32, c_vp, ctypes.POINTER(Timing)]),
+    "opscale_set_tuning": (c_i32, [c_i32, c_i32]),
+    "opscale_get_tuning": (c_i32, [c_i32]),
+    "opscale_linear_workspace_size": (c_sz, [c_i64, c_i64, c_i64, c_i32]),
+    "opscale_linear": (c_i32, [c_vp, c_vp, c_vp, c_vp, c_i64, c_i64, c_i64, c_i32, c_vp, c_sz, c_vp,
+                               ctypes.POINTER(Timing)]),
     "opscale_swiglu": (c_i32, [c_vp, c_vp, c_i64, c_i64, c_i32, c_vp, ctypes.POINTER(Timing)]),
     "opscale_attn_prefill": (c_i32, [c_vp, c_vp, c_vp, c_i64, c_i64, c_vp, c_vp, c_i32, c_i64, c_i32,
                                      c_i32, c_i32, c_i32, c_f32, c_i32, c_i32, c_vp, ctypes.POINTER(Timing)]),
@@ -245,23 +253,57 @@ def opscale_rmsnorm(x, w, y=None, eps: float = 1e-5, stream=None, timed: bool = 
     return (y, t) if timed else y
 
 
-def opscale_linear(x, W, bias=None, y=None, stream=None, timed: bool = False):
-    """y[M, N] = x[M, K] W[N, K]^T (+ bias)."""
+def opscale_set_tuning(knob: int, value: int):
+    """Force (value >= 0) or release (-1) one of the library's path choices."""
+    _check(load().opscale_set_tuning(knob, value))
+
+
+def opscale_get_tuning(knob: int) -> int:
+    return int(load().opscale_get_tuning(knob))
+
+
+def opscale_linear_workspace_size(M: int, N: int, K: int, dtype=None) -> int:
+    import torch
+    dt = OPSCALE_F32 if dtype == torch.float32 else OPSCALE_BF16
+    return int(load().opscale_linear_workspace_size(M, N, K, dt))
+
+
+def _linear_shapes(x, W):
+    K = x.shape[-1]
+    if W.shape[1] != K:
+        raise OpscaleError(OPSCALE_ERR_INVALID_ARG, f"W is {tuple(W.shape)}, expected [N, {K}]")
+    return x.numel() // K, W.shape[0], K
+
+
+def _linear_workspace(x, W, workspace):
+    """The workspace tensor to pass: given, allocated by torch (None), or none
+    at all (False: the library then takes a path that needs none)."""
+    import torch
+    if workspace is False:
+        return None
+    if workspace is None:
+        M, N, K = _linear_shapes(x, W)
+        need = opscale_linear_workspace_size(M, N, K, x.dtype) if M else 0
+        return torch.empty(need, dtype=torch.uint8, device=x.device) if need else None
+    return workspace
+
+
+def opscale_linear(x, W, bias=None, y=None, workspace=None, stream=None, timed: bool = False):
+    """y[M, N] = x[M, K] W[N, K]^T (+ bias).  `workspace` (a uint8 GPU tensor)
+    is allocated by torch when None; False passes none."""
     import torch
     lib = load()
-    _dev(x, W, bias, y)
+    _dev(x, W, bias, y, workspace if workspace is not False else None)
     for n, t_ in (("x", x), ("W", W), ("bias", bias), ("y", y)):
         if t_ is not None:
             _contig(n, t_)
-    K = x.shape[-1]
-    M = x.numel() // K
-    N = W.shape[0]
-    if W.shape[1] != K:
-        raise OpscaleError(OPSCALE_ERR_INVALID_ARG, f"W is {tuple(W.shape)}, expected [N, {K}]")
+    M, N, K = _linear_shapes(x, W)
     if y is None:
         y = torch.empty(*x.shape[:-1], N, dtype=x.dtype, device=x.device)
+    ws = _linear_workspace(x, W, workspace)
     t = Timing() if timed else None
-    _check(lib.opscale_linear(_ptr(x), _ptr(W), _ptr(bias), _ptr(y), M, N, K, _dt(x), _stream(stream),
+    _check(lib.opscale_linear(_ptr(x), _ptr(W), _ptr(bias), _ptr(y), M, N, K, _dt(x), _ptr(ws),
+                              0 if ws is None else ws.numel() * ws.element_size(), _stream(stream),
                               ctypes.byref(t) if t else None))
     return (y, t) if timed else y
 
@@ -572,10 +614,15 @@ def desc_rmsnorm(x, w, y, eps=1e-5) -> OpDesc:
     return d
 
 
-def desc_linear(x, W, y, bias=None) -> OpDesc:
+def desc_linear(x, W, y, bias=None, workspace=None) -> OpDesc:
+    """`workspace` must stay alive while the descriptor is used (see
+    opscale_linear for None / False)."""
     d = OpDesc(op=OP_LINEAR, dt=_dt(x))
-    K = x.shape[-1]
-    d.u.linear = _LinearArgs(_ptr(x), _ptr(W), _ptr(bias), _ptr(y), x.numel() // K, W.shape[0], K)
+    M, N, K = _linear_shapes(x, W)
+    ws = _linear_workspace(x, W, workspace)
+    d.u.linear = _LinearArgs(_ptr(x), _ptr(W), _ptr(bias), _ptr(y), M, N, K, _ptr(ws),
+                             0 if ws is None else ws.numel() * ws.element_size())
+    d._keep = ws
     return d
 
 

@@ -1,6 +1,7 @@
 // C ABI of libopscale: argument validation, dispatch to the gfx950 kernels,
 // kernel-only timing with device events and the per-operator profile.
 #include <algorithm>
+#include <atomic>
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
@@ -28,6 +29,28 @@ opscale_status fail(opscale_status st, const char* fmt, ...) {
 
 opscale_status hip_fail(hipError_t e, const char* what) {
   return fail(OPSCALE_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+// The tuning overrides (opscale_set_tuning); -1 everywhere means automatic.
+namespace {
+std::atomic<int32_t> g_tuning[OPSCALE_TUNE_COUNT] = {-1, -1, -1, -1, -1, -1, -1};
+}  // namespace
+
+int32_t tuning(opscale_tune knob) {
+  return (unsigned)knob < (unsigned)OPSCALE_TUNE_COUNT ? g_tuning[knob].load(std::memory_order_relaxed) : -1;
+}
+
+opscale_status set_tuning(opscale_tune knob, int32_t value) {
+  if ((unsigned)knob >= (unsigned)OPSCALE_TUNE_COUNT)
+    return fail(OPSCALE_ERR_INVALID_ARG, "set_tuning: unknown knob %d", (int)knob);
+  int32_t hi = 1;
+  if (knob == OPSCALE_TUNE_GEMM_TILE) hi = 2;
+  if (knob == OPSCALE_TUNE_SKINNY_NG) hi = 2;
+  const int32_t lo = knob == OPSCALE_TUNE_SKINNY_NG ? 1 : 0;
+  if (value != -1 && (value < lo || value > hi))
+    return fail(OPSCALE_ERR_INVALID_ARG, "set_tuning: value %d out of range for knob %d", (int)value, (int)knob);
+  g_tuning[knob].store(value, std::memory_order_relaxed);
+  return OPSCALE_OK;
 }
 
 }  // namespace opscale
@@ -197,7 +220,8 @@ opscale_status check_rmsnorm(const void* x, const void* w, void* y, int64_t M, i
 }
 
 opscale_status check_linear(const void* x, const void* W, const void* bias, void* y, int64_t M,
-                            int64_t N, int64_t K, opscale_dtype dt) {
+                            int64_t N, int64_t K, opscale_dtype dt, const void* ws, size_t ws_bytes,
+                            opscale::LinearPlan* plan) {
   if (!dtype_ok(dt)) return fail(OPSCALE_ERR_INVALID_ARG, "linear: unknown dtype %d", (int)dt);
   if (M < 0 || N <= 0 || K <= 0 || M >= kMaxDim || N >= kMaxDim || K > (1 << 20))
     return fail(OPSCALE_ERR_INVALID_ARG, "linear: bad sizes M=%lld N=%lld K=%lld", (long long)M,
@@ -212,6 +236,17 @@ opscale_status check_linear(const void* x, const void* W, const void* bias, void
     return fail(OPSCALE_ERR_INVALID_ARG, "linear: pointers must be 16-byte aligned");
   if (overlap(y, M * N * s, x, M * K * s) || overlap(y, M * N * s, W, N * K * s))
     return fail(OPSCALE_ERR_INVALID_ARG, "linear: y must not overlap x or W");
+  // no workspace: a path that needs none; a workspace: the path it allows,
+  // which must then fit
+  *plan = opscale::plan_linear(M, N, K, dt == OPSCALE_BF16, ws != nullptr);
+  if (plan->ws_bytes > 0) {
+    if (ws_bytes < plan->ws_bytes)
+      return fail(OPSCALE_ERR_WORKSPACE, "linear: workspace of %zu bytes, %zu needed", ws_bytes, plan->ws_bytes);
+    if (!aligned16(ws)) return fail(OPSCALE_ERR_INVALID_ARG, "linear: workspace must be 16-byte aligned");
+    if (overlap(ws, (int64_t)plan->ws_bytes, y, M * N * s) || overlap(ws, (int64_t)plan->ws_bytes, x, M * K * s) ||
+        overlap(ws, (int64_t)plan->ws_bytes, W, N * K * s))
+      return fail(OPSCALE_ERR_INVALID_ARG, "linear: workspace overlaps x, W or y");
+  }
   return OPSCALE_OK;
 }
 
@@ -469,15 +504,25 @@ opscale_status opscale_rmsnorm(const void* x, const void* w, void* y, int64_t M,
   return st;
 }
 
+opscale_status opscale_set_tuning(opscale_tune knob, int32_t value) { return opscale::set_tuning(knob, value); }
+
+int32_t opscale_get_tuning(opscale_tune knob) { return opscale::tuning(knob); }
+
+size_t opscale_linear_workspace_size(int64_t M, int64_t N, int64_t K, opscale_dtype dt) {
+  if (M <= 0 || N <= 0 || K <= 0 || !dtype_ok(dt)) return 0;
+  return opscale::plan_linear(M, N, K, dt == OPSCALE_BF16, true).ws_bytes;
+}
+
 opscale_status opscale_linear(const void* x, const void* W, const void* bias, void* y, int64_t M,
-                              int64_t N, int64_t K, opscale_dtype dt, hipStream_t stream,
-                              opscale_timing* timing) {
-  opscale_status st = check_linear(x, W, bias, y, M, N, K, dt);
+                              int64_t N, int64_t K, opscale_dtype dt, void* workspace, size_t workspace_bytes,
+                              hipStream_t stream, opscale_timing* timing) {
+  opscale::LinearPlan plan{};
+  opscale_status st = check_linear(x, W, bias, y, M, N, K, dt, workspace, workspace_bytes, &plan);
   if (st != OPSCALE_OK) return st;
   zero_timing(timing);
   if (M == 0) return OPSCALE_OK;
   st = run_timed(stream, timing, "linear launch", [&] {
-    return opscale::launch_linear(x, W, bias, y, M, N, K, dt == OPSCALE_BF16, stream);
+    return opscale::launch_linear(plan, x, W, bias, y, M, N, K, workspace, stream);
   });
   if (st == OPSCALE_OK && timing) {
     const Work wk = work_linear(M, N, K, esize(dt), bias != nullptr);
@@ -689,10 +734,11 @@ opscale_status prepare_op(const opscale_op_desc* d, hipStream_t stream, const ch
     }
     case OPSCALE_OP_LINEAR: {
       const auto& a = d->u.linear;
-      st = check_linear(a.x, a.W, a.bias, a.y, a.M, a.N, a.K, dt);
+      opscale::LinearPlan plan{};
+      st = check_linear(a.x, a.W, a.bias, a.y, a.M, a.N, a.K, dt, a.workspace, a.workspace_bytes, &plan);
       if (st != OPSCALE_OK) return st;
       if (a.M == 0) return fail(OPSCALE_ERR_INVALID_ARG, "%s: empty problem", who);
-      launch = [=] { return opscale::launch_linear(a.x, a.W, a.bias, a.y, a.M, a.N, a.K, bf16, stream); };
+      launch = [=] { return opscale::launch_linear(plan, a.x, a.W, a.bias, a.y, a.M, a.N, a.K, a.workspace, stream); };
       wk = work_linear(a.M, a.N, a.K, esize(dt), a.bias != nullptr);
       break;
     }

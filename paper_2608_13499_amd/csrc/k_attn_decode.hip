@@ -51,18 +51,12 @@ constexpr float kLog2e = 1.4426950408889634f;
 constexpr int kTile = 32;    // keys per wave step
 constexpr int kWaves = 8;    // waves per workgroup
 constexpr int kChunk = 512;  // keys per page window
-#ifndef OPSCALE_DECODE_MAX_WG
-#define OPSCALE_DECODE_MAX_WG 256
-#endif
-#ifndef OPSCALE_DECODE_SEQ_WG
-#define OPSCALE_DECODE_SEQ_WG 64
-#endif
 // Workgroups of a launch, at most (one per CU: the grid runs in one round,
 // and 8 waves per CU keep fewer loads in flight, which streams HBM faster
 // than 16 did); and per sequence of the batch, at most (so a sequence's merge
 // takes about one 64-wide pass).
-constexpr int kMaxWorkgroups = OPSCALE_DECODE_MAX_WG;
-constexpr int kSeqWorkgroups = OPSCALE_DECODE_SEQ_WG;
+constexpr int kMaxWorkgroups = 256;
+constexpr int kSeqWorkgroups = 64;
 constexpr int kInlineB = kWaves * 64;  // up to this batch every workgroup builds the plan itself
 // Page ids of one window of kChunk keys (any block size >= 1) fit in here.
 constexpr int kMaxPages = kChunk + 1;

@@ -430,12 +430,11 @@ hipError_t launch_attn_prefill(const void* q, const void* k, const void* v, int6
   // than three quarters of B x max_seqlen favour the work list.
   const int64_t max_items = (total_tokens / BQ + B) * (int64_t)Hkv * (G / hpb);
   bool list = B <= kMaxListB && (double)total_tokens < 0.75 * (double)B * (double)max_seqlen;
-  // OPSCALE_PREFILL_SCHEDULE=grid|list overrides the choice (tuning, tests);
+  // OPSCALE_TUNE_PREFILL_SCHEDULE overrides the choice (0 grid, 1 list);
   // batches of more than kMaxListB prompts always use the grid.
-  if (const char* force = std::getenv("OPSCALE_PREFILL_SCHEDULE")) {
-    if (std::strcmp(force, "grid") == 0) list = false;
-    else if (std::strcmp(force, "list") == 0) list = B <= kMaxListB;
-  }
+  const int32_t force = tuning(OPSCALE_TUNE_PREFILL_SCHEDULE);
+  if (force == 0) list = false;
+  else if (force == 1) list = B <= kMaxListB;
   const unsigned gx = list ? (unsigned)std::min<int64_t>(0x7fffffff, max_items) : (unsigned)(B * Hkv * (G / hpb));
   const unsigned gy = list ? 1u : (unsigned)std::min<int64_t>(65535, (max_seqlen + BQ - 1) / BQ);
 #define OPS_PF(DD, P)                                                                                   \

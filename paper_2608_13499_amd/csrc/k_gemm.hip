@@ -30,9 +30,7 @@ namespace opscale {
 namespace {
 
 constexpr int kNumCUs = 256;  // MI355X compute units
-#ifndef OPSCALE_GEMM_GROUP_MB
-#define OPSCALE_GEMM_GROUP_MB 16  // x rows per tile group, in MB (see launch_gemm_bf16)
-#endif
+constexpr int64_t kGroupBytes = (int64_t)16 << 20;  // x rows per tile group (see tile_group_rows)
 constexpr int64_t kSplitKMaxM = 2048;  // split-K is for small M (decode batches)
 
 // Tile configuration: BM x BN block tile, K in slices of BK, WGM x WGN waves
@@ -581,13 +579,33 @@ __global__ __launch_bounds__(256) void splitk_tile_reduce_kernel(const float* __
   }
 }
 
-// tail_splits > 1: the tiles of the last, partly filled round run as that many
-// K ranges each (compact fp32 partials in stream-ordered scratch, then an
-// ordered reduce); the other tiles as usual, in the same launch.
+// Tile-rows per group of the tile order (tile_coords): as many as keep the
+// group's x rows (BM x K bf16 each) within kGroupBytes, so they stay in the
+// last-level cache while the group sweeps the tile-columns; at least one, at
+// most all.
+template <class C>
+static int tile_group_rows(int64_t tiles_m, int64_t tiles_n, int64_t K) {
+  (void)tiles_n;
+  const int64_t row_block_bytes = (int64_t)C::BM * K * 2;
+  return (int)std::max<int64_t>(1, std::min<int64_t>(tiles_m, kGroupBytes / row_block_bytes));
+}
+
+// K range of one split: a whole number of BK slices; the number of ranges
+// that actually results (at most `splits`).
+static int64_t split_chunk(int64_t K, int splits, int BK) { return ((K + splits - 1) / splits + BK - 1) / BK * BK; }
+static int split_ranges(int64_t K, int splits, int BK) {
+  const int64_t c = split_chunk(K, splits, BK);
+  return (int)((K + c - 1) / c);
+}
+
+// splits > 1: every tile runs as that many K ranges (fp32 partials [splits, M,
+// N] in `part`, then an ordered reduce).  tail_splits > 1: only the tiles of
+// the last, partly filled round run split (compact fp32 partial tiles in
+// `part`), the other tiles as usual in the same launch.  `part` is the
+// caller's workspace, sized by plan_linear.
 template <class C>
 static hipError_t launch_gemm_bf16(const void* x, const void* W, const void* bias, void* y, int64_t M,
-                                   int64_t N, int64_t K, hipStream_t s, int splits = 1, float* part = nullptr,
-                                   int tail_splits = 0) {
+                                   int64_t N, int64_t K, hipStream_t s, int splits, int tail_splits, float* part) {
   // More than 64 KB of dynamic LDS per workgroup needs the limit raised once
   // per process (a host-side function attribute, no allocation).
   static const hipError_t attr = hipFuncSetAttribute(
@@ -595,47 +613,36 @@ static hipError_t launch_gemm_bf16(const void* x, const void* W, const void* bia
       C::kLdsBytes);
   if (attr != hipSuccess) return attr;
   const int64_t tiles_m = (M + C::BM - 1) / C::BM;
-  const int64_t tiles = tiles_m * ((N + C::BN - 1) / C::BN);
-  // Tile-rows per group: as many as keep the group's x rows (BM x K bf16 each)
-  // within 16 MB, so they stay in the last-level cache while the group sweeps
-  // the tile-columns; at least one, at most all.
-  constexpr int64_t kGroupBytes = (int64_t)OPSCALE_GEMM_GROUP_MB << 20;
-  const int64_t row_block_bytes = (int64_t)C::BM * K * 2;
-  const int group_m = (int)std::max<int64_t>(1, std::min<int64_t>(tiles_m, kGroupBytes / row_block_bytes));
+  const int64_t tiles_n = (N + C::BN - 1) / C::BN;
+  const int64_t tiles = tiles_m * tiles_n;
+  const int group_m = tile_group_rows<C>(tiles_m, tiles_n, K);
   if (tail_splits > 1) {
     const int64_t tail = tiles % kNumCUs, dp = tiles - tail;
-    const int64_t kchunk = ((K + tail_splits - 1) / tail_splits + C::BK - 1) / C::BK * C::BK;
-    const int64_t nsplit = (K + kchunk - 1) / kchunk;
-    void* ws = nullptr;
-    hipError_t e = scratch_alloc((size_t)nsplit * tail * C::BM * C::BN * sizeof(float), s, &ws);
-    if (e != hipSuccess) return e;
+    const int64_t kchunk = split_chunk(K, tail_splits, C::BK);
+    const int nsplit = split_ranges(K, tail_splits, C::BK);
     hipLaunchKernelGGL((gemm_bf16_kernel<C>), dim3((unsigned)(dp + tail * nsplit)), dim3(C::kThreads), C::kLdsBytes,
                        s, static_cast<const __bf16*>(x), static_cast<const __bf16*>(W),
                        static_cast<const __bf16*>(bias), static_cast<__bf16*>(y), (int)M, (int)N, (int)K, group_m,
-                       (int)kchunk, static_cast<float*>(ws), GroupedGemm{}, (int)dp, (int)tail);
-    e = hipGetLastError();
-    if (e == hipSuccess) {
-      hipLaunchKernelGGL((splitk_tile_reduce_kernel<C::BM, C::BN>), dim3((unsigned)tail, C::BM / 16), dim3(256), 0, s,
-                         static_cast<const float*>(ws), (int)nsplit, (int)dp, (int)tail, (int)M, (int)N,
-                         (int)tiles_m, (int)((N + C::BN - 1) / C::BN), group_m, static_cast<const __bf16*>(bias),
-                         static_cast<__bf16*>(y));
-      e = hipGetLastError();
-    }
-    const hipError_t f = scratch_free(ws, s);
-    return e != hipSuccess ? e : f;
+                       (int)kchunk, part, GroupedGemm{}, (int)dp, (int)tail);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL((splitk_tile_reduce_kernel<C::BM, C::BN>), dim3((unsigned)tail, C::BM / 16), dim3(256), 0, s,
+                       static_cast<const float*>(part), nsplit, (int)dp, (int)tail, (int)M, (int)N, (int)tiles_m,
+                       (int)tiles_n, group_m, static_cast<const __bf16*>(bias), static_cast<__bf16*>(y));
+    return hipGetLastError();
   }
-  // K range per split: a whole number of BK slices
-  const int64_t kchunk = part ? ((K + splits - 1) / splits + C::BK - 1) / C::BK * C::BK : K;
-  const int64_t nsplit = part ? (K + kchunk - 1) / kchunk : 1;
+  const bool split = splits > 1;
+  const int64_t kchunk = split ? split_chunk(K, splits, C::BK) : K;
+  const int nsplit = split ? split_ranges(K, splits, C::BK) : 1;
   hipLaunchKernelGGL((gemm_bf16_kernel<C>), dim3((unsigned)(tiles * nsplit)), dim3(C::kThreads), C::kLdsBytes, s,
                      static_cast<const __bf16*>(x), static_cast<const __bf16*>(W),
                      static_cast<const __bf16*>(bias), static_cast<__bf16*>(y), (int)M, (int)N, (int)K,
-                     group_m, (int)kchunk, part, GroupedGemm{}, 0, 0);
+                     group_m, (int)kchunk, split ? part : nullptr, GroupedGemm{}, 0, 0);
   hipError_t e = hipGetLastError();
-  if (e != hipSuccess || !part) return e;
+  if (e != hipSuccess || !split) return e;
   const int64_t MN = M * N;
   const unsigned blocks = (unsigned)std::min<int64_t>(4096, (MN / 4 + 255) / 256);
-  hipLaunchKernelGGL(splitk_reduce_kernel, dim3(blocks), dim3(256), 0, s, part, (int)nsplit,
+  hipLaunchKernelGGL(splitk_reduce_kernel, dim3(blocks), dim3(256), 0, s, part, nsplit,
                      static_cast<const __bf16*>(bias), static_cast<__bf16*>(y), MN, (int)N);
   return hipGetLastError();
 }
@@ -685,102 +692,126 @@ hipError_t launch_gemm_grouped(const void* x, int64_t x_rows, const void* W, int
   return launch_grouped<CfgBig8>(x, x_rows, W, w_stride, y, max_rows, N, K, E, gather, rows, tiles, swiglu_f, s);
 }
 
-hipError_t launch_linear(const void* x, const void* W, const void* bias, void* y, int64_t M,
-                         int64_t N, int64_t K, bool bf16, hipStream_t s) {
-#ifdef OPSCALE_GEMM_CFG
-  if (bf16) return launch_gemm_bf16<OPSCALE_GEMM_CFG>(x, W, bias, y, M, N, K, s);
-#else
-  if (bf16) {
-    // Decode-sized M: the weights dominate and the tiles below would leave
-    // most CUs idle.  OPSCALE_GEMM_SKINNY=0 (or a forced tile below) turns
-    // this path off, =1 takes it wherever it is supported (tuning and tests).
-    const char* sk = getenv("OPSCALE_GEMM_SKINNY");
-    const bool sk_off = (sk && strcmp(sk, "0") == 0) || getenv("OPSCALE_GEMM_TILE");
-    const bool sk_on = sk && strcmp(sk, "1") == 0;
-    if (!sk_off && (sk_on ? skinny_linear_supported(M, N, K) : skinny_linear_preferred(M, N, K)))
-      return launch_linear_skinny(x, W, bias, y, M, N, K, s);
-    // Otherwise decode-sized M splits K over workgroups (fp32 partials in
-    // stream-ordered scratch, summed in split order by a second kernel).
-    // OPSCALE_GEMM_SPLITK=0 turns this off (tuning and tests).
-    const char* spk = getenv("OPSCALE_GEMM_SPLITK");
-    const bool spk_off = (spk && strcmp(spk, "0") == 0) || getenv("OPSCALE_GEMM_TILE");
-    // Tile rows by M: 64 up to 64 rows (the matrix cores work on little
-    // padding), 128 up to 256.  The 128-row tile keeps three K slices in its
-    // LDS ring, so each CU has two weight slices in flight where the 256-row
-    // tile has one: the weights stream from HBM, latency-bound, so 129-256
-    // rows run as two 128-row tiles, without splitting K when those tiles
-    // fill the GPU (at most as slow as 256-row tiles, up to 12 % faster on
-    // the widest weights).  Larger M
-    // takes 256 rows with 256 or 128 columns, whichever gives more
-    // workgroups (ties: 256, which re-reads x half as often).
-    int rows = M <= 64 ? 64 : M <= 256 ? 128 : 256;
-    int splits = 0;
-    if (!spk_off) {
-      if (rows == 64) splits = splitk_count<CfgSk64>(M, N, K);
-      else if (rows == 128) {
-        splits = splitk_count<CfgSk128>(M, N, K);
-        if (splits <= 1 && M > 128) return launch_gemm_bf16<CfgSk128>(x, W, bias, y, M, N, K, s, 1, nullptr);
-      } else {
-        const int s_wide = splitk_count<CfgBig8>(M, N, K), s_mid = splitk_count<CfgMid>(M, N, K);
-        const int64_t w_wide = (int64_t)s_wide * ((N + 255) / 256), w_mid = (int64_t)s_mid * ((N + 127) / 128);
-        if (w_wide >= w_mid && s_wide > 1) splits = s_wide;
-        else { splits = s_mid; rows = 257; }  // 257: the 256x128 tile
+// The tiled configurations a plan can name.
+enum TileCfg { kCfgBig8 = 0, kCfgT192 = 1, kCfgMid = 2, kCfgSk64 = 3, kCfgSk128 = 4 };
+
+template <class C>
+static size_t split_bytes(int64_t M, int64_t N, int64_t K, int splits) {
+  return (size_t)split_ranges(K, splits, C::BK) * M * N * sizeof(float);
+}
+
+template <class C>
+static size_t tail_bytes(int64_t M, int64_t N, int64_t K, int tail_splits) {
+  const int64_t tiles = ((M + C::BM - 1) / C::BM) * ((N + C::BN - 1) / C::BN);
+  return (size_t)split_ranges(K, tail_splits, C::BK) * (tiles % kNumCUs) * C::BM * C::BN * sizeof(float);
+}
+
+// One rule for the path of a linear, shared by the workspace query and the
+// launch.  split_ok == false (no caller workspace) plans only paths that need
+// none: the small-M kernel or unsplit tiles.
+LinearPlan plan_linear(int64_t M, int64_t N, int64_t K, bool bf16, bool split_ok) {
+  LinearPlan p{};
+  if (!bf16) { p.path = LinearPlan::kF32; return p; }
+  const int32_t force_tile = tuning(OPSCALE_TUNE_GEMM_TILE);
+  const int32_t skinny = tuning(OPSCALE_TUNE_GEMM_SKINNY);
+  p.path = LinearPlan::kTiled;
+  // Decode-sized M: the weights dominate and large tiles would leave most CUs
+  // idle.  The small-M kernel reduces its K split in LDS and needs no
+  // workspace.
+  if (force_tile < 0 && skinny != 0 &&
+      (skinny == 1 ? skinny_linear_supported(M, N, K) : skinny_linear_preferred(M, N, K))) {
+    p.path = LinearPlan::kSkinny;
+    return p;
+  }
+  // Otherwise decode-sized M splits K over workgroups (fp32 partials in the
+  // workspace, summed in split order by a second kernel).  Tile rows follow
+  // M: 64 up to 64 rows (the matrix cores work on little padding), 128 up to
+  // 256; larger M takes 256 rows with 256 or 128 columns, whichever gives
+  // more workgroups (ties: 256, which re-reads x half as often).
+  if (force_tile < 0 && split_ok && tuning(OPSCALE_TUNE_GEMM_SPLITK) != 0) {
+    if (M <= 64) {
+      p.splits = splitk_count<CfgSk64>(M, N, K);
+      p.cfg = kCfgSk64;
+      if (p.splits > 1) { p.ws_bytes = split_bytes<CfgSk64>(M, N, K, p.splits); return p; }
+    } else if (M <= 256) {
+      p.splits = splitk_count<CfgSk128>(M, N, K);
+      p.cfg = kCfgSk128;
+      if (p.splits > 1) { p.ws_bytes = split_bytes<CfgSk128>(M, N, K, p.splits); return p; }
+    } else {
+      const int s_wide = splitk_count<CfgBig8>(M, N, K), s_mid = splitk_count<CfgMid>(M, N, K);
+      const int64_t w_wide = (int64_t)s_wide * ((N + 255) / 256), w_mid = (int64_t)s_mid * ((N + 127) / 128);
+      if (w_wide >= w_mid && s_wide > 1) {
+        p.cfg = kCfgBig8; p.splits = s_wide; p.ws_bytes = split_bytes<CfgBig8>(M, N, K, s_wide); return p;
       }
+      if (s_mid > 1) { p.cfg = kCfgMid; p.splits = s_mid; p.ws_bytes = split_bytes<CfgMid>(M, N, K, s_mid); return p; }
     }
-    if (splits > 1) {
-      void* part = nullptr;
-      hipError_t e = scratch_alloc((size_t)splits * M * N * sizeof(float), s, &part);
-      if (e != hipSuccess) return e;
-      float* pp = static_cast<float*>(part);
-      e = rows == 64    ? launch_gemm_bf16<CfgSk64>(x, W, bias, y, M, N, K, s, splits, pp)
-          : rows == 128 ? launch_gemm_bf16<CfgSk128>(x, W, bias, y, M, N, K, s, splits, pp)
-          : rows == 256 ? launch_gemm_bf16<CfgBig8>(x, W, bias, y, M, N, K, s, splits, pp)
-                        : launch_gemm_bf16<CfgMid>(x, W, bias, y, M, N, K, s, splits, pp);
-      const hipError_t f = scratch_free(part, s);
-      return e != hipSuccess ? e : f;
-    }
-    // A last round at most half full runs split over K: 2-4 ranges per tile
-    // (at most one workgroup per CU in all), each at least 8 slices long.
-    // OPSCALE_GEMM_TAIL=0 turns this off (tuning and tests).
-    const char* te = getenv("OPSCALE_GEMM_TAIL");
-    const bool tail_off = te && strcmp(te, "0") == 0;
-    auto tail_splits = [&](int64_t tiles) {
-      const int64_t tail = tiles % kNumCUs;
-      if (tail_off || tiles <= kNumCUs || tail == 0 || tail * 2 > kNumCUs) return 0;
-      const int ts = (int)std::min<int64_t>(std::min<int64_t>(4, kNumCUs / tail), K / (8 * 64));
-      return ts < 2 ? 0 : ts;
-    };
-    // One workgroup per CU at a time, so a launch runs in full rounds plus a
-    // last one (a split last round counts as 1 / splits of a round).  Pick
-    // the tile whose rounds x tile area x relative per-element cost is
-    // smallest: 256x256 moves the fewest operand bytes per flop, 192x256
-    // (about 15 % more per element) and 256x128 (about 30 % more) fill the
-    // last round better when 256x256 would leave it mostly idle.
-    struct Choice { int bm, bn; double cost; };
-    const Choice choices[] = {{256, 256, 1.0}, {192, 256, 1.15}, {256, 128, 1.3}};
-    int best = 0;
+    p.splits = 0;
+  }
+  // 129-256 rows whose 128-row tiles already fill more than half the GPU
+  // (the gate-up projection of a 256-sequence decode batch: 224 tiles) run
+  // unsplit as 128-row tiles: their 3-stage ring keeps two weight slices per
+  // CU in flight.
+  if (force_tile < 0 && M > 128 && M <= 256 && K >= 1024 &&
+      2 * ((N + CfgSk128::BN - 1) / CfgSk128::BN) > kNumCUs / 2) {
+    p.cfg = kCfgSk128;
+    return p;
+  }
+  // A last round at most half full runs split over K: 2-4 ranges per tile
+  // (at most one workgroup per CU in all), each at least 8 slices long.
+  const bool tail_ok = split_ok && tuning(OPSCALE_TUNE_GEMM_TAIL) != 0;
+  auto tail_splits = [&](int64_t tiles) {
+    const int64_t tail = tiles % kNumCUs;
+    if (!tail_ok || tiles <= kNumCUs || tail == 0 || tail * 2 > kNumCUs) return 0;
+    const int ts = (int)std::min<int64_t>(std::min<int64_t>(4, kNumCUs / tail), K / (8 * 64));
+    return ts < 2 ? 0 : ts;
+  };
+  // One workgroup per CU at a time, so a launch runs in full rounds plus a
+  // last one (a split last round counts as 1 / splits of a round).  Pick the
+  // tile whose rounds x tile area x relative per-element cost is smallest:
+  // 256x256 moves the fewest operand bytes per flop, 192x256 (about 15 % more
+  // per element) and 256x128 (about 30 % more) fill the last round better
+  // when 256x256 would leave it mostly idle.
+  struct Choice { int bm, bn; double cost; };
+  static constexpr Choice choices[] = {{256, 256, 1.0}, {192, 256, 1.15}, {256, 128, 1.3}};
+  int best = 0;
+  if (force_tile >= 0 && force_tile < 3) {
+    best = force_tile;
+  } else {
     double best_t = 0;
-    // OPSCALE_GEMM_TILE=256x256 | 192x256 | 256x128 forces a tile (tuning
-    // and tests); anything else is ignored.
-    const char* force = getenv("OPSCALE_GEMM_TILE");
     for (int c = 0; c < 3; ++c) {
-      if (force) {
-        char name[16];
-        snprintf(name, sizeof name, "%dx%d", choices[c].bm, choices[c].bn);
-        if (strcmp(force, name) == 0) { best = c; break; }
-      }
       const int64_t tiles = ((M + choices[c].bm - 1) / choices[c].bm) * ((N + choices[c].bn - 1) / choices[c].bn);
       const int ts = tail_splits(tiles);
       const double rounds = (double)(tiles / kNumCUs) + (tiles % kNumCUs == 0 ? 0.0 : ts ? 1.0 / ts : 1.0);
       const double t = rounds * choices[c].bm * choices[c].bn * choices[c].cost;
       if (c == 0 || t < best_t) { best = c; best_t = t; }
     }
-    const int ts = tail_splits(((M + choices[best].bm - 1) / choices[best].bm) * ((N + choices[best].bn - 1) / choices[best].bn));
-    if (best == 0) return launch_gemm_bf16<CfgBig8>(x, W, bias, y, M, N, K, s, 1, nullptr, ts);
-    if (best == 1) return launch_gemm_bf16<CfgT192>(x, W, bias, y, M, N, K, s, 1, nullptr, ts);
-    return launch_gemm_bf16<CfgMid>(x, W, bias, y, M, N, K, s, 1, nullptr, ts);
   }
-#endif
+  p.cfg = best == 0 ? kCfgBig8 : best == 1 ? kCfgT192 : kCfgMid;
+  p.tail_splits = tail_splits(((M + choices[best].bm - 1) / choices[best].bm) *
+                              ((N + choices[best].bn - 1) / choices[best].bn));
+  if (p.tail_splits > 1)
+    p.ws_bytes = p.cfg == kCfgBig8 ? tail_bytes<CfgBig8>(M, N, K, p.tail_splits)
+                 : p.cfg == kCfgT192 ? tail_bytes<CfgT192>(M, N, K, p.tail_splits)
+                                     : tail_bytes<CfgMid>(M, N, K, p.tail_splits);
+  return p;
+}
+
+hipError_t launch_linear(const LinearPlan& p, const void* x, const void* W, const void* bias, void* y, int64_t M,
+                         int64_t N, int64_t K, void* ws, hipStream_t s) {
+  float* part = static_cast<float*>(ws);
+  switch (p.path) {
+    case LinearPlan::kSkinny:
+      return launch_linear_skinny(x, W, bias, y, M, N, K, s);
+    case LinearPlan::kTiled:
+      switch (p.cfg) {
+        case kCfgBig8: return launch_gemm_bf16<CfgBig8>(x, W, bias, y, M, N, K, s, p.splits, p.tail_splits, part);
+        case kCfgT192: return launch_gemm_bf16<CfgT192>(x, W, bias, y, M, N, K, s, p.splits, p.tail_splits, part);
+        case kCfgMid: return launch_gemm_bf16<CfgMid>(x, W, bias, y, M, N, K, s, p.splits, p.tail_splits, part);
+        case kCfgSk64: return launch_gemm_bf16<CfgSk64>(x, W, bias, y, M, N, K, s, p.splits, p.tail_splits, part);
+        default: return launch_gemm_bf16<CfgSk128>(x, W, bias, y, M, N, K, s, p.splits, p.tail_splits, part);
+      }
+    default: break;
+  }
   const dim3 grid((unsigned)((N + 63) / 64), (unsigned)((M + 63) / 64));
   hipLaunchKernelGGL(gemm_f32_kernel, grid, dim3(256), 0, s, static_cast<const float*>(x),
                      static_cast<const float*>(W), static_cast<const float*>(bias),

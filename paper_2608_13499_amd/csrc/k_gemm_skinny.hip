@@ -133,9 +133,9 @@ hipError_t launch_linear_skinny(const void* x, const void* W, const void* bias, 
   // Every workgroup reads all of x, so x is read ceil(N / 16 NG) times, M / 16 NG
   // times the weight bytes.  32 columns per workgroup (NG = 2) halve that and
   // win from M = 16 on while they still give >= 192 workgroups; otherwise the
-  // extra workgroups of NG = 1 win.  OPSCALE_SKINNY_NG=1|2 forces it (tests).
-  const char* ng_env = getenv("OPSCALE_SKINNY_NG");
-  const int ng = ng_env ? atoi(ng_env) : (M >= 16 && (N + 31) / 32 >= 192 ? 2 : 1);
+  // extra workgroups of NG = 1 win.  OPSCALE_TUNE_SKINNY_NG forces it.
+  const int32_t forced = tuning(OPSCALE_TUNE_SKINNY_NG);
+  const int ng = forced == 1 || forced == 2 ? forced : (M >= 16 && (N + 31) / 32 >= 192 ? 2 : 1);
   if (ng == 2) {
     if (M <= 16) return launch_skinny<1, 2, 4>(x, W, bias, y, M, N, K, s);
     if (M <= 32) return launch_skinny<2, 2, 4>(x, W, bias, y, M, N, K, s);

@@ -313,9 +313,8 @@ hipError_t launch_fused_moe(const void* x, const void* w1, const void* w2, const
   // act = silu(W1g[e] x[token]) * (W1u[e] x[token])   (rows gathered), [R, F]:
   // the SwiGLU sits in the GEMM's epilogue when an expert's gate-up weight
   // spans less than 4 GB (32-bit row offsets); else gate_up [R, 2F] first
-  // (OPSCALE_MOE_FUSE=0 forces the unfused path, for tests)
-  const char* fz = getenv("OPSCALE_MOE_FUSE");
-  if ((int64_t)2 * F * H * 2 < ((int64_t)1 << 32) && !(fz && strcmp(fz, "0") == 0)) {
+  // (OPSCALE_TUNE_MOE_FUSE = 0 forces the unfused path, for tests)
+  if ((int64_t)2 * F * H * 2 < ((int64_t)1 << 32) && tuning(OPSCALE_TUNE_MOE_FUSE) != 0) {
     if ((e = launch_gemm_grouped(x, T, w1, (int64_t)2 * F * H, w.act, R, 2 * (int64_t)F, H, E, bm, w.gather, w.rows,
                                  w.tiles, F, s)) != hipSuccess)
       return e;

@@ -6,15 +6,34 @@
 #include <stddef.h>
 #include <stdint.h>
 
+#include "opscale.h"
+
 namespace opscale {
+
+// Process-wide tuning and test overrides set through opscale_set_tuning;
+// -1 means automatic (the shape decides).
+int32_t tuning(opscale_tune knob);
 
 hipError_t launch_rmsnorm(const void* x, const void* w, void* y, int64_t M, int64_t H, float eps,
                           bool bf16, hipStream_t s);
 
 hipError_t launch_swiglu(const void* gu, void* out, int64_t M, int64_t F, bool bf16, hipStream_t s);
 
-hipError_t launch_linear(const void* x, const void* W, const void* bias, void* y, int64_t M,
-                         int64_t N, int64_t K, bool bf16, hipStream_t s);
+// The path of one linear call: which kernel, which tile, how K is split and
+// how much caller workspace the split partials need.  split_ok == false
+// plans only paths that need no workspace.  The workspace query and the
+// launch both take it from plan_linear, so they always agree.
+struct LinearPlan {
+  enum Path { kF32 = 0, kSkinny = 1, kTiled = 2 };
+  int path;
+  int cfg;          // tiled: which block tile (k_gemm.hip)
+  int splits;       // > 1: every tile split over K (partials [splits, M, N] fp32)
+  int tail_splits;  // > 1: only the last partial round split over K
+  size_t ws_bytes;  // workspace the partials need (0: none)
+};
+LinearPlan plan_linear(int64_t M, int64_t N, int64_t K, bool bf16, bool split_ok);
+hipError_t launch_linear(const LinearPlan& plan, const void* x, const void* W, const void* bias, void* y, int64_t M,
+                         int64_t N, int64_t K, void* ws, hipStream_t s);
 
 // Grouped bf16 GEMM of a mixture-of-experts layer: output rows grouped by
 // expert (expert e owns rows [rows[e], rows[e+1]) and tile-rows [tiles[e],
@@ -79,11 +98,6 @@ hipError_t launch_moe_topk(const float* logits, int32_t* ids, float* wts, int64_
 hipError_t launch_fused_moe(const void* x, const void* w1, const void* w2, const int32_t* ids, const float* wts,
                             void* out, int64_t T, int32_t H, int32_t F, int32_t E, int32_t k, void* ws,
                             hipStream_t s);
-
-// Stream-ordered scratch from a per-device pool the library keeps (freed
-// memory is reused by later calls; nothing is returned to the driver).
-hipError_t scratch_alloc(size_t bytes, hipStream_t s, void** p);
-hipError_t scratch_free(void* p, hipStream_t s);
 
 // Reads `bytes` of `buf` through the caches (evicts L2 and the last-level
 // cache, leaving only clean lines, before a timed iteration).

@@ -26,3 +26,18 @@ def pytest_collection_modifyitems(config, items):
     for it in items:
         if "gpu" in it.keywords:
             it.add_marker(skip)
+
+
+@pytest.fixture
+def tune():
+    """Force library path choices for one test (opscale_set_tuning), e.g.
+    tune(gemm_tile=0, gemm_splitk=0); every knob is automatic again after it."""
+    import paper_2608_13499_amd as ops
+
+    def set_(**knobs):
+        for name, value in knobs.items():
+            ops.opscale_set_tuning(getattr(ops._lib, "TUNE_" + name.upper()), value)
+
+    yield set_
+    for knob in range(ops._lib.TUNE_MOE_FUSE + 1):
+        ops.opscale_set_tuning(knob, ops._lib.TUNE_AUTO)

@@ -71,12 +71,54 @@ def test_rmsnorm_validation(lib):
 
 
 def test_linear_validation(lib):
-    assert lib.opscale_linear(A16, A16 * 2, None, A16 * 4, 8, 256, 100, 1, None, None) == 1  # K*2 % 16
-    assert lib.opscale_linear(A16, A16 * 2, None, A16 * 4, 8, 12, 64, 1, None, None) == 1  # N*2 % 16
-    assert lib.opscale_linear(A16, A16 * 2, None, A16, 8, 256, 64, 1, None, None) == 1  # y aliases x
-    assert lib.opscale_linear(A16, None, None, A16 * 4, 8, 256, 64, 1, None, None) == 1
-    assert lib.opscale_linear(A16, A16 * 2, A16 + 4, A16 * 4, 8, 256, 64, 1, None, None) == 1  # bias align
-    assert lib.opscale_linear(None, None, None, None, 0, 256, 64, 1, None, None) == 0
+    f = lib.opscale_linear
+    assert f(A16, A16 * 2, None, A16 * 4, 8, 256, 100, 1, None, 0, None, None) == 1  # K*2 % 16
+    assert f(A16, A16 * 2, None, A16 * 4, 8, 12, 64, 1, None, 0, None, None) == 1  # N*2 % 16
+    assert f(A16, A16 * 2, None, A16, 8, 256, 64, 1, None, 0, None, None) == 1  # y aliases x
+    assert f(A16, None, None, A16 * 4, 8, 256, 64, 1, None, 0, None, None) == 1
+    assert f(A16, A16 * 2, A16 + 4, A16 * 4, 8, 256, 64, 1, None, 0, None, None) == 1  # bias align
+    assert f(None, None, None, None, 0, 256, 64, 1, None, 0, None, None) == 0
+
+
+G = 1 << 34  # fake addresses spaced far apart (never dereferenced)
+
+
+def test_linear_workspace(lib):
+    """The split partials live in a caller workspace whose size the query
+    returns; too small a workspace is rejected before anything is enqueued."""
+    size = lib.opscale_linear_workspace_size
+    # 100 rows: 128-row tiles, 16 of them over N = 4096, so K = 4096 splits
+    # into min(256 / 16, 4096 / 512) = 8 ranges of fp32 [M, N] partials
+    assert size(100, 4096, 4096, 1) == 8 * 100 * 4096 * 4
+    # the 8871-token gate-up projection: 35 x 112 tiles of 256 x 256 leave a
+    # last round of 80 tiles, split into min(4, 256 // 80, 4096 // 512) = 3
+    # K ranges of compact fp32 tiles
+    assert size(8871, 28672, 4096, 1) == 3 * 80 * 256 * 256 * 4
+    assert size(8, 4096, 4096, 1) == 0  # small-M kernel: reduces in LDS
+    assert size(100, 4096, 4096, 0) == 0  # fp32 path
+    assert size(0, 4096, 4096, 1) == 0
+    f = lib.opscale_linear
+    need = size(100, 4096, 4096, 1)
+    x, W, y, ws = G, 2 * G, 3 * G, 4 * G
+    assert f(x, W, None, y, 100, 4096, 4096, 1, ws, need - 1, None, None) == 3
+    assert "workspace" in _err(lib)
+    assert f(x, W, None, y, 100, 4096, 4096, 1, ws + 8, need, None, None) == 1  # misaligned
+    assert f(x, W, None, y, 100, 4096, 4096, 1, y, need, None, None) == 1  # overlaps y
+    assert "overlap" in _err(lib)
+
+
+def test_tuning_hook(lib):
+    TILE, SPLITK, NG = 0, 2, 4
+    assert lib.opscale_set_tuning(99, 0) == 1 and lib.opscale_get_tuning(99) == -1
+    assert lib.opscale_set_tuning(TILE, 3) == 1  # three tiles: 0, 1, 2
+    assert lib.opscale_set_tuning(NG, 0) == 1  # 16 or 32 columns: 1, 2
+    assert lib.opscale_get_tuning(SPLITK) == -1
+    try:
+        assert lib.opscale_set_tuning(SPLITK, 0) == 0 and lib.opscale_get_tuning(SPLITK) == 0
+        assert lib.opscale_linear_workspace_size(100, 4096, 4096, 1) == 0  # no split planned
+    finally:
+        assert lib.opscale_set_tuning(SPLITK, -1) == 0
+    assert lib.opscale_linear_workspace_size(100, 4096, 4096, 1) > 0
 
 
 def test_swiglu_validation(lib):

@@ -66,13 +66,13 @@ def _moe_case(ops, T, H, F, E, k, seed, ids=None, wts=None):
     return f64(out), ref
 
 
-@pytest.mark.parametrize("fuse", ["1", "0"])
+@pytest.mark.parametrize("fuse", [-1, 0])
 @pytest.mark.parametrize("T,H,F,E,k", [(37, 64, 96, 8, 2), (300, 128, 256, 64, 8), (1, 64, 64, 4, 1),
                                         (600, 256, 512, 3, 2), (257, 96, 40, 16, 4)])
-def test_fused_moe(ops, monkeypatch, fuse, T, H, F, E, k):
+def test_fused_moe(ops, tune, fuse, T, H, F, E, k):
     """Both paths: the SwiGLU fused into the gate-up GEMM's epilogue (gate
     and up rows interleaved), and the separate gate-up output plus SwiGLU."""
-    monkeypatch.setenv("OPSCALE_MOE_FUSE", fuse)
+    tune(moe_fuse=fuse)  # -1: automatic (fused at these sizes); 0: unfused
     say(f"fused_moe T={T} H={H} F={F} E={E} topk={k} fuse={fuse}")
     got, ref = _moe_case(ops, T, H, F, E, k, seed=T * 7 + E)
     assert_close(got, ref, "bf16", "fused_moe")

@@ -16,6 +16,10 @@ from parity_util import assert_close, cuda, f64, gen, say, torch_dtype
 pytestmark = pytest.mark.gpu
 
 
+TILES = {"256x256": 0, "192x256": 1, "256x128": 2}  # opscale_tune GEMM_TILE values
+SCHEDULES = {"grid": 0, "list": 1}                   # opscale_tune PREFILL_SCHEDULE values
+
+
 @pytest.fixture(scope="module")
 def ops():
     import torch
@@ -75,11 +79,11 @@ def test_linear(ops, dtype, M, N, K, bias):
 @pytest.mark.parametrize("tile", ["256x256", "192x256", "256x128"])
 @pytest.mark.parametrize("M,N,K,bias", [(300, 264, 200, True), (513, 1024, 4096, False), (1, 256, 64, False),
                                         (700, 520, 136, False)])
-def test_linear_each_tile(ops, monkeypatch, tile, M, N, K, bias):
+def test_linear_each_tile(ops, tune, tile, M, N, K, bias):
     """Every bf16 tile shape the dispatcher can pick, with ragged M, N and K."""
     import torch
     say(f"linear bf16 tile={tile} M={M} N={N} K={K} bias={bias}")
-    monkeypatch.setenv("OPSCALE_GEMM_TILE", tile)
+    tune(gemm_tile=TILES[tile])
     x = gen(23, "x", (M, K), "bf16")
     W = gen(23, "w_qkv", (N, K), "bf16", std=0.02)
     b = gen(23, "bias", (N,), "bf16") if bias else None
@@ -93,15 +97,13 @@ def test_linear_each_tile(ops, monkeypatch, tile, M, N, K, bias):
     (64, 4096, 14336, False), (100, 1000, 4096, True), (129, 264, 256, False), (256, 6144, 4096, False),
     (256, 4104, 32, True),
 ])
-@pytest.mark.parametrize("ng", ["1", "2"])
-def test_linear_small_m(ops, monkeypatch, ng, M, N, K, bias):
+@pytest.mark.parametrize("ng", [1, 2])
+def test_linear_small_m(ops, tune, ng, M, N, K, bias):
     """The decode-batch path (M <= 256, K % 32 == 0), forced on, with 16 and
     32 columns per workgroup: every row-group count, N tails shorter than one
     column group, K of one k-step per wave and fewer k-steps than waves."""
     import torch
-    monkeypatch.delenv("OPSCALE_GEMM_TILE", raising=False)
-    monkeypatch.setenv("OPSCALE_GEMM_SKINNY", "1")
-    monkeypatch.setenv("OPSCALE_SKINNY_NG", ng)
+    tune(gemm_skinny=1, skinny_ng=ng)
     say(f"linear bf16 small-M NG={ng} M={M} N={N} K={K} bias={bias}")
     x = gen(24, "x", (M, K), "bf16")
     W = gen(24, "w_qkv", (N, K), "bf16", std=0.02)
@@ -119,51 +121,61 @@ def test_linear_small_m(ops, monkeypatch, ng, M, N, K, bias):
     (96, 4096, 4096, False), (128, 28672, 1024, True), (256, 4096, 14336, False),
     (200, 16648, 1024, True), (256, 28672, 4096, False),
 ])
-def test_linear_split_k(ops, monkeypatch, M, N, K, bias):
+def test_linear_split_k(ops, tune, M, N, K, bias):
     """Decode-sized M with K split over workgroups (fp32 partials summed in
     split order), on each tile the path picks (64 or 128 rows up to 256, 256
     rows with 256 or 128 columns above): ragged M, N and K, a K range that
     does not divide evenly, bias; 129-256 rows whose 128-row tiles fill the
-    GPU without a split (the last two cases); bitwise equal across calls."""
+    GPU without a split (the last two cases); bitwise equal across calls.
+    The partials live in the caller's workspace (poisoned before the call:
+    its contents on entry must not matter); without one the same shapes take
+    an unsplit path."""
     import torch
-    monkeypatch.delenv("OPSCALE_GEMM_TILE", raising=False)
-    monkeypatch.delenv("OPSCALE_GEMM_SPLITK", raising=False)
-    monkeypatch.setenv("OPSCALE_GEMM_SKINNY", "0")
+    tune(gemm_skinny=0)
     say(f"linear bf16 split-K M={M} N={N} K={K} bias={bias}")
     x = gen(25, "x", (M, K), "bf16")
     W = gen(25, "w_qkv", (N, K), "bf16", std=0.02)
     b = gen(25, "bias", (N,), "bf16") if bias else None
-    y = ops.opscale_linear(cuda(x), cuda(W), None if b is None else cuda(b))
-    y2 = ops.opscale_linear(cuda(x), cuda(W), None if b is None else cuda(b))
+    args = (cuda(x), cuda(W), None if b is None else cuda(b))
+    need = ops.opscale_linear_workspace_size(M, N, K)
+    ws = torch.full((max(need, 16),), 0x7f, dtype=torch.uint8, device="cuda")  # fp32 3.4e38 if read
+    y = ops.opscale_linear(*args, workspace=ws)
+    y2 = ops.opscale_linear(*args, workspace=ws)
+    y0 = ops.opscale_linear(*args, workspace=False)
     torch.cuda.synchronize()
     assert torch.equal(y, y2)
-    assert_close(f64(y.cpu()), oracle.linear(f64(x), f64(W), None if b is None else f64(b)), "bf16", "linear")
+    ref = oracle.linear(f64(x), f64(W), None if b is None else f64(b))
+    assert_close(f64(y.cpu()), ref, "bf16", "linear")
+    assert_close(f64(y0.cpu()), ref, "bf16", "linear without a workspace")
 
 
 @pytest.mark.parametrize("tile,M,N,K,bias", [("256x256", 4352, 4096, 1024, True), ("256x256", 4300, 4104, 2056, False),
                                              ("192x256", 4352, 4096, 1024, False)])
-def test_linear_split_tail(ops, monkeypatch, tile, M, N, K, bias):
+def test_linear_split_tail(ops, tune, tile, M, N, K, bias):
     """More tiles than CUs with the last round at most half full: those tiles
     run as 2-4 K ranges (fp32 partials summed in split order) in the same
     launch as the others.  Ragged M, N and K, bias; bitwise equal across
-    calls; the same result with the split tail turned off."""
+    calls; the same result with the split tail turned off and with no
+    workspace (which also plans no split)."""
     import torch
     say(f"linear bf16 split tail tile={tile} M={M} N={N} K={K} bias={bias}")
-    monkeypatch.setenv("OPSCALE_GEMM_TILE", tile)
-    monkeypatch.delenv("OPSCALE_GEMM_TAIL", raising=False)
+    tune(gemm_tile=TILES[tile])
+    assert ops.opscale_linear_workspace_size(M, N, K) > 0
     x = gen(26, "x", (M, K), "bf16")
     W = gen(26, "w_qkv", (N, K), "bf16", std=0.02)
     b = gen(26, "bias", (N,), "bf16") if bias else None
     args = (cuda(x), cuda(W), None if b is None else cuda(b))
     y = ops.opscale_linear(*args)
     y2 = ops.opscale_linear(*args)
-    monkeypatch.setenv("OPSCALE_GEMM_TAIL", "0")
+    yn = ops.opscale_linear(*args, workspace=False)
+    tune(gemm_tail=0)
     y0 = ops.opscale_linear(*args)
     torch.cuda.synchronize()
     assert torch.equal(y, y2)
     ref = oracle.linear(f64(x), f64(W), None if b is None else f64(b))
     assert_close(f64(y.cpu()), ref, "bf16", "linear split tail")
     assert_close(f64(y0.cpu()), ref, "bf16", "linear without split tail")
+    assert torch.equal(y0, yn)  # both unsplit
 
 
 def test_linear_identity_weight(ops):
@@ -239,12 +251,12 @@ def test_attn_prefill(ops, dtype, lens, Hq, Hkv, D, causal, packed):
     ([900, 5, 1, 260], 3, 3, 128),                   # G = 1 (128-query tiles)
     ([1, 2, 3, 17] * 20 + [700], 8, 1, 64),          # 81 prompts: more than one wave of 64
 ])
-def test_attn_prefill_schedules(ops, monkeypatch, lens, Hq, Hkv, D):
+def test_attn_prefill_schedules(ops, tune, lens, Hq, Hkv, D):
     """Both schedules (grid; level-major work list) against the oracle, and
     bitwise equal to each other (each tile is computed the same way)."""
     outs = {}
     for sched in ("grid", "list"):
-        monkeypatch.setenv("OPSCALE_PREFILL_SCHEDULE", sched)
+        tune(prefill_schedule=SCHEDULES[sched])
         say(f"attn_prefill bf16 schedule={sched} lens={lens} Hq={Hq} Hkv={Hkv} D={D}")
         got, ref = _prefill_case(ops, "bf16", lens, Hq, Hkv, D, True, True)
         assert_close(got, ref, "bf16", f"attn_prefill ({sched})")
@@ -252,19 +264,19 @@ def test_attn_prefill_schedules(ops, monkeypatch, lens, Hq, Hkv, D):
     assert np.array_equal(outs["grid"], outs["list"])
 
 
-def test_attn_prefill_many_prompts(ops, monkeypatch):
+def test_attn_prefill_many_prompts(ops, tune):
     """More prompts than the work list holds in LDS: the launcher takes the grid
     even when the list is asked for."""
-    monkeypatch.setenv("OPSCALE_PREFILL_SCHEDULE", "list")
+    tune(prefill_schedule=SCHEDULES["list"])
     say("attn_prefill bf16 1101 prompts")
     lens = ([1, 2, 3, 17] * 276)[:1101]
     got, ref = _prefill_case(ops, "bf16", lens, 8, 2, 128, True, True)
     assert_close(got, ref, "bf16", "attn_prefill 1101 prompts")
 
 
-def test_attn_prefill_1024_prompts_list(ops, monkeypatch):
+def test_attn_prefill_1024_prompts_list(ops, tune):
     """The largest batch the work list takes (1024 prompts, 16 waves of 64)."""
-    monkeypatch.setenv("OPSCALE_PREFILL_SCHEDULE", "list")
+    tune(prefill_schedule=SCHEDULES["list"])
     say("attn_prefill bf16 1024 prompts (work list)")
     lens = ([1, 40, 3, 97, 0, 64] * 171)[:1024]
     got, ref = _prefill_case(ops, "bf16", lens, 8, 2, 64, True, True)
