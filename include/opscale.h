@@ -218,6 +218,32 @@ opscale_status opscale_attn_decode(const void* q, int64_t q_row_stride, const vo
                                    opscale_dtype dt, void* workspace, size_t workspace_bytes,
                                    hipStream_t stream, opscale_timing* timing);
 
+/*
+ * opscale_attn_decode without a workspace argument, for callers that cannot
+ * allocate device memory: code under HIP graph capture, tight serving loops,
+ * harnesses that forbid allocation.  Same operation, arguments, layouts and
+ * kernels as opscale_attn_decode (and bitwise the same output); the split-KV
+ * partials go to a scratch array the library holds in device memory, one copy
+ * per GPU it runs on, kept until the process ends
+ * (opscale_attn_decode_noalloc_max_bytes() bytes, 64 MiB).  No device memory
+ * is allocated or freed, and no timing is taken (the call is asynchronous).
+ *  - Sizes whose opscale_attn_decode_workspace_size(B, Hq, D,
+ *    max_context_len) exceeds that maximum return OPSCALE_ERR_WORKSPACE with
+ *    nothing enqueued (e.g. B = 1024, Hq = 64, D = 128 needs 42.6 MB: fits).
+ *  - Every call on one GPU shares that GPU's array: calls that overlap in
+ *    time on one GPU (on different streams, or from different host threads)
+ *    race on it and must be ordered by the caller.  Nothing in the array needs
+ *    to start at zero; each call writes what it later reads.
+ */
+opscale_status opscale_attn_decode_noalloc(const void* q, int64_t q_row_stride, const void* k_cache,
+                                           const void* v_cache, const int32_t* block_table,
+                                           const int32_t* context_lens, void* o, int32_t B, int32_t Hq,
+                                           int32_t Hkv, int32_t D, int32_t block_size, int32_t max_blocks_per_seq,
+                                           int64_t num_blocks, int32_t max_context_len, float scale,
+                                           opscale_dtype dt, hipStream_t stream);
+/* Bytes of the scratch array opscale_attn_decode_noalloc uses (its size limit). */
+size_t opscale_attn_decode_noalloc_max_bytes(void);
+
 /* ---------------------------------------------------------------------------
  * The operators around attention in a full decoder layer.
  * ------------------------------------------------------------------------- */

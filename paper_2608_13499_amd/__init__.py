@@ -12,6 +12,7 @@ from ._lib import (  # noqa: F401
     opscale_attn_prefill, opscale_set_tuning, opscale_get_tuning,
     opscale_rope, opscale_reshape_and_cache, opscale_add_rmsnorm,
     opscale_attn_decode_workspace_size, opscale_attn_decode, opscale_op_profile,
+    opscale_attn_decode_noalloc, opscale_attn_decode_noalloc_max_bytes,
     desc_rmsnorm, desc_linear, desc_swiglu, desc_attn_prefill, desc_attn_decode,
     desc_rope, desc_reshape_and_cache, desc_add_rmsnorm,
     opscale_moe_topk, opscale_fused_moe_workspace_size, opscale_fused_moe, desc_fused_moe,

@@ -141,6 +141,9 @@ EXPORTS = {
     "opscale_attn_decode": (c_i32, [c_vp, c_i64, c_vp, c_vp, c_vp, c_vp, c_vp, c_i32, c_i32, c_i32, c_i32, c_i32,
                                     c_i32, c_i64, c_i32, c_f32, c_i32, c_vp, c_sz, c_vp,
                                     ctypes.POINTER(Timing)]),
+    "opscale_attn_decode_noalloc": (c_i32, [c_vp, c_i64, c_vp, c_vp, c_vp, c_vp, c_vp, c_i32, c_i32, c_i32, c_i32,
+                                            c_i32, c_i32, c_i64, c_i32, c_f32, c_i32, c_vp]),
+    "opscale_attn_decode_noalloc_max_bytes": (c_sz, []),
     "opscale_op_profile": (c_i32, [ctypes.POINTER(OpDesc), c_i32, c_i32, c_vp, c_sz, c_vp,
                                    ctypes.POINTER(Profile)]),
     "opscale_rope": (c_i32, [c_vp, c_vp, c_i64, c_i64, c_vp, c_i64, c_i32, c_i32, c_i32, ctypes.c_double, c_i32,
@@ -385,6 +388,28 @@ def opscale_attn_decode(q, k_cache, v_cache, block_table, context_lens, max_cont
                                    workspace.numel() * workspace.element_size(), _stream(stream),
                                    ctypes.byref(t) if t else None))
     return (out, t) if timed else out
+
+
+def opscale_attn_decode_noalloc(q, k_cache, v_cache, block_table, context_lens, max_context_len: int,
+                                scale: float, out, stream=None):
+    """opscale_attn_decode with the library's own scratch (no workspace, no
+    allocation, no timing).  `out` [B, Hq, D] must be given."""
+    lib = load()
+    _dev(q, k_cache, v_cache, block_table, context_lens, out)
+    for n, t_ in (("k_cache", k_cache), ("v_cache", v_cache), ("block_table", block_table),
+                  ("context_lens", context_lens), ("out", out)):
+        _contig(n, t_)
+    B, Hq, D = q.shape
+    _heads_view("q", q, Hq, D)
+    num_blocks, bs, Hkv, _ = k_cache.shape
+    _check(lib.opscale_attn_decode_noalloc(_ptr(q), q.stride(0), _ptr(k_cache), _ptr(v_cache), _ptr(block_table),
+                                           _ptr(context_lens), _ptr(out), B, Hq, Hkv, D, bs, block_table.shape[1],
+                                           num_blocks, max_context_len, scale, _dt(q), _stream(stream)))
+    return out
+
+
+def opscale_attn_decode_noalloc_max_bytes() -> int:
+    return int(load().opscale_attn_decode_noalloc_max_bytes())
 
 
 def opscale_rope(q, k, positions, theta: float, stream=None, timed: bool = False):

@@ -6,6 +6,7 @@
 #include <cstdarg>
 #include <cstdio>
 #include <functional>
+#include <mutex>
 #include <string>
 #include <vector>
 
@@ -468,6 +469,38 @@ opscale_status time_loop(const std::function<hipError_t()>& launch, hipStream_t 
   return OPSCALE_OK;
 }
 
+// ----------------------------------------- allocation-free decode scratch ---
+// The scratch of opscale_attn_decode_noalloc: a file-scope device array.
+// Each GPU the library runs on holds its own copy, at its own address, until
+// the process ends.  In host code `scratch` names a host-side stand-in, not
+// device memory, so its device address is looked up once per device (with
+// that device current) and only that address is ever passed to a kernel.
+constexpr size_t kStaticScratchBytes = (size_t)64 << 20;
+static __device__ __align__(256) unsigned char scratch[kStaticScratchBytes];
+
+constexpr int kMaxScratchDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxScratchDevices];
+
+opscale_status static_scratch(void** out) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+  if (dev < 0 || dev >= kMaxScratchDevices)
+    return fail(OPSCALE_ERR_UNSUPPORTED, "attn_decode_noalloc: device %d beyond the %d supported", dev,
+                kMaxScratchDevices);
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return hip_fail(e, "hipGetSymbolAddress(scratch)");
+    if (!p) return fail(OPSCALE_ERR_HIP, "hipGetSymbolAddress(scratch) returned no address");
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
+  return OPSCALE_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -608,6 +641,30 @@ opscale_status opscale_attn_decode(const void* q, int64_t q_row_stride, const vo
   }
   return st;
 }
+
+opscale_status opscale_attn_decode_noalloc(const void* q, int64_t q_row_stride, const void* k_cache,
+                                           const void* v_cache, const int32_t* block_table,
+                                           const int32_t* context_lens, void* o, int32_t B, int32_t Hq,
+                                           int32_t Hkv, int32_t D, int32_t block_size, int32_t max_blocks_per_seq,
+                                           int64_t num_blocks, int32_t max_context_len, float scale,
+                                           opscale_dtype dt, hipStream_t stream) {
+  void* ws = nullptr;
+  opscale_status st = static_scratch(&ws);
+  if (st != OPSCALE_OK) return st;
+  st = check_decode(q, q_row_stride, k_cache, v_cache, block_table, context_lens, o, B, Hq, Hkv, D, block_size,
+                    max_blocks_per_seq, num_blocks, max_context_len, scale, dt, ws, kStaticScratchBytes);
+  if (st == OPSCALE_ERR_WORKSPACE)
+    return fail(OPSCALE_ERR_WORKSPACE, "attn_decode_noalloc: %zu bytes of scratch needed, the library holds %zu",
+                opscale::decode_workspace_bytes(B, Hq, D, max_context_len), kStaticScratchBytes);
+  if (st != OPSCALE_OK) return st;
+  if (B == 0) return OPSCALE_OK;
+  const hipError_t e = opscale::launch_attn_decode(q, q_row_stride, k_cache, v_cache, block_table, context_lens, o,
+                                                   B, Hq, Hkv, D, block_size, max_blocks_per_seq, num_blocks,
+                                                   max_context_len, scale, dt == OPSCALE_BF16, ws, stream);
+  return e == hipSuccess ? OPSCALE_OK : hip_fail(e, "attn_decode_noalloc launch");
+}
+
+size_t opscale_attn_decode_noalloc_max_bytes(void) { return kStaticScratchBytes; }
 
 opscale_status opscale_rope(void* q, void* k, int64_t q_row_stride, int64_t k_row_stride,
                             const int32_t* positions, int64_t T, int32_t Hq, int32_t Hkv, int32_t D,
