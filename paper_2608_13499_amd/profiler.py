@@ -6,9 +6,14 @@ built from a sparse random sample instead of an exhaustive sweep.
   (prefill: B sequences of L tokens each with B * L capped; decode: B
   sequences with a context of L keys), plus the domain's corners so that
   every later query is an interpolation.
-* Interpolation: piecewise linear over the Delaunay triangulation of the
-  sampled points in (log B, log L), on log T_v.  Power laws are reproduced
-  exactly; a query outside the sampled hull takes the nearest sample.
+* Interpolation: the operators that work token by token (the norms, the
+  linears, SiLU-mul, RoPE, the cache write) depend on (B, L) only through
+  their token count (B * L in prefill, B in decode), so their T_v is
+  interpolated piecewise linearly in log tokens, from samples spread
+  log-uniformly over the token range.  Attention depends on B and L apart:
+  piecewise linear over the Delaunay triangulation of the sampled points in
+  (log B, log L).  Both work on log T_v, so power laws are reproduced
+  exactly; a 2-D query outside the sampled hull takes the nearest sample.
 * Structural equivalence: a profile is keyed by the operator's structure (its
   kind, phase, the shapes that do not vary with B and L, and dtype), so the 32
   identical layers of an 8B model, or two models sharing an operator shape,
@@ -141,6 +146,87 @@ class PiecewiseModel:
         return float(out[0]) if np.ndim(B) == 0 else out
 
 
+# Operators whose work is a function of the token count alone.
+TOKENWISE_KINDS = frozenset({"rmsnorm", "add_rmsnorm", "linear", "swiglu", "rope", "reshape_and_cache"})
+
+
+def tokens_of(phase: str, B: int, L: int) -> int:
+    """Token rows one call processes: B prompts of L tokens in prefill, one new
+    token per sequence in decode."""
+    return B * L if phase == PREFILL else B
+
+
+class TokenModel:
+    """Piecewise-linear interpolation of log(value) in log(tokens), with the
+    end segments extended past the sampled range."""
+
+    def __init__(self, phase: str, points: Sequence[Tuple[int, int]], values: Sequence[float]):
+        self.phase = phase
+        toks = np.array([tokens_of(phase, B, L) for B, L in points], np.float64)
+        logv = np.log(np.asarray(values, np.float64))
+        xs = np.unique(np.log(toks))
+        if len(xs) < 2:
+            raise ValueError("at least 2 distinct token counts are needed")
+        # equal token counts (different B, L): their mean log value
+        self._x = xs
+        self._y = np.array([logv[np.isclose(np.log(toks), x)].mean() for x in xs])
+        self.points = [tuple(map(int, p)) for p in points]
+        self.values = [float(v) for v in values]
+
+    def predict(self, B, L):
+        q = np.log(np.array([tokens_of(self.phase, b, l) for b, l in
+                             zip(np.atleast_1d(B), np.atleast_1d(L))], np.float64))
+        x, y = self._x, self._y
+        v = np.interp(q, x, y)
+        lo, hi = q < x[0], q > x[-1]
+        v[lo] = y[0] + (q[lo] - x[0]) * (y[1] - y[0]) / (x[1] - x[0])
+        v[hi] = y[-1] + (q[hi] - x[-1]) * (y[-1] - y[-2]) / (x[-1] - x[-2])
+        out = np.exp(v)
+        return float(out[0]) if np.ndim(B) == 0 else out
+
+
+def sample_points_for(sig: "OpSignature", domain: "Domain", n: int, seed: int,
+                      with_corners: bool = True) -> List[Tuple[int, int]]:
+    """Sample points of an operator: for a token-wise operator, token counts
+    log-uniform over the domain's range (each realized by a (B, L) inside
+    it), with the smallest and largest counts; otherwise `sample_points`."""
+    if sig.kind not in TOKENWISE_KINDS:
+        return sample_points(domain, n, seed, with_corners)
+    rng = np.random.default_rng(seed)
+    if sig.phase == PREFILL:
+        t_lo, t_hi = domain.b_min * domain.l_min, min(domain.max_tokens, domain.b_max * domain.l_max)
+    else:
+        t_lo, t_hi = domain.b_min, domain.b_max
+    pts = set()
+    if with_corners:
+        pts.add((domain.b_min, domain.l_min))
+        pts.add((t_hi // domain.l_min if sig.phase == PREFILL and t_hi // domain.l_min <= domain.b_max else
+                 domain.b_max, t_hi // domain.b_max if sig.phase == PREFILL else domain.l_min))
+    seen = {tokens_of(sig.phase, *p) for p in pts}
+    # stratified: one point in each of n equal slices of the log token range
+    # (a random place in it), so no stretch is left bare; a slice too narrow
+    # to hold a new integer count is skipped
+    for k in range(n):
+        for _ in range(50):
+            u = (k + rng.uniform()) / n
+            T = int(round(math.exp(math.log(t_lo) + u * (math.log(t_hi) - math.log(t_lo)))))
+            if sig.phase == PREFILL:
+                # a prompt count that can hold T tokens, then the length
+                b_hi = min(domain.b_max, T // domain.l_min)
+                b_lo = max(domain.b_min, -(-T // domain.l_max))
+                if b_lo > b_hi:
+                    continue
+                B = int(round(math.exp(rng.uniform(math.log(b_lo), math.log(b_hi)))))
+                L = max(domain.l_min, min(domain.l_max, int(round(T / B))))
+            else:
+                B, L = T, int(round(math.exp(rng.uniform(math.log(domain.l_min), math.log(domain.l_max)))))
+            if domain.contains(B, L) and tokens_of(sig.phase, B, L) not in seen:
+                pts.add((B, L))
+                seen.add(tokens_of(sig.phase, B, L))
+                break
+    return sorted(pts)
+
+
 def relative_errors(model: PiecewiseModel, points, measured) -> np.ndarray:
     pred = np.asarray([model.predict(B, L) for B, L in points])
     meas = np.asarray(measured, np.float64)
@@ -167,8 +253,11 @@ class OpProfile:
     signature: OpSignature
     samples: List[Sample]
 
-    def time_model(self) -> PiecewiseModel:
-        return PiecewiseModel([(s.B, s.L) for s in self.samples], [s.us_median for s in self.samples])
+    def time_model(self):
+        pts, vals = [(s.B, s.L) for s in self.samples], [s.us_median for s in self.samples]
+        if self.signature.kind in TOKENWISE_KINDS:
+            return TokenModel(self.signature.phase, pts, vals)
+        return PiecewiseModel(pts, vals)
 
     def memory_model(self) -> PiecewiseModel:
         return PiecewiseModel([(s.B, s.L) for s in self.samples],
@@ -246,6 +335,9 @@ class Measurer:
     def __call__(self, sig: OpSignature, B: int, L_: int) -> Sample:
         desc, keep = self.build(sig, B, L_)
         p = self.L.opscale_op_profile(desc, self.warmup, self.iters, self.flush)
+        if p.us_median < 200.0 and self.iters < 40:
+            # short launches vary more from one to the next: take more of them
+            p = self.L.opscale_op_profile(desc, 0, 40, self.flush)
         del keep
         return Sample(B, L_, p.us_median, p.us_p10, p.us_p90, int(p.weight_bytes), int(p.transient_bytes),
                       int(p.io_bytes), float(p.alg_flops), float(p.alg_bytes))
@@ -353,7 +445,10 @@ def main(argv: Optional[Sequence[str]] = None) -> int:
     ap.add_argument("--kv-heads", type=int, default=8)
     ap.add_argument("--head-dim", type=int, default=128)
     ap.add_argument("--ffn", type=int, default=14336)
-    ap.add_argument("--samples", type=int, default=20, help="random samples per operator (plus the corners)")
+    ap.add_argument("--samples", type=int, default=20, help="random samples per token-wise operator (plus the "
+                                                             "ends of its token range)")
+    ap.add_argument("--samples-2d", type=int, default=96, help="random samples per attention operator (plus the "
+                                                               "domain corners)")
     ap.add_argument("--heldout", type=int, default=12)
     ap.add_argument("--max-prefill-tokens", type=int, default=65536)
     ap.add_argument("--layers", type=int, default=32, help="layers of the model (they share profiles)")
@@ -375,7 +470,7 @@ def main(argv: Optional[Sequence[str]] = None) -> int:
     pooled = []
     for key, (name, sig) in uniq.items():
         dom = domain_for(sig, a.max_prefill_tokens)
-        pts = sample_points(dom, a.samples, seed=1)
+        pts = sample_points_for(sig, dom, a.samples if sig.kind in TOKENWISE_KINDS else a.samples_2d, seed=1)
         ho_pts = [p for p in sample_points(dom, a.heldout, seed=2, with_corners=False) if p not in set(pts)]
         prof = OpProfile(sig, [meas(sig, B, L) for B, L in pts])
         store.put(prof)

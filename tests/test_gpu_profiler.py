@@ -1,12 +1,16 @@
-"""The operator profiler on the GPU: sparse profiles of a few 8B-layer
-operators over a reduced (B, L) domain, their prediction error on held-out
-points, and the memory / payload fields of the measured samples."""
+"""The operator profiler on the GPU (Section 4.2; Section 5.7, Table 2): sparse
+profiles of 8B-layer operators over the full (B, L) domain predict held-out
+points within the paper's operator-profile error (7 % mean, 15 % P90, pooled
+over held-out points), and the samples carry the memory / payload fields."""
 import numpy as np
 import pytest
 
 from parity_util import say
 
 pytestmark = pytest.mark.gpu
+
+# Section 5.7 / Table 2: operator-profile prediction error
+TABLE2_MEAN, TABLE2_P90 = 0.07, 0.15
 
 
 def test_sparse_profiles_predict_heldout_points():
@@ -18,20 +22,22 @@ def test_sparse_profiles_predict_heldout_points():
     ops.load()
     shape = LayerShape(4096, 32, 8, 128, 14336)
     sigs = dict(pr.layer_operators(shape))
-    meas = pr.Measurer(warmup=2, iters=7, flush_mib=256)
+    meas = pr.Measurer()
     pooled = []
-    for name in ("prefill.input_norm", "prefill.qkv_proj", "prefill.attention", "decode.attention"):
+    for name in ("prefill.input_norm", "prefill.qkv_proj", "prefill.down_proj", "prefill.attention",
+                 "decode.gate_up_proj", "decode.attention"):
         sig = sigs[name]
-        dom = (pr.Domain(1, 16, 16, 4096, 16384) if sig.phase == pr.PREFILL else pr.Domain(1, 128, 16, 4096, 128 * 4096))
-        pts = pr.sample_points(dom, 10, seed=1)
+        dom = pr.domain_for(sig)
+        n = 20 if sig.kind in pr.TOKENWISE_KINDS else 96
+        pts = pr.sample_points_for(sig, dom, n, seed=1)
         prof = pr.OpProfile(sig, [meas(sig, B, L) for B, L in pts])
-        ho = [meas(sig, B, L) for B, L in pr.sample_points(dom, 6, seed=2, with_corners=False) if (B, L) not in pts]
+        ho = [meas(sig, B, L) for B, L in pr.sample_points(dom, 12, seed=2, with_corners=False) if (B, L) not in pts]
         r = pr.evaluate(prof, ho)
         say(f"  {name}: {len(pts)} samples, {len(ho)} held out: mean error {100 * r['mean_rel_err']:.1f}%, "
             f"p90 {100 * r['p90_rel_err']:.1f}%")
         pooled += list(pr.relative_errors(prof.time_model(), [(h.B, h.L) for h in ho], [h.us_median for h in ho]))
         s = prof.samples[-1]
-        T = s.B * s.L if sig.phase == pr.PREFILL else s.B
+        T = pr.tokens_of(sig.phase, s.B, s.L)
         if sig.kind == "linear":
             assert s.weight_bytes == sig.p("N") * sig.p("K") * 2
             assert s.io_bytes == T * sig.p("N") * 2
@@ -39,6 +45,6 @@ def test_sparse_profiles_predict_heldout_points():
             assert s.weight_bytes == 4096 * 2 and s.io_bytes == 2 * T * 4096 * 2
         assert all(x.us_median > 0 for x in prof.samples)
     pooled = np.asarray(pooled)
-    say(f"  pooled over {pooled.size} held-out points: mean {100 * pooled.mean():.1f}%, "
-        f"p90 {100 * np.quantile(pooled, 0.9):.1f}%")
-    assert pooled.mean() < 0.3
+    mean, p90 = float(pooled.mean()), float(np.quantile(pooled, 0.9))
+    say(f"  pooled over {pooled.size} held-out points: mean {100 * mean:.1f}%, p90 {100 * p90:.1f}%")
+    assert mean <= TABLE2_MEAN and p90 <= TABLE2_P90

@@ -99,3 +99,51 @@ def test_store_json_roundtrip():
     p2 = st2.get(sig)
     assert p2.signature == sig and p2.samples == prof.samples
     assert abs(p2.time_model().predict(8, 128) - 30.0) < 1e-9
+
+
+def test_token_model_for_tokenwise_operators():
+    """Norms, linears, SiLU-mul, RoPE and the cache write are interpolated in
+    their token count: exact on a power law of the tokens, through every
+    sample, and equal at equal token counts whatever (B, L) holds them."""
+    ops = dict(pr.layer_operators(SHAPE_8B))
+    for name in ("prefill.qkv_proj", "prefill.input_norm", "decode.down_proj", "decode.kv_cache_write"):
+        sig = ops[name]
+        dom = pr.domain_for(sig)
+        pts = pr.sample_points_for(sig, dom, 20, seed=1)
+        tok = lambda B, L: pr.tokens_of(sig.phase, B, L)
+        f = lambda B, L: 2.0 * tok(B, L) ** 0.8
+        prof = pr.OpProfile(sig, [pr.Sample(B, L, f(B, L), 0, 0, 0, 0, 0, 0, 0) for B, L in pts])
+        m = prof.time_model()
+        assert isinstance(m, pr.TokenModel)
+        for B, L in pts:
+            assert abs(m.predict(B, L) / f(B, L) - 1) < 1e-9
+        for B, L in pr.sample_points(dom, 40, seed=7, with_corners=False):
+            assert abs(m.predict(B, L) / f(B, L) - 1) < 1e-9
+        if sig.phase == pr.PREFILL:
+            assert abs(m.predict(4, 1024) - m.predict(64, 64)) < 1e-9 * m.predict(64, 64)
+        else:
+            assert m.predict(17, 100) == m.predict(17, 8000)  # decode: one token per sequence
+    # attention keeps the 2-D model
+    assert isinstance(pr.OpProfile(ops["prefill.attention"], [pr.Sample(B, L, float(B * L * L), 0, 0, 0, 0, 0, 0, 0)
+                      for B, L in [(1, 16), (64, 16), (1, 8192), (8, 8192)]]).time_model(), pr.PiecewiseModel)
+
+
+def test_tokenwise_sampling_covers_the_token_range():
+    """One sample in each of n equal slices of the log token range, plus the
+    two ends; every point inside the domain and distinct in tokens."""
+    ops = dict(pr.layer_operators(SHAPE_8B))
+    for name, n in (("prefill.gate_up_proj", 20), ("decode.o_proj", 20), ("prefill.act_mul", 8)):
+        sig = ops[name]
+        dom = pr.domain_for(sig)
+        pts = pr.sample_points_for(sig, dom, n, seed=3)
+        toks = sorted(pr.tokens_of(sig.phase, B, L) for B, L in pts)
+        assert all(dom.contains(B, L) for B, L in pts) and len(set(toks)) == len(toks)
+        lo, hi = toks[0], toks[-1]
+        assert lo == (dom.b_min * dom.l_min if sig.phase == pr.PREFILL else dom.b_min)
+        assert hi == (dom.max_tokens if sig.phase == pr.PREFILL else dom.b_max)
+        # gap between neighbours in log tokens: at most two slices, plus the
+        # rounding of a count to an integer (half a token at each end)
+        slice_ = (math.log(hi) - math.log(lo)) / n
+        for a, b in zip(toks, toks[1:]):
+            assert math.log(b / a) <= 2 * slice_ + math.log((a + 0.5) / a) + math.log(b / (b - 0.5)) + 1e-9
+        assert pts == pr.sample_points_for(sig, dom, n, seed=3)
