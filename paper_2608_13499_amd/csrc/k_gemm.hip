@@ -35,9 +35,14 @@ constexpr int64_t kSplitKMaxM = 2048;  // split-K is for small M (decode batches
 
 // Tile configuration: BM x BN block tile, K in slices of BK, WGM x WGN waves
 // (each owns a (BM/WGM) x (BN/WGN) sub-tile), STAGES-deep LDS ring.
-template <int BM_, int BN_, int BK_, int WGM_, int WGN_, int STAGES_>
+// DEEP: the ring keeps STAGES - 1 slices in flight while a slice is used
+// (decode-sized M, where the loop waits on memory, not on the matrix cores);
+// otherwise the next slice is made visible one step early so its first
+// fragment reads overlap the current slice's last MFMAs.
+template <int BM_, int BN_, int BK_, int WGM_, int WGN_, int STAGES_, bool DEEP_ = false>
 struct GemmCfg {
   static constexpr int BM = BM_, BN = BN_, BK = BK_, WGM = WGM_, WGN = WGN_, STAGES = STAGES_;
+  static constexpr bool DEEP = DEEP_;
   static constexpr int WM = BM / WGM, WN = BN / WGN;  // wave tile (m x n)
   static constexpr int kThreads = WGM * WGN * 64;
   static constexpr int kWaves = WGM * WGN;
@@ -61,8 +66,8 @@ using CfgT192 = GemmCfg<192, 256, 64, 2, 4, 2>;    // 8 waves of 96x64, 2 x 56 K
 using CfgMid = GemmCfg<256, 128, 64, 2, 2, 3>;     // 4 waves of 128x64, 3 x 48 KB stages
 using CfgRow64 = GemmCfg<64, 256, 64, 1, 4, 2>;    // 4 waves of 64x64, 2 x 40 KB stages (few rows)
 // split-K tiles for decode-sized M: a K range is short, so the ring is deep
-using CfgSk64 = GemmCfg<64, 256, 64, 1, 4, 4>;     // M <= 64: 4 waves of 64x64, 4 x 40 KB stages
-using CfgSk128 = GemmCfg<128, 256, 64, 2, 4, 3>;   // M <= 128: 8 waves of 64x64, 3 x 48 KB stages
+using CfgSk64 = GemmCfg<64, 256, 64, 1, 4, 4, true>;    // M <= 64: 4 waves of 64x64, 4 x 40 KB stages
+using CfgSk128 = GemmCfg<128, 256, 64, 2, 4, 3, true>;  // M <= 256: 8 waves of 64x64, 3 x 48 KB stages
 
 
 // 16-byte chunk c of LDS row r is stored at physical chunk c ^ swz(r).
@@ -354,7 +359,34 @@ __global__ __launch_bounds__(C::kThreads, 1) void gemm_bf16_kernel(const __bf16*
     }
   };
 
-  if constexpr (S == 2) {
+  // vmcnt <= n loads of this wave (n a multiple of kLoadsPerTile, < S slices)
+  auto wait_slices = [&](int n) {
+    constexpr int L = C::kLoadsPerTile;
+    if (n <= 0) wait_vmcnt<0>();
+    else if (n == 1) wait_vmcnt<L>();
+    else if (n == 2) wait_vmcnt<(S > 2 ? 2 : 1) * L>();
+    else wait_vmcnt<(S > 3 ? 3 : 1) * L>();
+  };
+  if constexpr (C::DEEP) {
+    static_assert(S >= 3 && S <= 4, "deep ring of 3 or 4 stages");
+    // Slices kt + 1 .. kt + S - 1 are in flight while slice kt is used; the
+    // stage of slice kt - 1 is refilled right after the barrier that ends it.
+    wait_slices(min(S - 2, nk - 1));
+    __syncthreads();
+    for (int kt = 0; kt < nk; ++kt) {
+      if (kt + S - 1 < nk) load(kt + S - 1);
+      const OPS_LDS char* st = smem + (kt % S) * C::kStageBytes;
+      frags(st, 0, 0);
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks) {
+        if (ks + 1 < KS) frags(st, ks + 1, (ks + 1) & 1);
+        mfmas(ks & 1);
+      }
+      // slice kt + 1 landed: the loads issued after it may stay in flight
+      if (kt + 1 < nk) wait_slices(min(S - 2, nk - 2 - kt));
+      __syncthreads();
+    }
+  } else if constexpr (S == 2) {
     // Slice kt + 1 is made visible before the last k-step of slice kt: that
     // step already reads slice kt + 1's first fragments, and the MFMAs issued
     // just before the barrier keep the matrix cores busy while the waves
