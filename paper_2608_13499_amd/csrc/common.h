@@ -138,6 +138,19 @@ __device__ __forceinline__ void wait_vmcnt_le() {
   __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
 }
 
+// Workgroup barrier for rings filled by LDS DMA (buffer_load ... lds): this
+// wave's LDS reads are complete and the compiler moves no memory access across
+// it, but its LDS DMA loads stay in flight.  __syncthreads() would also wait
+// for those (a workgroup fence counts an LDS DMA load as an LDS write), which
+// drains a multi-stage ring at every barrier; the caller instead waits for the
+// slice it needs with wait_vmcnt_le<N>() first.
+__device__ __forceinline__ void barrier_keep_loads() {
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0); vmcnt and expcnt unconstrained
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
+
 // Block id -> tile id such that the consecutive tile ids land on one XCD.
 // Workgroups are dealt round-robin to the 8 XCDs, so block b runs on XCD
 // b % 8; giving each XCD a contiguous range of tiles keeps neighbouring tiles

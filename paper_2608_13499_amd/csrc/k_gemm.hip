@@ -372,7 +372,7 @@ __global__ __launch_bounds__(C::kThreads, 1) void gemm_bf16_kernel(const __bf16*
     // Slices kt + 1 .. kt + S - 1 are in flight while slice kt is used; the
     // stage of slice kt - 1 is refilled right after the barrier that ends it.
     wait_slices(min(S - 2, nk - 1));
-    __syncthreads();
+    barrier_keep_loads();
     for (int kt = 0; kt < nk; ++kt) {
       if (kt + S - 1 < nk) load(kt + S - 1);
       const OPS_LDS char* st = smem + (kt % S) * C::kStageBytes;
@@ -382,9 +382,9 @@ __global__ __launch_bounds__(C::kThreads, 1) void gemm_bf16_kernel(const __bf16*
         if (ks + 1 < KS) frags(st, ks + 1, (ks + 1) & 1);
         mfmas(ks & 1);
       }
-      // slice kt + 1 landed: the loads issued after it may stay in flight
+      // slice kt + 1 landed: the loads issued after it stay in flight
       if (kt + 1 < nk) wait_slices(min(S - 2, nk - 2 - kt));
-      __syncthreads();
+      barrier_keep_loads();
     }
   } else if constexpr (S == 2) {
     // Slice kt + 1 is made visible before the last k-step of slice kt: that
