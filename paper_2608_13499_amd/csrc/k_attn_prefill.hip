@@ -74,6 +74,27 @@ __device__ __forceinline__ u32x2 lds_read_tr16(const OPS_LDS char* p) {
   return __builtin_bit_cast(u32x2, v);
 }
 
+// The value lane i ^ 32 holds (v_permlane32_swap: no LDS round trip).
+__device__ __forceinline__ float other_half(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  // lanes 0-31: r[1] holds lanes 32-63; lanes 32-63: r[0] holds lanes 0-31
+  return __uint_as_float((__lane_id() < 32) ? r[1] : r[0]);
+}
+
+// 16 bytes per lane from a buffer into LDS at lds_wave_base + lane * 16
+// (buffer_load_dwordx4 ... lds, the LDS base in M0), written as assembly so
+// that the compiler does not track it.  Tracked, it makes the first V read of
+// every step wait for all loads in flight (it cannot tell that they fill the
+// other stage), so the next tile's loads would never overlap P V.  The
+// kernel orders these loads itself: wait_vmem() and a barrier before any
+// wave reads a stage they fill, and a barrier before a stage is refilled.
+__device__ __forceinline__ void lds_dma16(uint64_t base, uint32_t nrec, OPS_LDS char* lds_wave_base,
+                                          uint32_t voff) {
+  const u32x4 rs = {(uint32_t)base, (uint32_t)(base >> 32) & 0xffffu, nrec, (uint32_t)kBufferFlags};
+  const uint32_t m0v = __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)lds_wave_base);
+  asm volatile("buffer_load_dwordx4 %1, %2, 0 offen lds" : : "{m0}"(m0v), "v"(voff), "s"(rs));
+}
+
 // Prompts the work-list schedule can hold in LDS (more use the grid schedule).
 constexpr int kMaxListB = 1024;
 
@@ -128,10 +149,12 @@ __global__ __launch_bounds__(256, 2) void attn_prefill_bf16_kernel(
     // This wave's 32 query rows as MFMA B operand: chunk 2*s + fh of row q_pos.
     bf16x8 qf[DSTEPS];
     {
+      // (the record count is wave-uniform; readfirstlane keeps the
+      // descriptor in scalar registers)
       const int rows = max(0, min(32, L - q_lo));
-      const __amdgpu_buffer_rsrc_t qr = make_rsrc(
-          q + (int64_t)(seq0 + q_lo) * q_stride + (int64_t)h * D,
+      const uint32_t nrec = __builtin_amdgcn_readfirstlane(
           rows > 0 ? (uint32_t)(((int64_t)(rows - 1) * q_stride + D) * 2) : 0u);
+      const __amdgpu_buffer_rsrc_t qr = make_rsrc(q + (int64_t)(seq0 + q_lo) * q_stride + (int64_t)h * D, nrec);
 #pragma unroll
       for (int s = 0; s < DSTEPS; ++s) {
         const u32x4 w = buffer_load16(qr, (uint32_t)(((int64_t)fr * q_stride + (2 * s + fh) * 8) * 2));
@@ -147,10 +170,9 @@ __global__ __launch_bounds__(256, 2) void attn_prefill_bf16_kernel(
     // K and V tiles: LDS DMA, rows past the prompt read as zeros.
     auto load_kv = [&](int kv0, int stage) {
       const int rows = min(kBKV, L - kv0);
-      const uint32_t nrec = (uint32_t)(((int64_t)(rows - 1) * kv_stride + D) * 2);
+      const uint32_t nrec = __builtin_amdgcn_readfirstlane((uint32_t)(((int64_t)(rows - 1) * kv_stride + D) * 2));
       const int64_t off = (int64_t)(seq0 + kv0) * kv_stride + (int64_t)g * D;
-      const __amdgpu_buffer_rsrc_t kr = make_rsrc(k + off, nrec);
-      const __amdgpu_buffer_rsrc_t vr = make_rsrc(v + off, nrec);
+      const uint64_t kb = (uint64_t)(uintptr_t)(k + off), vb = (uint64_t)(uintptr_t)(v + off);
       OPS_LDS char* dk = smem + stage * S::kStage;
       OPS_LDS char* dv = dk + S::kTileBytes;
       constexpr int ROWS_PER_LOAD = 64 / CPR;  // rows covered by one 1 KB wave load
@@ -160,8 +182,8 @@ __global__ __launch_bounds__(256, 2) void attn_prefill_bf16_kernel(
         const int grp = i * 4 + wave;
         const int r = grp * ROWS_PER_LOAD + lane / CPR;
         const int pc = lane % CPR;
-        buffer_load16_lds(kr, dk + grp * 1024, (uint32_t)(((int64_t)r * kv_stride + (pc ^ k_swz<D>(r)) * 8) * 2));
-        buffer_load16_lds(vr, dv + grp * 1024, (uint32_t)(((int64_t)r * kv_stride + (pc ^ v_swz<D>(r)) * 8) * 2));
+        lds_dma16(kb, nrec, dk + grp * 1024, (uint32_t)(((int64_t)r * kv_stride + (pc ^ k_swz<D>(r)) * 8) * 2));
+        lds_dma16(vb, nrec, dv + grp * 1024, (uint32_t)(((int64_t)r * kv_stride + (pc ^ v_swz<D>(r)) * 8) * 2));
       }
     };
 
@@ -204,7 +226,7 @@ __global__ __launch_bounds__(256, 2) void attn_prefill_bf16_kernel(
       for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
         for (int e = 0; e < 16; ++e) tmax = fmaxf(tmax, st[kb][e]);
-      tmax = fmaxf(tmax, __shfl_xor(tmax, 32, 64)) * scale_log2;
+      tmax = fmaxf(tmax, other_half(tmax)) * scale_log2;
       // move the reference max only when the tile's max exceeds it by kLazy
       if (tmax > m_run + kLazy) {
         const float alpha = fast_exp2(m_run - tmax);  // 0 on the first tile
@@ -245,7 +267,7 @@ __global__ __launch_bounds__(256, 2) void attn_prefill_bf16_kernel(
 
     // normalize and store: lane owns query q_pos; acc[dt][e] is
     // d = dt*32 + (e/4)*8 + fh*4 + e%4.
-    const float l_tot = l_part + __shfl_xor(l_part, 32, 64);
+    const float l_tot = l_part + other_half(l_part);
     if (q_pos < L && q_lo < L) {
       const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
       __bf16* orow = o + ((int64_t)(seq0 + q_pos) * Hq + h) * D;
@@ -259,6 +281,7 @@ __global__ __launch_bounds__(256, 2) void attn_prefill_bf16_kernel(
           *reinterpret_cast<u32x2*>(orow + dt * 32 + gq * 8 + fh * 4) = out;
         }
     }
+    wait_vmem();      // (a stage load of a wave with no active step may still be in flight)
     __syncthreads();  // the next tile reuses the LDS stages
   };
 
