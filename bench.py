@@ -435,6 +435,11 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--calibrate-copy-mib", type=int, default=0,
                     help="run one device copy of this many MiB before the steps (counter calibration)")
+    ap.add_argument("--no-extras", action="store_true",
+                    help="time the step only (no isolated, extra-operator, configuration, peak or copy records)")
+    ap.add_argument("--config", default=None,
+                    help="time only this prefill configuration's layer, operator by operator (e.g. "
+                         "llama70b_prefill_16k, llama8b_bursty_longctx) and print its record")
     a = ap.parse_args()
     if a.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
         print(f"bench.py runs on one GPU only (asked for {a.gpus}); multi-GPU sharding is not part of "
@@ -448,6 +453,11 @@ def main():
     assert torch.cuda.is_available(), "no GPU"
     ops.load()
     torch.cuda.set_device(0)
+    if a.config is not None:
+        cfg = wl.CONFIGS[a.config]
+        log(f"config {cfg.name} ...")
+        print(json.dumps(time_prefill_config(ops, wl, torch, cfg, a.steps, a.warmup)), flush=True)
+        return
     log("building inputs ...")
     layer = Layer(ops, wl, torch, wl.C2, wl.C3)
     torch.cuda.synchronize()
@@ -492,6 +502,11 @@ def main():
     roof["traffic"] = measured_traffic(dom, kernel)
     roof["kernel"] = f"{kernel} ({dom})"
     roof["work_per_launch"] = {"flops": fl, "bytes": by}
+    if a.no_extras:
+        print(json.dumps({"metric": "per-operator prefill tokens/s + % of MFMA/HBM roofline, Llama-8B-shaped layer",
+                          "value": round(layer.p["M"] / (ms_step * 1e-3), 1), "unit": "tokens/s",
+                          "ms_per_step": round(ms_step, 4), "per_op": per_op, "roofline": roof}), flush=True)
+        return
     # Each operator of the step alone on its stream: with a 512 MiB write
     # between iterations (primary: weights and activations come from HBM, not
     # the 256 MB last-level cache) and warm, median / p10 / p90 of HIP events,
@@ -564,6 +579,37 @@ def main():
     for cfg, n in ((wl.C4, max(3, a.steps // 2)), (wl.C5, 3)):
         log(f"config {cfg.name} ...")
         configs[cfg.name] = time_prefill_config(ops, wl, torch, cfg, n, 1)
+    # The copy ceiling of the memory-bound operators: a device copy of the
+    # same bytes (read + write) from cold caches (after a 512 MiB read), the
+    # bound for an operator that streams its operands once.
+    log("copy ceiling ...")
+    flush = torch.ones(128 << 20, dtype=torch.float32, device="cuda")
+    M_, H_, F_ = layer.p["M"], layer.pc.hidden, layer.pc.ffn
+    copy_ceiling = {}
+    for nm, nbytes in (("rmsnorm", 2 * (2 * M_ * H_ + H_)), ("add_rmsnorm", 2 * (4 * M_ * H_ + H_)),
+                       ("swiglu", 3 * 2 * M_ * F_)):
+        src = torch.empty(nbytes // 2, dtype=torch.uint8, device="cuda")
+        dst = torch.empty_like(src)
+        ts = []
+        for i in range(13):
+            flush.sum()
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            dst.copy_(src)
+            e1.record()
+            torch.cuda.synchronize()
+            if i >= 2:
+                ts.append(e0.elapsed_time(e1) * 1e3)
+        ts.sort()
+        us = ts[len(ts) // 2]
+        copy_ceiling[nm] = {"bytes": nbytes, "copy_us_median": round(us, 2),
+                            "copy_gbps": round(nbytes / us * 1e-3, 1),
+                            "copy_frac_of_spec": round(nbytes / us * 1e-3 / (PEAK_HBM * 1e-9), 4)}
+        del src, dst
+    del flush
+    for nm, key in (("rmsnorm", "rmsnorm_1"), ("swiglu", "swiglu")):
+        if key in isolated:
+            copy_ceiling[nm]["op_us_flushed"] = isolated[key]["flushed"]["us_median"]
     # Peaks re-measured on this GPU (sustained clock, real data): the spec
     # peaks above stay the primary denominators.
     log("peak probes ...")
@@ -597,6 +643,7 @@ def main():
         "configs": configs,
         "isolated": isolated,
         "measured_peaks": meas,
+        "copy_ceiling": copy_ceiling,
         "gpu_state": {"before": state_before, "after": state_after},
     }
     if not a.no_cpu_baseline:

@@ -187,8 +187,10 @@ __global__ __launch_bounds__(256) void add_rmsnorm_kernel(const void* x, void* r
     const int idx = lane + i * 64;
     if (idx < nvec) {
       float a[EPV], b[EPV];
-      unpack(__builtin_nontemporal_load(xr + idx), a);
-      unpack(__builtin_nontemporal_load(rr + idx), b);
+      // plain (cached) loads and stores, as in the RMS Norm kernel (faster
+      // than the nontemporal forms on a streamed row block)
+      unpack(xr[idx], a);
+      unpack(rr[idx], b);
 #pragma unroll
       for (int e = 0; e < EPV; ++e) {
         sum[i][e] = a[e] + b[e];
@@ -205,12 +207,12 @@ __global__ __launch_bounds__(256) void add_rmsnorm_kernel(const void* x, void* r
   for (int i = 0; i < VPL; ++i) {
     const int idx = lane + i * 64;
     if (idx >= nvec) continue;
-    __builtin_nontemporal_store(pack(sum[i]), rr + idx);
+    rr[idx] = pack(sum[i]);
     float g[EPV], o[EPV];
     unpack(wr[idx], g);
 #pragma unroll
     for (int e = 0; e < EPV; ++e) o[e] = sum[i][e] * r * g[e];
-    __builtin_nontemporal_store(pack(o), yr + idx);
+    yr[idx] = pack(o);
   }
 }
 
