@@ -92,7 +92,11 @@ __device__ __forceinline__ void lds_dma16(uint64_t base, uint32_t nrec, OPS_LDS 
                                           uint32_t voff) {
   const u32x4 rs = {(uint32_t)base, (uint32_t)(base >> 32) & 0xffffu, nrec, (uint32_t)kBufferFlags};
   const uint32_t m0v = __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)lds_wave_base);
-  asm volatile("buffer_load_dwordx4 %1, %2, 0 offen lds" : : "{m0}"(m0v), "v"(voff), "s"(rs));
+  // s_nop 4: the compiler's hazard check does not see into the assembly, so
+  // the wait states it would insert come first: an LDS DMA reading M0 right
+  // after M0 is written (one), and a buffer instruction reading an SGPR of its
+  // descriptor that a VALU instruction (v_readfirstlane) wrote (five, gfx9)
+  asm volatile("s_nop 4\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds" : : "{m0}"(m0v), "v"(voff), "s"(rs));
 }
 
 // Prompts the work-list schedule can hold in LDS (more use the grid schedule).

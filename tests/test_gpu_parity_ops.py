@@ -250,6 +250,13 @@ def test_attn_prefill(ops, dtype, lens, Hq, Hkv, D, causal, packed):
     ([96, 96, 96], 4, 2, 64),                        # uniform, G = 2 (64-query tiles)
     ([900, 5, 1, 260], 3, 3, 128),                   # G = 1 (128-query tiles)
     ([1, 2, 3, 17] * 20 + [700], 8, 1, 64),          # 81 prompts: more than one wave of 64
+    # a long prompt before a short one, two equal prompts, one tile and a key:
+    # the K/V loads in these tiles must land where their stage says (a missing
+    # wait state before a load once wrote some of them to the previous load's
+    # place, in the grid schedule only)
+    ([300, 1], 4, 1, 128),
+    ([130, 130], 4, 1, 128),
+    ([65], 4, 1, 128),
 ])
 def test_attn_prefill_schedules(ops, tune, lens, Hq, Hkv, D):
     """Both schedules (grid; level-major work list) against the oracle, and
