@@ -82,8 +82,9 @@ typedef struct {
  * Returns OPSCALE_ERR_INVALID_ARG for an unknown knob or a value out of range.
  */
 typedef enum {
-  OPSCALE_TUNE_GEMM_TILE = 0,        /* bf16 linear block tile: 0 = 256x256, 1 = 192x256, 2 = 256x128
-                                        (forcing one also turns off the small-M and split-K paths) */
+  OPSCALE_TUNE_GEMM_TILE = 0,        /* bf16 linear block tile: 0 = 256x256 (four waves), 1 = 192x256,
+                                        2 = 256x128, 3 = 256x256 as eight waves (forcing one also turns
+                                        off the small-M and split-K paths) */
   OPSCALE_TUNE_GEMM_SKINNY = 1,      /* 0: never the small-M kernel; 1: wherever it is supported */
   OPSCALE_TUNE_GEMM_SPLITK = 2,      /* 0: no K split for decode-sized M */
   OPSCALE_TUNE_GEMM_TAIL = 3,        /* 0: no K split of the last partly filled round */

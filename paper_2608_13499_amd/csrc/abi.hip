@@ -45,7 +45,7 @@ opscale_status set_tuning(opscale_tune knob, int32_t value) {
   if ((unsigned)knob >= (unsigned)OPSCALE_TUNE_COUNT)
     return fail(OPSCALE_ERR_INVALID_ARG, "set_tuning: unknown knob %d", (int)knob);
   int32_t hi = 1;
-  if (knob == OPSCALE_TUNE_GEMM_TILE) hi = 2;
+  if (knob == OPSCALE_TUNE_GEMM_TILE) hi = 3;
   if (knob == OPSCALE_TUNE_SKINNY_NG) hi = 2;
   const int32_t lo = knob == OPSCALE_TUNE_SKINNY_NG ? 1 : 0;
   if (value != -1 && (value < lo || value > hi))

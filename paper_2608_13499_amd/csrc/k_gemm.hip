@@ -5,9 +5,11 @@
 // block tile is staged through an LDS ring in BK-wide K slices; the next slices
 // are fetched with buffer_load ... lds (HBM/L2 -> LDS without passing through
 // registers) while the current one feeds the matrix cores.  Large problems
-// use eight waves of 128x64 sub-tiles (two waves per SIMD, so one wave's LDS
-// reads overlap the other's MFMAs); problems with fewer than 256 such tiles
-// use a 256x128 tile of four waves, which doubles the workgroup count.  Rows
+// use four waves of 128x128 sub-tiles, one per SIMD, with the accumulators in
+// AGPRs (gemm_bf16_w4_kernel); the eight-wave form of the same tile (two waves
+// of 128x64 per SIMD) serves the grouped mixture-of-experts GEMMs.  Problems
+// whose last round of 256x256 tiles would be mostly idle take 192x256 or
+// 256x128 tiles; decode-sized M splits K.  Rows
 // and K columns beyond the matrix read as zeros through the buffer
 // descriptor's range check, so ragged M, N and K need no separate code path.
 //
@@ -21,6 +23,7 @@
 #include <cstdio>
 #include <cstdlib>
 #include <cstring>
+#include <type_traits>
 
 #include "common.h"
 #include "launch.h"
@@ -64,6 +67,7 @@ struct GemmCfg {
 using CfgBig8 = GemmCfg<256, 256, 64, 2, 4, 2>;    // 8 waves of 128x64, 2 x 64 KB stages
 using CfgT192 = GemmCfg<192, 256, 64, 2, 4, 2>;    // 8 waves of 96x64, 2 x 56 KB stages
 using CfgMid = GemmCfg<256, 128, 64, 2, 2, 3>;     // 4 waves of 128x64, 3 x 48 KB stages
+using CfgW4 = GemmCfg<256, 256, 64, 2, 2, 2>;      // 4 waves of 128x128, 2 x 64 KB stages
 using CfgRow64 = GemmCfg<64, 256, 64, 1, 4, 2>;    // 4 waves of 64x64, 2 x 40 KB stages (few rows)
 // split-K tiles for decode-sized M: a K range is short, so the ring is deep
 using CfgSk64 = GemmCfg<64, 256, 64, 1, 4, 4, true>;    // M <= 64: 4 waves of 64x64, 4 x 40 KB stages
@@ -511,6 +515,232 @@ __global__ __launch_bounds__(C::kThreads, 1) void gemm_bf16_kernel(const __bf16*
   }
 }
 
+// One MFMA 16x16x32 on an accumulator held in AGPRs.  Issued from inline
+// assembly so that the 64 accumulators of a 128x128 wave tile stay in place:
+// with the builtin the register allocator rotated them through AGPR copies and
+// spilled.  An assembly statement with side effects also fixes the order of
+// the memory instructions around it, which places the fragment reads and the
+// tile loads between the MFMAs exactly as written.
+__device__ __forceinline__ void mfma_agpr(f32x4& acc, const bf16x8& a, const bf16x8& b) {
+  asm volatile("v_mfma_f32_16x16x32_bf16 %0, %1, %2, %0" : "+a"(acc) : "v"(a), "v"(b));
+}
+
+// An accumulator's four values into VGPRs.  Read through assembly as well:
+// were the epilogue's arithmetic to read the AGPRs directly, the compiler
+// would give the accumulators VGPR homes and copy them around every MFMA.
+__device__ __forceinline__ f32x4 agpr_read(const f32x4& acc) {
+  f32x4 v;
+#pragma unroll
+  for (int e = 0; e < 4; ++e) asm volatile("v_accvgpr_read_b32 %0, %1" : "=v"(v[e]) : "a"(acc[e]));
+  return v;
+}
+
+// The 256x256 tile as four waves of 128x128, one wave per SIMD.  With two
+// waves per SIMD (gemm_bf16_kernel's eight-wave form) the older wave takes
+// the matrix core first and then waits at the slice barrier while the younger
+// one finishes alone; here every SIMD runs one wave and the slice's fragment
+// reads fall from 192 to 128 KB per workgroup.  Ring, swizzle, loads, split
+// tail and epilogue are those of gemm_bf16_kernel.  A k-step is 64 MFMAs; the
+// 16 fragment reads of the next k-step go one after each of its first 16
+// MFMAs (in the order the next k-step consumes them), and in the last k-step
+// of a slice the 16 loads of slice kt + 2 go one after every fourth MFMA.
+template <class C>
+__global__ __launch_bounds__(C::kThreads, 1) void gemm_bf16_w4_kernel(const __bf16* __restrict__ x,
+                                                                      const __bf16* __restrict__ W,
+                                                                      const __bf16* __restrict__ bias,
+                                                                      __bf16* __restrict__ y, int M, int N,
+                                                                      int K_total, int group_m, int kchunk,
+                                                                      float* __restrict__ part, GroupedGemm,
+                                                                      int dp_cnt, int tail_cnt) {
+  static_assert(C::kWaves == 4 && C::STAGES == 2 && C::WM == 128 && C::WN == 128 && !C::DEEP,
+                "four waves of 128x128 in a two-stage ring");
+  extern __shared__ __attribute__((aligned(16))) char smem_raw[];
+  OPS_LDS char* smem = (OPS_LDS char*)smem_raw;
+  constexpr int BM = C::BM, BN = C::BN, BK = C::BK, WM = C::WM, WN = C::WN;
+  constexpr int MI = 16, TM = WM / MI, TN = WN / MI, KS = BK / 32;
+
+  const int tiles_n = (N + BN - 1) / BN;
+  const int tiles_m = (M + BM - 1) / BM;
+  const int tiles = tiles_m * tiles_n;
+  const int ld = K_total;
+  int split = 0, kc = kchunk;
+  float* tile_part = nullptr;
+  uint32_t tid;
+  if (tail_cnt == 0) {
+    split = blockIdx.x / tiles;
+    tid = xcd_remap(blockIdx.x - split * tiles, (uint32_t)tiles);
+  } else if ((int)blockIdx.x < dp_cnt) {
+    tid = xcd_remap(blockIdx.x, (uint32_t)dp_cnt);
+    kc = K_total;
+  } else {
+    const int b = blockIdx.x - dp_cnt;
+    split = b / tail_cnt;
+    const int t = (int)xcd_remap(b - split * tail_cnt, (uint32_t)tail_cnt);
+    tid = dp_cnt + t;
+    tile_part = part + ((int64_t)split * tail_cnt + t) * BM * BN;
+  }
+  int tm, tn;
+  tile_coords(tid, tiles_m, tiles_n, group_m, tm, tn);
+  const int m0 = tm * BM, n0 = tn * BN;
+  const int m_rows = min(BM, M - m0);
+  const int k_begin = split * kc;
+  const int K = min(K_total - k_begin, kc);
+
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
+  const int wm = wave % C::WGM, wn = wave / C::WGM;
+  const __amdgpu_buffer_rsrc_t xr =
+      make_rsrc(x + (int64_t)m0 * ld + k_begin, (uint32_t)(((int64_t)(m_rows - 1) * ld + K) * 2));
+  const __amdgpu_buffer_rsrc_t wr =
+      make_rsrc(W + (int64_t)n0 * ld + k_begin, (uint32_t)(((int64_t)(min(BN, N - n0) - 1) * ld + K) * 2));
+  constexpr int LX = BM / C::kRowsPerLoad / C::kWaves, LW = BN / C::kRowsPerLoad / C::kWaves;
+  constexpr int L = LX + LW;
+  static_assert(L * 4 == TM * TN, "one load after every fourth MFMA of a k-step");
+  uint32_t xro[LX], wro[LW];
+#pragma unroll
+  for (int g = 0; g < LX; ++g) xro[g] = (uint32_t)(((g * C::kWaves + wave) * C::kRowsPerLoad + lane / C::kCPR) * ld * 2);
+#pragma unroll
+  for (int g = 0; g < LW; ++g) wro[g] = (uint32_t)(((g * C::kWaves + wave) * C::kRowsPerLoad + lane / C::kCPR) * ld * 2);
+
+  f32x4 acc[TN][TM];
+#pragma unroll
+  for (int i = 0; i < TN; ++i)
+#pragma unroll
+    for (int j = 0; j < TM; ++j) acc[i][j] = f32x4{};
+
+  const int nk = (K + BK - 1) / BK;
+  auto load = [&](int kt) {
+    OPS_LDS char* st = smem + (kt & 1) * C::kStageBytes;
+    load_slice<C, BM>(xr, st, xro, K, kt * BK, wave, lane);
+    load_slice<C, BN>(wr, st + BM * C::kRowBytes, wro, K, kt * BK, wave, lane);
+  };
+  const int fr = lane & (MI - 1), fh = lane / MI;
+  int lane_off[KS];
+#pragma unroll
+  for (int ks = 0; ks < KS; ++ks) lane_off[ks] = fr * C::kRowBytes + (((4 * ks + fh) ^ swz<C::kCPR>(fr)) << 4);
+  const int x_row0 = wm * WM * C::kRowBytes, w_row0 = BM * C::kRowBytes + wn * WN * C::kRowBytes;
+
+  bf16x8 a[2][TN], b[2][TM];
+  // fragment read r (0 .. TN + TM - 1) of a k-step, in the order the MFMAs
+  // (i outer, j inner) first need them: b0, a0, b1 .. b7, a1 .. a7
+  auto read_frag = [&](const OPS_LDS char* st, int ks, int buf, int r) {
+    if (r == 0) b[buf][0] = lds_frag<C>(st + x_row0 + lane_off[ks]);
+    else if (r == 1) a[buf][0] = lds_frag<C>(st + w_row0 + lane_off[ks]);
+    else if (r < TM + 1) b[buf][r - 1] = lds_frag<C>(st + x_row0 + (r - 1) * MI * C::kRowBytes + lane_off[ks]);
+    else a[buf][r - TM] = lds_frag<C>(st + w_row0 + (r - TM) * MI * C::kRowBytes + lane_off[ks]);
+  };
+  // load q (0 .. L - 1) of slice kt + 2 into stage dst (zeros past the end)
+  auto load_one = [&](OPS_LDS char* dst, int kt, int q) {
+    const int rl = lane / C::kCPR, pc = lane % C::kCPR;
+    const bool isx = q < LX;
+    const int grp = (isx ? q : q - LX) * C::kWaves + wave;
+    const int r = grp * C::kRowsPerLoad + rl;
+    const int k = (kt + 2) * BK + ((pc ^ swz<C::kCPR>(r)) << 3);
+    const uint32_t ro = isx ? xro[q < LX ? q : 0] : wro[q >= LX ? q - LX : 0];
+    const uint32_t voff = (kt + 2 < nk && k < K) ? ro + (uint32_t)k * 2u : kOobOffset;
+    buffer_load16_lds<kNoL1>(isx ? xr : wr, dst + (isx ? 0 : BM * C::kRowBytes) + grp * 1024, voff);
+  };
+  // one k-step on fragment buffer buf; READ: the next k-step's fragments
+  // (stage rd, k-step rks) into buf ^ 1; LOAD: slice kt + 2 into stage dst
+  auto kstep = [&](auto buf_c, auto read_c, auto load_c, const OPS_LDS char* rd, int rks, OPS_LDS char* dst,
+                   int kt) {
+    constexpr int buf = decltype(buf_c)::value;
+    constexpr bool READ = decltype(read_c)::value, LOAD = decltype(load_c)::value;
+    // This k-step's fragments were read one k-step ago and have landed; with
+    // the counter cleared the compiler needs no wait inside the MFMA run (it
+    // could not name one that lets the new reads stay in flight: the LDS
+    // counter holds at most 15).
+    __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0); vmcnt and expcnt unconstrained
+#pragma unroll
+    for (int q = 0; q < TN * TM; ++q) {
+      mfma_agpr(acc[q / TM][q % TM], a[buf][q / TM], b[buf][q % TM]);
+      if (READ && q < TN + TM) read_frag(rd, rks, buf ^ 1, q);
+      if (LOAD && (q & 3) == 3) load_one(dst, kt, q >> 2);
+    }
+  };
+  using B0 = std::integral_constant<int, 0>;
+  using B1 = std::integral_constant<int, 1>;
+  using T = std::true_type;
+  using F = std::false_type;
+  static_assert(KS == 2, "two k-steps per slice");
+
+  load(0);
+  wait_vmcnt<0>();
+  __syncthreads();
+  if (nk > 1) load(1);
+#pragma unroll
+  for (int r = 0; r < TN + TM; ++r) read_frag(smem, 0, 0, r);
+  // the accumulators were zeroed by VALU writes: two wait states before an
+  // MFMA reads them (the assembler statement hides them from the compiler)
+  asm volatile("s_nop 1" ::);
+  for (int kt = 0; kt < nk; ++kt) {
+    OPS_LDS char* st = smem + (kt & 1) * C::kStageBytes;
+    OPS_LDS char* st_next = smem + ((kt + 1) & 1) * C::kStageBytes;
+    // Past the last slice the loads read zeros into the stage no wave reads
+    // any more, and the last slice's look-ahead reads fetch fragments that
+    // are never used: one branch-free body keeps every accumulator in one
+    // place.
+    OPS_LDS char* dst = kt + 1 < nk ? st : st_next;
+    kstep(B0{}, T{}, F{}, st, 1, dst, kt);
+    wait_vmcnt<0>();
+    __syncthreads();
+    kstep(B1{}, T{}, T{}, st_next, 0, dst, kt);
+  }
+  // The epilogue's reads of the accumulators follow the last MFMA's writes:
+  // a 16-pass XDL write needs up to 19 wait states before another
+  // instruction reads its result.
+  asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 7" ::);
+  wait_vmem();
+
+  if (tile_part) {
+#pragma unroll
+    for (int j = 0; j < TM; ++j) {
+      const int r = wm * WM + j * MI + fr;
+#pragma unroll
+      for (int i = 0; i < TN; ++i) {
+        const int c = wn * WN + i * MI + fh * 4;
+        *reinterpret_cast<f32x4*>(tile_part + r * BN + c) = agpr_read(acc[i][j]);
+      }
+    }
+    return;
+  }
+  if (part && tail_cnt == 0) {
+    float* pbase = part + (int64_t)split * M * N;
+#pragma unroll
+    for (int j = 0; j < TM; ++j) {
+      const int m = m0 + wm * WM + j * MI + fr;
+      if (m - m0 >= m_rows) continue;
+#pragma unroll
+      for (int i = 0; i < TN; ++i) {
+        const int n = n0 + wn * WN + i * MI + fh * 4;
+        if (n >= N) continue;
+        *reinterpret_cast<f32x4*>(pbase + (int64_t)m * N + n) = agpr_read(acc[i][j]);
+      }
+    }
+    return;
+  }
+#pragma unroll
+  for (int j = 0; j < TM; ++j) {
+    const int m = m0 + wm * WM + j * MI + fr;
+    if (m - m0 >= m_rows) continue;
+    __bf16* yrow = y + (int64_t)m * N;
+#pragma unroll
+    for (int i = 0; i < TN; ++i) {
+      const int n = n0 + wn * WN + i * MI + fh * 4;
+      if (n >= N) continue;
+      const f32x4 v = agpr_read(acc[i][j]);
+      float v0 = v[0], v1 = v[1], v2 = v[2], v3 = v[3];
+      if (bias) {
+        const u32x2 bb = *reinterpret_cast<const u32x2*>(bias + n);
+        v0 += bf_lo(bb[0]);
+        v1 += bf_hi(bb[0]);
+        v2 += bf_lo(bb[1]);
+        v3 += bf_hi(bb[1]);
+      }
+      *reinterpret_cast<u32x2*>(yrow + n) = u32x2{pack_bf2(v0, v1), pack_bf2(v2, v3)};
+    }
+  }
+}
+
 // ------------------------------------------------------------ fp32 path ----
 // 64x64 output tile, 256 threads with 4x4 outputs each, K in slices of 16.
 __global__ __launch_bounds__(256) void gemm_f32_kernel(const float* __restrict__ x,
@@ -636,12 +866,19 @@ static int split_ranges(int64_t K, int splits, int BK) {
 // `part`), the other tiles as usual in the same launch.  `part` is the
 // caller's workspace, sized by plan_linear.
 template <class C>
+static constexpr auto gemm_kernel() {
+  if constexpr (std::is_same<C, CfgW4>::value) return &gemm_bf16_w4_kernel<C>;
+  else return &gemm_bf16_kernel<C, false>;
+}
+
+template <class C>
 static hipError_t launch_gemm_bf16(const void* x, const void* W, const void* bias, void* y, int64_t M,
                                    int64_t N, int64_t K, hipStream_t s, int splits, int tail_splits, float* part) {
+  constexpr auto kern = gemm_kernel<C>();
   // More than 64 KB of dynamic LDS per workgroup needs the limit raised once
   // per process (a host-side function attribute, no allocation).
   static const hipError_t attr = hipFuncSetAttribute(
-      reinterpret_cast<const void*>(gemm_bf16_kernel<C>), hipFuncAttributeMaxDynamicSharedMemorySize,
+      reinterpret_cast<const void*>(kern), hipFuncAttributeMaxDynamicSharedMemorySize,
       C::kLdsBytes);
   if (attr != hipSuccess) return attr;
   const int64_t tiles_m = (M + C::BM - 1) / C::BM;
@@ -652,7 +889,7 @@ static hipError_t launch_gemm_bf16(const void* x, const void* W, const void* bia
     const int64_t tail = tiles % kNumCUs, dp = tiles - tail;
     const int64_t kchunk = split_chunk(K, tail_splits, C::BK);
     const int nsplit = split_ranges(K, tail_splits, C::BK);
-    hipLaunchKernelGGL((gemm_bf16_kernel<C>), dim3((unsigned)(dp + tail * nsplit)), dim3(C::kThreads), C::kLdsBytes,
+    hipLaunchKernelGGL(kern, dim3((unsigned)(dp + tail * nsplit)), dim3(C::kThreads), C::kLdsBytes,
                        s, static_cast<const __bf16*>(x), static_cast<const __bf16*>(W),
                        static_cast<const __bf16*>(bias), static_cast<__bf16*>(y), (int)M, (int)N, (int)K, group_m,
                        (int)kchunk, part, GroupedGemm{}, (int)dp, (int)tail);
@@ -666,7 +903,7 @@ static hipError_t launch_gemm_bf16(const void* x, const void* W, const void* bia
   const bool split = splits > 1;
   const int64_t kchunk = split ? split_chunk(K, splits, C::BK) : K;
   const int nsplit = split ? split_ranges(K, splits, C::BK) : 1;
-  hipLaunchKernelGGL((gemm_bf16_kernel<C>), dim3((unsigned)(tiles * nsplit)), dim3(C::kThreads), C::kLdsBytes, s,
+  hipLaunchKernelGGL(kern, dim3((unsigned)(tiles * nsplit)), dim3(C::kThreads), C::kLdsBytes, s,
                      static_cast<const __bf16*>(x), static_cast<const __bf16*>(W),
                      static_cast<const __bf16*>(bias), static_cast<__bf16*>(y), (int)M, (int)N, (int)K,
                      group_m, (int)kchunk, split ? part : nullptr, GroupedGemm{}, 0, 0);
@@ -725,7 +962,7 @@ hipError_t launch_gemm_grouped(const void* x, int64_t x_rows, const void* W, int
 }
 
 // The tiled configurations a plan can name.
-enum TileCfg { kCfgBig8 = 0, kCfgT192 = 1, kCfgMid = 2, kCfgSk64 = 3, kCfgSk128 = 4 };
+enum TileCfg { kCfgBig8 = 0, kCfgT192 = 1, kCfgMid = 2, kCfgSk64 = 3, kCfgSk128 = 4, kCfgW4 = 5 };
 
 template <class C>
 static size_t split_bytes(int64_t M, int64_t N, int64_t K, int splits) {
@@ -773,7 +1010,7 @@ LinearPlan plan_linear(int64_t M, int64_t N, int64_t K, bool bf16, bool split_ok
       const int s_wide = splitk_count<CfgBig8>(M, N, K), s_mid = splitk_count<CfgMid>(M, N, K);
       const int64_t w_wide = (int64_t)s_wide * ((N + 255) / 256), w_mid = (int64_t)s_mid * ((N + 127) / 128);
       if (w_wide >= w_mid && s_wide > 1) {
-        p.cfg = kCfgBig8; p.splits = s_wide; p.ws_bytes = split_bytes<CfgBig8>(M, N, K, s_wide); return p;
+        p.cfg = kCfgW4; p.splits = s_wide; p.ws_bytes = split_bytes<CfgW4>(M, N, K, s_wide); return p;
       }
       if (s_mid > 1) { p.cfg = kCfgMid; p.splits = s_mid; p.ws_bytes = split_bytes<CfgMid>(M, N, K, s_mid); return p; }
     }
@@ -800,14 +1037,14 @@ LinearPlan plan_linear(int64_t M, int64_t N, int64_t K, bool bf16, bool split_ok
   // One workgroup per CU at a time, so a launch runs in full rounds plus a
   // last one (a split last round counts as 1 / splits of a round).  Pick the
   // tile whose rounds x tile area x relative per-element cost is smallest:
-  // 256x256 moves the fewest operand bytes per flop, 192x256 (about 15 % more
-  // per element) and 256x128 (about 30 % more) fill the last round better
-  // when 256x256 would leave it mostly idle.
+  // 256x256 moves the fewest operand bytes per flop; 192x256 (measured about
+  // 17 % more time per element) and 256x128 (about 60 % more) fill the last
+  // round better when 256x256 would leave it mostly idle.
   struct Choice { int bm, bn; double cost; };
-  static constexpr Choice choices[] = {{256, 256, 1.0}, {192, 256, 1.15}, {256, 128, 1.3}};
+  static constexpr Choice choices[] = {{256, 256, 1.0}, {192, 256, 1.17}, {256, 128, 1.6}};
   int best = 0;
-  if (force_tile >= 0 && force_tile < 3) {
-    best = force_tile;
+  if (force_tile >= 0 && force_tile <= 3) {
+    best = force_tile == 3 ? 0 : force_tile;
   } else {
     double best_t = 0;
     for (int c = 0; c < 3; ++c) {
@@ -818,11 +1055,11 @@ LinearPlan plan_linear(int64_t M, int64_t N, int64_t K, bool bf16, bool split_ok
       if (c == 0 || t < best_t) { best = c; best_t = t; }
     }
   }
-  p.cfg = best == 0 ? kCfgBig8 : best == 1 ? kCfgT192 : kCfgMid;
+  p.cfg = best == 0 ? (force_tile == 3 ? kCfgBig8 : kCfgW4) : best == 1 ? kCfgT192 : kCfgMid;
   p.tail_splits = tail_splits(((M + choices[best].bm - 1) / choices[best].bm) *
                               ((N + choices[best].bn - 1) / choices[best].bn));
   if (p.tail_splits > 1)
-    p.ws_bytes = p.cfg == kCfgBig8 ? tail_bytes<CfgBig8>(M, N, K, p.tail_splits)
+    p.ws_bytes = p.cfg == kCfgBig8 || p.cfg == kCfgW4 ? tail_bytes<CfgBig8>(M, N, K, p.tail_splits)
                  : p.cfg == kCfgT192 ? tail_bytes<CfgT192>(M, N, K, p.tail_splits)
                                      : tail_bytes<CfgMid>(M, N, K, p.tail_splits);
   return p;
@@ -837,6 +1074,7 @@ hipError_t launch_linear(const LinearPlan& p, const void* x, const void* W, cons
     case LinearPlan::kTiled:
       switch (p.cfg) {
         case kCfgBig8: return launch_gemm_bf16<CfgBig8>(x, W, bias, y, M, N, K, s, p.splits, p.tail_splits, part);
+        case kCfgW4: return launch_gemm_bf16<CfgW4>(x, W, bias, y, M, N, K, s, p.splits, p.tail_splits, part);
         case kCfgT192: return launch_gemm_bf16<CfgT192>(x, W, bias, y, M, N, K, s, p.splits, p.tail_splits, part);
         case kCfgMid: return launch_gemm_bf16<CfgMid>(x, W, bias, y, M, N, K, s, p.splits, p.tail_splits, part);
         case kCfgSk64: return launch_gemm_bf16<CfgSk64>(x, W, bias, y, M, N, K, s, p.splits, p.tail_splits, part);

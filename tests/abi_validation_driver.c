@@ -49,7 +49,7 @@ int main(void) {
   EXPECT(opscale_linear(A(1), A(2), NULL, A(3), 100, 4096, 4096, OPSCALE_BF16, A(4), need - 1, 0, NULL), WS);
   EXPECT(opscale_linear(A(1), A(2), NULL, A(3), 100, 4096, 4096, OPSCALE_BF16, A(3), need, 0, NULL), INV);
   EXPECT(opscale_set_tuning((opscale_tune)99, 0), INV);
-  EXPECT(opscale_set_tuning(OPSCALE_TUNE_GEMM_TILE, 3), INV);
+  EXPECT(opscale_set_tuning(OPSCALE_TUNE_GEMM_TILE, 4), INV);
   EXPECT(opscale_set_tuning(OPSCALE_TUNE_GEMM_SPLITK, 0), OPSCALE_OK);
   if (opscale_linear_workspace_size(100, 4096, 4096, OPSCALE_BF16) != 0) ++g_bad;
   EXPECT(opscale_set_tuning(OPSCALE_TUNE_GEMM_SPLITK, -1), OPSCALE_OK);

@@ -110,7 +110,7 @@ def test_linear_workspace(lib):
 def test_tuning_hook(lib):
     TILE, SPLITK, NG = 0, 2, 4
     assert lib.opscale_set_tuning(99, 0) == 1 and lib.opscale_get_tuning(99) == -1
-    assert lib.opscale_set_tuning(TILE, 3) == 1  # three tiles: 0, 1, 2
+    assert lib.opscale_set_tuning(TILE, 4) == 1  # four tile forms: 0 .. 3
     assert lib.opscale_set_tuning(NG, 0) == 1  # 16 or 32 columns: 1, 2
     assert lib.opscale_get_tuning(SPLITK) == -1
     try:

@@ -16,7 +16,7 @@ from parity_util import assert_close, cuda, f64, gen, say, torch_dtype
 pytestmark = pytest.mark.gpu
 
 
-TILES = {"256x256": 0, "192x256": 1, "256x128": 2}  # opscale_tune GEMM_TILE values
+TILES = {"256x256": 0, "192x256": 1, "256x128": 2, "256x256w8": 3}  # opscale_tune GEMM_TILE values
 SCHEDULES = {"grid": 0, "list": 1}                   # opscale_tune PREFILL_SCHEDULE values
 
 
@@ -76,7 +76,7 @@ def test_linear(ops, dtype, M, N, K, bias):
     assert_close(f64(y.cpu()), oracle.linear(f64(x), f64(W), None if b is None else f64(b)), dtype, "linear")
 
 
-@pytest.mark.parametrize("tile", ["256x256", "192x256", "256x128"])
+@pytest.mark.parametrize("tile", ["256x256", "192x256", "256x128", "256x256w8"])
 @pytest.mark.parametrize("M,N,K,bias", [(300, 264, 200, True), (513, 1024, 4096, False), (1, 256, 64, False),
                                         (700, 520, 136, False)])
 def test_linear_each_tile(ops, tune, tile, M, N, K, bias):
@@ -149,8 +149,30 @@ def test_linear_split_k(ops, tune, M, N, K, bias):
     assert_close(f64(y0.cpu()), ref, "bf16", "linear without a workspace")
 
 
+@pytest.mark.parametrize("M,N,K,bias", [(777, 1304, 2120, True), (2048, 6144, 4096, False), (256, 512, 64, True)])
+def test_linear_four_and_eight_waves_agree(ops, tune, M, N, K, bias):
+    """The 256x256 tile as four waves of 128x128 (accumulators in AGPRs) and
+    as eight waves of 128x64 accumulate every output over the same k-steps
+    with the same MFMA, so their results are bitwise equal; both match the
+    oracle."""
+    import torch
+    say(f"linear bf16 four vs eight waves M={M} N={N} K={K} bias={bias}")
+    x = gen(27, "x", (M, K), "bf16")
+    W = gen(27, "w_qkv", (N, K), "bf16", std=0.02)
+    b = gen(27, "bias", (N,), "bf16") if bias else None
+    args = (cuda(x), cuda(W), None if b is None else cuda(b))
+    tune(gemm_tile=TILES["256x256"])
+    y4 = ops.opscale_linear(*args)
+    tune(gemm_tile=TILES["256x256w8"])
+    y8 = ops.opscale_linear(*args)
+    torch.cuda.synchronize()
+    assert torch.equal(y4.view(torch.int16), y8.view(torch.int16))
+    assert_close(f64(y4.cpu()), oracle.linear(f64(x), f64(W), None if b is None else f64(b)), "bf16", "linear")
+
+
 @pytest.mark.parametrize("tile,M,N,K,bias", [("256x256", 4352, 4096, 1024, True), ("256x256", 4300, 4104, 2056, False),
-                                             ("192x256", 4352, 4096, 1024, False)])
+                                             ("192x256", 4352, 4096, 1024, False),
+                                             ("256x256w8", 4300, 4104, 2056, True)])
 def test_linear_split_tail(ops, tune, tile, M, N, K, bias):
     """More tiles than CUs with the last round at most half full: those tiles
     run as 2-4 K ranges (fp32 partials summed in split order) in the same
