@@ -28,7 +28,8 @@ sys.path.insert(0, ROOT)
 PEAK_BF16 = 2.5e15     # dense bf16 MFMA, FLOP/s
 PEAK_HBM = 8.0e12      # HBM3E, B/s
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_counters.json")
-KERNEL_SOURCES = {"gemm_bf16_kernel": "paper_2608_13499_amd/csrc/k_gemm.hip",
+KERNEL_SOURCES = {"gemm_bf16_w4_kernel": "paper_2608_13499_amd/csrc/k_gemm.hip",
+                  "gemm_bf16_kernel": "paper_2608_13499_amd/csrc/k_gemm.hip",
                   "rope_kernel": "paper_2608_13499_amd/csrc/k_layer_ops.hip",
                   "cache_write_kernel": "paper_2608_13499_amd/csrc/k_layer_ops.hip",
                   "add_rmsnorm_kernel": "paper_2608_13499_amd/csrc/k_layer_ops.hip",
@@ -489,7 +490,7 @@ def main():
     per_op = per_op_records(layer.names, per_op_us, work)
     dom = max(layer.names, key=lambda nm: per_op_us[nm])
     fl, by, bound, _, _ = work[dom]
-    kernel = {"mfma": "gemm_bf16_kernel", "hbm": "rmsnorm_kernel"}[bound] if "linear" in dom or "norm" in dom else \
+    kernel = {"mfma": "gemm_bf16_w4_kernel", "hbm": "rmsnorm_kernel"}[bound] if "linear" in dom or "norm" in dom else \
         {"attn_prefill": "attn_prefill_bf16_kernel", "attn_decode": "attn_decode_split_kernel",
          "swiglu": "swiglu_kernel"}[dom]
     t_dom = per_op_us[dom] * 1e-6
