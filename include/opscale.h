@@ -91,7 +91,8 @@ typedef enum {
   OPSCALE_TUNE_SKINNY_NG = 4,        /* 1 or 2: 16 or 32 output columns per small-M workgroup */
   OPSCALE_TUNE_PREFILL_SCHEDULE = 5, /* 0: one workgroup per grid cell; 1: the work list */
   OPSCALE_TUNE_MOE_FUSE = 6,         /* 0: gate-up output, then the SwiGLU kernel */
-  OPSCALE_TUNE_COUNT = 7
+  OPSCALE_TUNE_GEMM_DECODE = 7,      /* 0: never the decode-batch kernel; 1: wherever it is supported */
+  OPSCALE_TUNE_COUNT = 8
 } opscale_tune;
 opscale_status opscale_set_tuning(opscale_tune knob, int32_t value);
 /* The current value of a knob (-1: automatic, also for an unknown knob). */
@@ -126,8 +127,9 @@ size_t opscale_linear_workspace_size(int64_t M, int64_t N, int64_t K, opscale_dt
  * x: [M, K]; W: [N, K] (the nn.Linear weight layout); bias: [N] or NULL;
  * y: [M, N], must not alias x or W.  bf16: MFMA with fp32 accumulation.
  * K * sizeof(dt) and N * sizeof(dt) must be multiples of 16.
- * The bf16 path (small-M kernel, or a 256x256, 192x256 or 256x128 block tile,
- * with K split over workgroups where that fills the GPU) is chosen per shape.
+ * The bf16 path (small-M kernel, decode-batch kernel for 33-128 rows, or a
+ * 256x256, 192x256 or 256x128 block tile, with K split over workgroups where
+ * that fills the GPU) is chosen per shape.
  * workspace: NULL, or DEVICE scratch of workspace_bytes, 16-byte aligned, not
  *   overlapping x, W or y.  NULL takes a path that needs none (no K split;
  *   slower for decode-sized M and for a last round of tiles that is mostly

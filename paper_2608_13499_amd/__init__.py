@@ -21,5 +21,5 @@ from ._lib import (  # noqa: F401
     OPSCALE_OK, OPSCALE_ERR_INVALID_ARG, OPSCALE_ERR_UNSUPPORTED, OPSCALE_ERR_WORKSPACE,
     OPSCALE_ERR_HIP, OPSCALE_F32, OPSCALE_BF16,
     TUNE_AUTO, TUNE_GEMM_TILE, TUNE_GEMM_SKINNY, TUNE_GEMM_SPLITK, TUNE_GEMM_TAIL, TUNE_SKINNY_NG,
-    TUNE_PREFILL_SCHEDULE, TUNE_MOE_FUSE,
+    TUNE_PREFILL_SCHEDULE, TUNE_MOE_FUSE, TUNE_GEMM_DECODE,
 )

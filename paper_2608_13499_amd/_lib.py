@@ -19,7 +19,7 @@ OPSCALE_F32, OPSCALE_BF16 = 0, 1
 (OP_RMSNORM, OP_LINEAR, OP_SWIGLU, OP_ATTN_PREFILL, OP_ATTN_DECODE, OP_ROPE, OP_RESHAPE_AND_CACHE,
  OP_ADD_RMSNORM, OP_FUSED_MOE) = range(9)
 (TUNE_GEMM_TILE, TUNE_GEMM_SKINNY, TUNE_GEMM_SPLITK, TUNE_GEMM_TAIL, TUNE_SKINNY_NG, TUNE_PREFILL_SCHEDULE,
- TUNE_MOE_FUSE) = range(7)
+ TUNE_MOE_FUSE, TUNE_GEMM_DECODE) = range(8)
 TUNE_AUTO = -1
 
 c_i32, c_i64, c_f32, c_f64, c_vp, c_sz = (ctypes.c_int32, ctypes.c_int64, ctypes.c_float,

@@ -34,7 +34,7 @@ opscale_status hip_fail(hipError_t e, const char* what) {
 
 // The tuning overrides (opscale_set_tuning); -1 everywhere means automatic.
 namespace {
-std::atomic<int32_t> g_tuning[OPSCALE_TUNE_COUNT] = {-1, -1, -1, -1, -1, -1, -1};
+std::atomic<int32_t> g_tuning[OPSCALE_TUNE_COUNT] = {-1, -1, -1, -1, -1, -1, -1, -1};
 }  // namespace
 
 int32_t tuning(opscale_tune knob) {

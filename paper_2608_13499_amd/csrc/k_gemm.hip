@@ -909,9 +909,14 @@ static hipError_t launch_gemm_bf16(const void* x, const void* W, const void* bia
                      group_m, (int)kchunk, split ? part : nullptr, GroupedGemm{}, 0, 0);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || !split) return e;
+  return launch_splitk_reduce(part, nsplit, bias, y, M, N, s);
+}
+
+hipError_t launch_splitk_reduce(const float* part, int splits, const void* bias, void* y, int64_t M, int64_t N,
+                                hipStream_t s) {
   const int64_t MN = M * N;
   const unsigned blocks = (unsigned)std::min<int64_t>(4096, (MN / 4 + 255) / 256);
-  hipLaunchKernelGGL(splitk_reduce_kernel, dim3(blocks), dim3(256), 0, s, part, nsplit,
+  hipLaunchKernelGGL(splitk_reduce_kernel, dim3(blocks), dim3(256), 0, s, part, splits,
                      static_cast<const __bf16*>(bias), static_cast<__bf16*>(y), MN, (int)N);
   return hipGetLastError();
 }
@@ -992,6 +997,22 @@ LinearPlan plan_linear(int64_t M, int64_t N, int64_t K, bool bf16, bool split_ok
     p.path = LinearPlan::kSkinny;
     return p;
   }
+  // Decode batches of 33-128 rows with K up to 8192: the weight-streaming
+  // kernel, its K split (if any) through the workspace.  Measured cold on
+  // the 8B-layer projections it is 3-13 % faster there than the split-K tiles
+  // (QKV, O, gate-up at M = 64 and 128); at 192-256 rows and for the
+  // 14336-wide down projection the tiles below are faster.
+  const int32_t dec = tuning(OPSCALE_TUNE_GEMM_DECODE);
+  if (force_tile < 0 && dec != 0 && decode_linear_supported(M, N, K) &&
+      (dec == 1 || (M > 32 && M <= 128 && K <= 8192))) {
+    const int ds = tuning(OPSCALE_TUNE_GEMM_SPLITK) == 0 ? 1 : decode_linear_splits(M, N, K);
+    if (ds <= 1 || split_ok) {
+      p.path = LinearPlan::kDecode;
+      p.splits = ds;
+      p.ws_bytes = ds > 1 ? decode_linear_ws_bytes(M, N, K) : 0;
+      return p;
+    }
+  }
   // Otherwise decode-sized M splits K over workgroups (fp32 partials in the
   // workspace, summed in split order by a second kernel).  Tile rows follow
   // M: 64 up to 64 rows (the matrix cores work on little padding), 128 up to
@@ -1071,6 +1092,8 @@ hipError_t launch_linear(const LinearPlan& p, const void* x, const void* W, cons
   switch (p.path) {
     case LinearPlan::kSkinny:
       return launch_linear_skinny(x, W, bias, y, M, N, K, s);
+    case LinearPlan::kDecode:
+      return launch_linear_decode(x, W, bias, y, M, N, K, p.splits, ws, s);
     case LinearPlan::kTiled:
       switch (p.cfg) {
         case kCfgBig8: return launch_gemm_bf16<CfgBig8>(x, W, bias, y, M, N, K, s, p.splits, p.tail_splits, part);

@@ -24,7 +24,7 @@ hipError_t launch_swiglu(const void* gu, void* out, int64_t M, int64_t F, bool b
 // plans only paths that need no workspace.  The workspace query and the
 // launch both take it from plan_linear, so they always agree.
 struct LinearPlan {
-  enum Path { kF32 = 0, kSkinny = 1, kTiled = 2 };
+  enum Path { kF32 = 0, kSkinny = 1, kTiled = 2, kDecode = 3 };
   int path;
   int cfg;          // tiled: which block tile (k_gemm.hip)
   int splits;       // > 1: every tile split over K (partials [splits, M, N] fp32)
@@ -58,6 +58,22 @@ bool skinny_linear_supported(int64_t M, int64_t N, int64_t K);
 bool skinny_linear_preferred(int64_t M, int64_t N, int64_t K);
 hipError_t launch_linear_skinny(const void* x, const void* W, const void* bias, void* y, int64_t M, int64_t N,
                                 int64_t K, hipStream_t s);
+
+// The decode-batch bf16 linear (k_gemm_decode.hip): 128 output columns and
+// all M rows per workgroup, the weights streamed into registers, K split
+// over workgroups up to about one per CU (fp32 partials [splits, M, N] in the
+// workspace, then launch_splitk_reduce).  Supported for 1 <= M <=
+// kDecodeMaxM with K % 64 == 0.
+constexpr int64_t kDecodeMaxM = 256;
+bool decode_linear_supported(int64_t M, int64_t N, int64_t K);
+int decode_linear_splits(int64_t M, int64_t N, int64_t K);
+size_t decode_linear_ws_bytes(int64_t M, int64_t N, int64_t K);
+hipError_t launch_linear_decode(const void* x, const void* W, const void* bias, void* y, int64_t M, int64_t N,
+                                int64_t K, int splits, void* ws, hipStream_t s);
+// y[m][n] = bf16(sum over s < splits of part[s][m][n], in split order, +
+// bias[n]); N % 8 == 0.
+hipError_t launch_splitk_reduce(const float* part, int splits, const void* bias, void* y, int64_t M, int64_t N,
+                                hipStream_t s);
 
 hipError_t launch_attn_prefill(const void* q, const void* k, const void* v, int64_t q_stride,
                                int64_t kv_stride, void* o, const int32_t* cu, int32_t B,

@@ -39,5 +39,5 @@ def tune():
             ops.opscale_set_tuning(getattr(ops._lib, "TUNE_" + name.upper()), value)
 
     yield set_
-    for knob in range(ops._lib.TUNE_MOE_FUSE + 1):
+    for knob in range(ops._lib.TUNE_GEMM_DECODE + 1):
         ops.opscale_set_tuning(knob, ops._lib.TUNE_AUTO)

@@ -87,9 +87,16 @@ def test_linear_workspace(lib):
     """The split partials live in a caller workspace whose size the query
     returns; too small a workspace is rejected before anything is enqueued."""
     size = lib.opscale_linear_workspace_size
-    # 100 rows: 128-row tiles, 16 of them over N = 4096, so K = 4096 splits
-    # into min(256 / 16, 4096 / 512) = 8 ranges of fp32 [M, N] partials
+    # 100 rows: the decode-batch kernel's 128-column tiles, 32 of them over
+    # N = 4096, so K = 4096 (8 rounds of 8 slices) splits into
+    # min(256 / 32, 8) = 8 ranges of fp32 [M, N] partials
     assert size(100, 4096, 4096, 1) == 8 * 100 * 4096 * 4
+    # 128 rows: QKV's 48 tiles -> min(5, 8) = 5 ranges rounded to whole
+    # rounds: 2 rounds each, 4 ranges; gate-up's 224 tiles fill the GPU unsplit
+    assert size(128, 6144, 4096, 1) == 4 * 128 * 6144 * 4
+    assert size(128, 28672, 4096, 1) == 0
+    # 256 rows: the split-K tiles (128 x 256, 2 x 16 over N = 4096): 8 ranges
+    assert size(256, 4096, 4096, 1) == 8 * 256 * 4096 * 4
     # the 8871-token gate-up projection: 35 x 112 tiles of 256 x 256 leave a
     # last round of 80 tiles, split into min(4, 256 // 80, 4096 // 512) = 3
     # K ranges of compact fp32 tiles

@@ -131,7 +131,7 @@ def test_linear_split_k(ops, tune, M, N, K, bias):
     its contents on entry must not matter); without one the same shapes take
     an unsplit path."""
     import torch
-    tune(gemm_skinny=0)
+    tune(gemm_skinny=0, gemm_decode=0)
     say(f"linear bf16 split-K M={M} N={N} K={K} bias={bias}")
     x = gen(25, "x", (M, K), "bf16")
     W = gen(25, "w_qkv", (N, K), "bf16", std=0.02)
@@ -139,6 +139,40 @@ def test_linear_split_k(ops, tune, M, N, K, bias):
     args = (cuda(x), cuda(W), None if b is None else cuda(b))
     need = ops.opscale_linear_workspace_size(M, N, K)
     ws = torch.full((max(need, 16),), 0x7f, dtype=torch.uint8, device="cuda")  # fp32 3.4e38 if read
+    y = ops.opscale_linear(*args, workspace=ws)
+    y2 = ops.opscale_linear(*args, workspace=ws)
+    y0 = ops.opscale_linear(*args, workspace=False)
+    torch.cuda.synchronize()
+    assert torch.equal(y, y2)
+    ref = oracle.linear(f64(x), f64(W), None if b is None else f64(b))
+    assert_close(f64(y.cpu()), ref, "bf16", "linear")
+    assert_close(f64(y0.cpu()), ref, "bf16", "linear without a workspace")
+
+
+@pytest.mark.parametrize("M,N,K,bias", [
+    (256, 6144, 4096, False), (256, 4096, 4096, True), (256, 4096, 14336, False), (256, 28672, 4096, False),
+    (200, 1000, 2048, True), (129, 264, 256, False), (100, 520, 1088, True), (65, 136, 64, True),
+    (33, 8, 512, False), (1, 256, 64, False), (64, 6144, 4096, True), (256, 4104, 576, True),
+    (256, 256, 16384, False), (128, 1304, 832, False),
+])
+def test_linear_decode_batch(ops, tune, M, N, K, bias):
+    """The decode-batch kernel (weights streamed into registers, 128 columns
+    and all M rows per workgroup), forced on: every row-block count (M up to
+    64, 128, 256 and ragged between), N tails down to 8 columns and waves
+    with no weight rows, K of one slice, ranges that are not a multiple of the
+    8-slice round and uneven K ranges, K split over workgroups through the
+    caller's workspace (poisoned: its contents on entry must not matter) or
+    not at all; bitwise equal across calls.  Without a workspace a shape that
+    would split takes another path."""
+    import torch
+    tune(gemm_decode=1)
+    say(f"linear bf16 decode-batch M={M} N={N} K={K} bias={bias}")
+    x = gen(28, "x", (M, K), "bf16")
+    W = gen(28, "w_qkv", (N, K), "bf16", std=0.02)
+    b = gen(28, "bias", (N,), "bf16") if bias else None
+    args = (cuda(x), cuda(W), None if b is None else cuda(b))
+    need = ops.opscale_linear_workspace_size(M, N, K)
+    ws = torch.full((max(need, 16),), 0x7f, dtype=torch.uint8, device="cuda")
     y = ops.opscale_linear(*args, workspace=ws)
     y2 = ops.opscale_linear(*args, workspace=ws)
     y0 = ops.opscale_linear(*args, workspace=False)
