@@ -61,21 +61,12 @@ __device__ __forceinline__ void mfma32(f32x16& acc, const bf16x8& a, const bf16x
 }
 __device__ __forceinline__ void sched_fence() { __builtin_amdgcn_sched_barrier(0); }
 
-// s_waitcnt vmcnt(<= n) for n known only at run time among a few values:
-// the loads this wave issued after the one waited for.
-template <int A, int B, int C>
-__device__ __forceinline__ void wait_vm_3(int sel) {
-  if (sel == 0) wait_vmcnt_le<A>();
-  else if (sel == 1) wait_vmcnt_le<B>();
-  else wait_vmcnt_le<C>();
-}
-
 }  // namespace
 
 // MB: 32-row blocks of x (M <= 32 * MB).  Grid: tiles_n x nsplit workgroups.
-template <int MB>
 // x and W are deliberately not __restrict__: with it the compiler treats
 // their loads as invariant and moves them across the fences below.
+template <int MB>
 __global__ __launch_bounds__(256, 1) void gemm_decode_bf16_kernel(const __bf16* x, const __bf16* W,
                                                                   const __bf16* __restrict__ bias,
                                                                   __bf16* __restrict__ y, int M, int N, int K,
