@@ -539,12 +539,20 @@ __device__ __forceinline__ f32x4 agpr_read(const f32x4& acc) {
 // waves per SIMD (gemm_bf16_kernel's eight-wave form) the older wave takes
 // the matrix core first and then waits at the slice barrier while the younger
 // one finishes alone; here every SIMD runs one wave and the slice's fragment
-// reads fall from 192 to 128 KB per workgroup.  Ring, swizzle, loads, split
-// tail and epilogue are those of gemm_bf16_kernel.  A k-step is 64 MFMAs; the
-// 16 fragment reads of the next k-step go one after each of its first 16
-// MFMAs (in the order the next k-step consumes them), and in the last k-step
-// of a slice the 16 loads of slice kt + 2 go one after every fourth MFMA.
-template <class C>
+// reads fall from 192 to 128 KB per workgroup.  Swizzle, loads, split tail
+// and epilogue are those of gemm_bf16_kernel.  A k-step is 64 MFMAs; the 16
+// fragment reads of the next k-step go one after each of its first 16 MFMAs
+// (in the order the next k-step consumes them), and in the last k-step of a
+// slice 16 loads go one after every fourth MFMA.
+//
+// The LDS ring is five 32 KB half-slices (160 KB) rather than two 64 KB
+// slices: the x half and the W half of a slice rotate through the buffers
+// separately, so once slice kt is read its buffers take the W half of slice
+// kt + 2 and the x half of slice kt + 3.  About 1.5 slices (96 KB) are in
+// flight per CU instead of at most one, and the x halves get two slices of
+// time to land.  The loads are latency bound: the tile-load pattern alone
+// moves 18 TB/s over the chip this way against 13.7 TB/s with two stages.
+template <class C, bool XLEAD>
 __global__ __launch_bounds__(C::kThreads, 1) void gemm_bf16_w4_kernel(const __bf16* __restrict__ x,
                                                                       const __bf16* __restrict__ W,
                                                                       const __bf16* __restrict__ bias,
@@ -552,8 +560,7 @@ __global__ __launch_bounds__(C::kThreads, 1) void gemm_bf16_w4_kernel(const __bf
                                                                       int K_total, int group_m, int kchunk,
                                                                       float* __restrict__ part, GroupedGemm,
                                                                       int dp_cnt, int tail_cnt) {
-  static_assert(C::kWaves == 4 && C::STAGES == 2 && C::WM == 128 && C::WN == 128 && !C::DEEP,
-                "four waves of 128x128 in a two-stage ring");
+  static_assert(C::kWaves == 4 && C::WM == 128 && C::WN == 128 && !C::DEEP, "four waves of 128x128");
   extern __shared__ __attribute__((aligned(16))) char smem_raw[];
   OPS_LDS char* smem = (OPS_LDS char*)smem_raw;
   constexpr int BM = C::BM, BN = C::BN, BK = C::BK, WM = C::WM, WN = C::WN;
@@ -608,41 +615,48 @@ __global__ __launch_bounds__(C::kThreads, 1) void gemm_bf16_w4_kernel(const __bf
     for (int j = 0; j < TM; ++j) acc[i][j] = f32x4{};
 
   const int nk = (K + BK - 1) / BK;
-  auto load = [&](int kt) {
-    OPS_LDS char* st = smem + (kt & 1) * C::kStageBytes;
-    load_slice<C, BM>(xr, st, xro, K, kt * BK, wave, lane);
-    load_slice<C, BN>(wr, st + BM * C::kRowBytes, wro, K, kt * BK, wave, lane);
+  // The ring holds five half-slices of HB bytes: the lead operand's rows of
+  // slice s (x if XLEAD, else W) are half 2s, the other operand's half 2s + 1,
+  // and half u lives in buffer u mod 5.
+  constexpr int HB = BM * C::kRowBytes;
+  // load g (0 .. 7) of the x (ISX) or W half of slice s into buffer dst
+  // (zeros past the end)
+  auto load_half = [&](auto isx_c, OPS_LDS char* dst, int s, int g) {
+    constexpr bool ISX = decltype(isx_c)::value;
+    const int rl = lane / C::kCPR, pc = lane % C::kCPR;
+    const int grp = g * C::kWaves + wave;
+    const int r = grp * C::kRowsPerLoad + rl;
+    // (a slice past the end starts at K, so every lane's k is out of range:
+    // one select per load and no branch)
+    const int k = (s < nk ? s * BK : K) + ((pc ^ swz<C::kCPR>(r)) << 3);
+    const uint32_t voff = k < K ? (ISX ? xro[g] : wro[g]) + (uint32_t)k * 2u : kOobOffset;
+    buffer_load16_lds<kNoL1>(ISX ? xr : wr, dst + grp * 1024, voff);
   };
+  using TL = std::integral_constant<bool, XLEAD>;   // the lead operand (true: x)
+  using TF = std::integral_constant<bool, !XLEAD>;  // the other one
   const int fr = lane & (MI - 1), fh = lane / MI;
   int lane_off[KS];
 #pragma unroll
   for (int ks = 0; ks < KS; ++ks) lane_off[ks] = fr * C::kRowBytes + (((4 * ks + fh) ^ swz<C::kCPR>(fr)) << 4);
-  const int x_row0 = wm * WM * C::kRowBytes, w_row0 = BM * C::kRowBytes + wn * WN * C::kRowBytes;
+  const int x_row0 = wm * WM * C::kRowBytes, w_row0 = wn * WN * C::kRowBytes;
 
   bf16x8 a[2][TN], b[2][TM];
-  // fragment read r (0 .. TN + TM - 1) of a k-step, in the order the MFMAs
-  // (i outer, j inner) first need them: b0, a0, b1 .. b7, a1 .. a7
-  auto read_frag = [&](const OPS_LDS char* st, int ks, int buf, int r) {
-    if (r == 0) b[buf][0] = lds_frag<C>(st + x_row0 + lane_off[ks]);
-    else if (r == 1) a[buf][0] = lds_frag<C>(st + w_row0 + lane_off[ks]);
-    else if (r < TM + 1) b[buf][r - 1] = lds_frag<C>(st + x_row0 + (r - 1) * MI * C::kRowBytes + lane_off[ks]);
-    else a[buf][r - TM] = lds_frag<C>(st + w_row0 + (r - TM) * MI * C::kRowBytes + lane_off[ks]);
-  };
-  // load q (0 .. L - 1) of slice kt + 2 into stage dst (zeros past the end)
-  auto load_one = [&](OPS_LDS char* dst, int kt, int q) {
-    const int rl = lane / C::kCPR, pc = lane % C::kCPR;
-    const bool isx = q < LX;
-    const int grp = (isx ? q : q - LX) * C::kWaves + wave;
-    const int r = grp * C::kRowsPerLoad + rl;
-    const int k = (kt + 2) * BK + ((pc ^ swz<C::kCPR>(r)) << 3);
-    const uint32_t ro = isx ? xro[q < LX ? q : 0] : wro[q >= LX ? q - LX : 0];
-    const uint32_t voff = (kt + 2 < nk && k < K) ? ro + (uint32_t)k * 2u : kOobOffset;
-    buffer_load16_lds<kNoL1>(isx ? xr : wr, dst + (isx ? 0 : BM * C::kRowBytes) + grp * 1024, voff);
+  // fragment read r (0 .. TN + TM - 1) of a k-step from the x half rx and the
+  // W half rw, in the order the MFMAs (i outer, j inner) first need them:
+  // b0, a0, b1 .. b7, a1 .. a7
+  auto read_frag = [&](const OPS_LDS char* rx, const OPS_LDS char* rw, int ks, int buf, int r) {
+    if (r == 0) b[buf][0] = lds_frag<C>(rx + x_row0 + lane_off[ks]);
+    else if (r == 1) a[buf][0] = lds_frag<C>(rw + w_row0 + lane_off[ks]);
+    else if (r < TM + 1) b[buf][r - 1] = lds_frag<C>(rx + x_row0 + (r - 1) * MI * C::kRowBytes + lane_off[ks]);
+    else a[buf][r - TM] = lds_frag<C>(rw + w_row0 + (r - TM) * MI * C::kRowBytes + lane_off[ks]);
   };
   // one k-step on fragment buffer buf; READ: the next k-step's fragments
-  // (stage rd, k-step rks) into buf ^ 1; LOAD: slice kt + 2 into stage dst
-  auto kstep = [&](auto buf_c, auto read_c, auto load_c, const OPS_LDS char* rd, int rks, OPS_LDS char* dst,
-                   int kt) {
+  // (halves rx / rw, k-step rks) into buf ^ 1; LOAD: the other operand's half
+  // of slice kt + 2 into df, then the lead operand's half of slice kt + 3
+  // into dl (in this order: the next barrier waits for the first and leaves
+  // the second in flight)
+  auto kstep = [&](auto buf_c, auto read_c, auto load_c, const OPS_LDS char* rx, const OPS_LDS char* rw, int rks,
+                   OPS_LDS char* df, OPS_LDS char* dl, int kt) {
     constexpr int buf = decltype(buf_c)::value;
     constexpr bool READ = decltype(read_c)::value, LOAD = decltype(load_c)::value;
     // This k-step's fragments were read one k-step ago and have landed; with
@@ -653,8 +667,12 @@ __global__ __launch_bounds__(C::kThreads, 1) void gemm_bf16_w4_kernel(const __bf
 #pragma unroll
     for (int q = 0; q < TN * TM; ++q) {
       mfma_agpr(acc[q / TM][q % TM], a[buf][q / TM], b[buf][q % TM]);
-      if (READ && q < TN + TM) read_frag(rd, rks, buf ^ 1, q);
-      if (LOAD && (q & 3) == 3) load_one(dst, kt, q >> 2);
+      if (READ && q < TN + TM) read_frag(rx, rw, rks, buf ^ 1, q);
+      if (LOAD && (q & 3) == 3) {
+        const int l = q >> 2;
+        if (l < LW) load_half(TF{}, df, kt + 2, l);
+        else load_half(TL{}, dl, kt + 3, l - LW);
+      }
     }
   };
   using B0 = std::integral_constant<int, 0>;
@@ -662,28 +680,47 @@ __global__ __launch_bounds__(C::kThreads, 1) void gemm_bf16_w4_kernel(const __bf
   using T = std::true_type;
   using F = std::false_type;
   static_assert(KS == 2, "two k-steps per slice");
+  static_assert(BM == BN && LX == 8 && LW == 8, "square tile: x and W halves of 8 loads per wave");
 
-  load(0);
-  wait_vmcnt<0>();
-  __syncthreads();
-  if (nk > 1) load(1);
+  // prologue: halves 0 .. 4 (slices 0 and 1, the lead half of slice 2)
 #pragma unroll
-  for (int r = 0; r < TN + TM; ++r) read_frag(smem, 0, 0, r);
+  for (int g = 0; g < LX; ++g) load_half(TL{}, smem, 0, g);
+#pragma unroll
+  for (int g = 0; g < LW; ++g) load_half(TF{}, smem + HB, 0, g);
+#pragma unroll
+  for (int g = 0; g < LX; ++g) load_half(TL{}, smem + 2 * HB, 1, g);
+#pragma unroll
+  for (int g = 0; g < LW; ++g) load_half(TF{}, smem + 3 * HB, 1, g);
+#pragma unroll
+  for (int g = 0; g < LX; ++g) load_half(TL{}, smem + 4 * HB, 2, g);
+  wait_vmcnt<3 * LX>();  // slice 0 has landed (three halves still in flight)
+  barrier_keep_loads();
+#pragma unroll
+  for (int r = 0; r < TN + TM; ++r) read_frag(XLEAD ? smem : smem + HB, XLEAD ? smem + HB : smem, 0, 0, r);
   // the accumulators were zeroed by VALU writes: two wait states before an
   // MFMA reads them (the assembler statement hides them from the compiler)
   asm volatile("s_nop 1" ::);
+  int li = 0, fi = 1;  // buffers of slice kt's lead and other halves
   for (int kt = 0; kt < nk; ++kt) {
-    OPS_LDS char* st = smem + (kt & 1) * C::kStageBytes;
-    OPS_LDS char* st_next = smem + ((kt + 1) & 1) * C::kStageBytes;
-    // Past the last slice the loads read zeros into the stage no wave reads
+    const int ln = li + 2 < 5 ? li + 2 : li - 3, fn = fi + 2 < 5 ? fi + 2 : fi - 3;  // slice kt + 1
+    OPS_LDS char* sl = smem + li * HB;
+    OPS_LDS char* sf = smem + fi * HB;
+    // Past the last slice the loads read zeros into buffers no wave reads
     // any more, and the last slice's look-ahead reads fetch fragments that
     // are never used: one branch-free body keeps every accumulator in one
     // place.
-    OPS_LDS char* dst = kt + 1 < nk ? st : st_next;
-    kstep(B0{}, T{}, F{}, st, 1, dst, kt);
-    wait_vmcnt<0>();
-    __syncthreads();
-    kstep(B1{}, T{}, T{}, st_next, 0, dst, kt);
+    kstep(B0{}, T{}, F{}, XLEAD ? sl : sf, XLEAD ? sf : sl, 1, sl, sf, kt);
+    // slice kt + 1 has landed in every wave (only the lead half of slice
+    // kt + 2 stays in flight) and every wave is done reading slice kt, whose
+    // buffers take the other half of slice kt + 2 (half 2kt + 5) and the lead
+    // half of slice kt + 3 (half 2kt + 6)
+    wait_vmcnt<LX>();
+    barrier_keep_loads();
+    OPS_LDS char* nl = smem + ln * HB;
+    OPS_LDS char* nf = smem + fn * HB;
+    kstep(B1{}, T{}, T{}, XLEAD ? nl : nf, XLEAD ? nf : nl, 0, sl, sf, kt);
+    li = ln;
+    fi = fn;
   }
   // The epilogue's reads of the accumulators follow the last MFMA's writes:
   // a 16-pass XDL write needs up to 19 wait states before another
@@ -870,31 +907,49 @@ static int split_ranges(int64_t K, int splits, int BK) {
 // the last, partly filled round run split (compact fp32 partial tiles in
 // `part`), the other tiles as usual in the same launch.  `part` is the
 // caller's workspace, sized by plan_linear.
-template <class C>
+template <class C, bool XLEAD>
 static constexpr auto gemm_kernel() {
-  if constexpr (std::is_same<C, CfgW4>::value) return &gemm_bf16_w4_kernel<C>;
+  if constexpr (std::is_same<C, CfgW4>::value) return &gemm_bf16_w4_kernel<C, XLEAD>;
   else return &gemm_bf16_kernel<C, false>;
+}
+
+// Dynamic LDS of a launch: the four-wave kernel's ring is five half-slices
+// (x or W rows of one slice each), the others STAGES whole slices.
+template <class C>
+static constexpr int gemm_lds_bytes() {
+  if constexpr (std::is_same<C, CfgW4>::value) return 5 * C::BM * C::kRowBytes;
+  else return C::kLdsBytes;
 }
 
 template <class C>
 static hipError_t launch_gemm_bf16(const void* x, const void* W, const void* bias, void* y, int64_t M,
                                    int64_t N, int64_t K, hipStream_t s, int splits, int tail_splits, float* part) {
-  constexpr auto kern = gemm_kernel<C>();
   // More than 64 KB of dynamic LDS per workgroup needs the limit raised once
   // per process (a host-side function attribute, no allocation).
-  static const hipError_t attr = hipFuncSetAttribute(
-      reinterpret_cast<const void*>(kern), hipFuncAttributeMaxDynamicSharedMemorySize,
-      C::kLdsBytes);
+  static const hipError_t attr = [] {
+    const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(gemm_kernel<C, true>()),
+                                             hipFuncAttributeMaxDynamicSharedMemorySize, gemm_lds_bytes<C>());
+    if (e != hipSuccess) return e;
+    return hipFuncSetAttribute(reinterpret_cast<const void*>(gemm_kernel<C, false>()),
+                               hipFuncAttributeMaxDynamicSharedMemorySize, gemm_lds_bytes<C>());
+  }();
   if (attr != hipSuccess) return attr;
   const int64_t tiles_m = (M + C::BM - 1) / C::BM;
   const int64_t tiles_n = (N + C::BN - 1) / C::BN;
   const int64_t tiles = tiles_m * tiles_n;
   const int group_m = tile_group_rows<C>(tiles_m, tiles_n, K);
+  // The four-wave kernel's ring gives two slices of lead to one operand: the
+  // one with fewer distinct blocks among the 32 tiles an XCD runs at once (x
+  // when a group spans at most 4 tile-rows, i.e. K >= 8192; W for the 8-row
+  // groups of K = 4096).  Same-box, flushed: the 8B gate-up 1579 -> 1526 us
+  // with W leading, down 769 -> 752 us and the 70B gate-up and down 3-4 %
+  // faster with x leading.
+  const auto kern = group_m <= 4 ? gemm_kernel<C, true>() : gemm_kernel<C, false>();
   if (tail_splits > 1) {
     const int64_t tail = tiles % kNumCUs, dp = tiles - tail;
     const int64_t kchunk = split_chunk(K, tail_splits, C::BK);
     const int nsplit = split_ranges(K, tail_splits, C::BK);
-    hipLaunchKernelGGL(kern, dim3((unsigned)(dp + tail * nsplit)), dim3(C::kThreads), C::kLdsBytes,
+    hipLaunchKernelGGL(kern, dim3((unsigned)(dp + tail * nsplit)), dim3(C::kThreads), gemm_lds_bytes<C>(),
                        s, static_cast<const __bf16*>(x), static_cast<const __bf16*>(W),
                        static_cast<const __bf16*>(bias), static_cast<__bf16*>(y), (int)M, (int)N, (int)K, group_m,
                        (int)kchunk, part, GroupedGemm{}, (int)dp, (int)tail);
@@ -908,7 +963,7 @@ static hipError_t launch_gemm_bf16(const void* x, const void* W, const void* bia
   const bool split = splits > 1;
   const int64_t kchunk = split ? split_chunk(K, splits, C::BK) : K;
   const int nsplit = split ? split_ranges(K, splits, C::BK) : 1;
-  hipLaunchKernelGGL(kern, dim3((unsigned)(tiles * nsplit)), dim3(C::kThreads), C::kLdsBytes, s,
+  hipLaunchKernelGGL(kern, dim3((unsigned)(tiles * nsplit)), dim3(C::kThreads), gemm_lds_bytes<C>(), s,
                      static_cast<const __bf16*>(x), static_cast<const __bf16*>(W),
                      static_cast<const __bf16*>(bias), static_cast<__bf16*>(y), (int)M, (int)N, (int)K,
                      group_m, (int)kchunk, split ? part : nullptr, GroupedGemm{}, 0, 0);
