@@ -508,10 +508,10 @@ def main():
                           "value": round(layer.p["M"] / (ms_step * 1e-3), 1), "unit": "tokens/s",
                           "ms_per_step": round(ms_step, 4), "per_op": per_op, "roofline": roof}), flush=True)
         return
-    # Each operator of the step alone on its stream: with a 512 MiB write
-    # between iterations (primary: weights and activations come from HBM, not
-    # the 256 MB last-level cache) and warm, median / p10 / p90 of HIP events,
-    # with the clocks before and after.
+    # Each operator of the step alone on its stream: with a read of a 512 MiB
+    # buffer between iterations (primary: weights and activations come from
+    # HBM, not the 256 MB last-level cache) and warm, median / p10 / p90 of HIP
+    # events, with the clocks before and after.
     flush = torch.empty(512 << 20, dtype=torch.uint8, device="cuda")
     iso_iters = max(20, a.steps)
     isolated = {}

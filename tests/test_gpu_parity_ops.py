@@ -188,7 +188,9 @@ def test_linear_four_and_eight_waves_agree(ops, tune, M, N, K, bias):
     """The 256x256 tile as four waves of 128x128 (accumulators in AGPRs) and
     as eight waves of 128x64 accumulate every output over the same k-steps
     with the same MFMA, so their results are bitwise equal; both match the
-    oracle."""
+    oracle.  The four-wave ring gives the two-slice lead to x on the first
+    shape (tile groups of at most four tile-rows) and to W on the second
+    (eight-row groups at K = 4096)."""
     import torch
     say(f"linear bf16 four vs eight waves M={M} N={N} K={K} bias={bias}")
     x = gen(27, "x", (M, K), "bf16")
