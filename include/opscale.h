@@ -468,8 +468,11 @@ opscale_status opscale_fused_moe(const void* x, const void* w1, const void* w2, 
  * XCD n % num_xcds, 0 when it is CU n % (num_cus / num_xcds) of XCD
  * n / (num_cus / num_xcds).  The mapping is measured once per device, at the
  * first call, by running opscale_cu_probe on a stream masked to the first
- * num_cus / num_xcds bits (blocking).  OPSCALE_ERR_UNSUPPORTED if the probe
- * matches neither mapping.
+ * num_cus / num_xcds bits (blocking).  That first call is set-up, not an
+ * operator call: it allocates and frees an 8-byte-per-workgroup result buffer
+ * for the probe and creates and destroys the masked stream; later calls touch
+ * the device not at all.  OPSCALE_ERR_UNSUPPORTED if the probe matches neither
+ * mapping.
  */
 opscale_status opscale_cu_layout(int32_t* num_cus, int32_t* num_xcds, int32_t* interleaved);
 
