@@ -183,14 +183,17 @@ def test_linear_decode_batch(ops, tune, M, N, K, bias):
     assert_close(f64(y0.cpu()), ref, "bf16", "linear without a workspace")
 
 
-@pytest.mark.parametrize("M,N,K,bias", [(777, 1304, 2120, True), (2048, 6144, 4096, False), (256, 512, 64, True)])
+@pytest.mark.parametrize("M,N,K,bias", [(777, 1304, 2120, True), (2048, 6144, 4096, False), (256, 512, 64, True),
+                                        (1300, 1000, 2056, True), (520, 384, 8256, False)])
 def test_linear_four_and_eight_waves_agree(ops, tune, M, N, K, bias):
     """The 256x256 tile as four waves of 128x128 (accumulators in AGPRs) and
     as eight waves of 128x64 accumulate every output over the same k-steps
     with the same MFMA, so their results are bitwise equal; both match the
-    oracle.  The four-wave ring gives the two-slice lead to x on the first
-    shape (tile groups of at most four tile-rows) and to W on the second
-    (eight-row groups at K = 4096)."""
+    oracle.  The four-wave ring gives the two-slice lead to x on the first,
+    third and fifth shapes (tile groups of at most four tile-rows) and to W
+    on the second and fourth (groups of more rows); the ragged K of the first
+    and fourth ends in a partial slice, the fifth runs 129 slices and the
+    third a single one."""
     import torch
     say(f"linear bf16 four vs eight waves M={M} N={N} K={K} bias={bias}")
     x = gen(27, "x", (M, K), "bf16")
